@@ -1,0 +1,174 @@
+"""Seeded synthetic workloads for the compressed MoE layer.
+
+Every stream is drawn from ``numpy.random.SeedSequence(MASTER_SEED,
+spawn_key=key)`` with a key that names what is drawn (workload, layer, expert,
+projection), so any single tensor can be regenerated on its own.
+
+Workloads (shapes follow DeepSeek-V3: hidden 7168, expert intermediate 2048,
+256 routed experts in 8 groups, 4 groups and 8 experts per token, routed
+scaling 2.5; 192 kept experts is the paper's retention ratio r = 0.75):
+
+* ``tiny``        hidden 512, intermediate 256, 16 experts with 12 kept,
+                  1 shared, 2 groups / 1 group / top-2, 8 tokens, all 4-bit;
+* ``v3_decode``   V3 shape, 192 of 256 kept, 1 shared; routed gate/up 3-bit,
+                  routed down 4-bit, shared 4-bit; 1 and 16 tokens;
+* ``v3_prefill``  V3 shape, 2048 tokens, Zipf(1.1)-skewed routing, every
+                  tensor's width drawn from {2, 3, 4} with p = (0.6, 0.2, 0.2);
+* ``v3_stack``    58 independent V3-shape layers, widths from {2, 3, 4} with
+                  p = (0.7, 0.1, 0.2), batch 1, independent inputs per layer;
+* ``v3_sweep``    kept in {256, 192, 128} x widths {uniform 2, uniform 4,
+                  mixed} x batch {1, 16, 64} x routing {normal, Zipf}.
+
+Value distributions: weights N(0, 0.02) (then quantized by whoever consumes
+them), activations N(0, 1) rounded to bfloat16, router logits N(0, 1) in
+float32, or ``log p + Gumbel(0, 1)`` with ``p`` a Zipf(1.1) law over a seeded
+permutation of the kept experts.
+"""
+import dataclasses
+import zlib
+
+import numpy as np
+
+MASTER_SEED = 20250930
+PROJ_GATE, PROJ_UP, PROJ_DOWN = 0, 1, 2
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerShape:
+    hidden: int
+    inter: int
+    n_experts: int
+    n_kept: int
+    n_shared: int
+    n_group: int
+    topk_group: int
+    top_k: int
+    group_topn: int = 2
+    norm_topk: int = 1
+    routed_scale: float = 2.5
+
+    def rows_cols(self, proj):
+        """(rows, K) of a projection: gate/up are [inter, hidden], down [hidden, inter]."""
+        return (self.hidden, self.inter) if proj == PROJ_DOWN else (self.inter, self.hidden)
+
+
+TINY = LayerShape(hidden=512, inter=256, n_experts=16, n_kept=12, n_shared=1,
+                  n_group=2, topk_group=1, top_k=2)
+V3 = LayerShape(hidden=7168, inter=2048, n_experts=256, n_kept=192, n_shared=1,
+                n_group=8, topk_group=4, top_k=8)
+
+WORKLOADS = {
+    "tiny": dict(shape=TINY, tokens=(8,), bits="all4", routing="normal"),
+    "v3_decode": dict(shape=V3, tokens=(1, 16), bits="gu3_d4_sh4", routing="normal"),
+    "v3_prefill": dict(shape=V3, tokens=(2048,), bits="p234_602020", routing="zipf"),
+    "v3_stack": dict(shape=V3, tokens=(1,), bits="p234_701020", routing="normal", layers=58),
+    "v3_sweep": dict(shape=V3, tokens=(1, 16, 64), bits=("all2", "all4", "mixed"),
+                     routing=("normal", "zipf"), kept=(256, 192, 128)),
+}
+
+
+def _key_int(part):
+    if isinstance(part, (int, np.integer)):
+        return int(part)
+    return zlib.crc32(str(part).encode())
+
+
+def rng(*key):
+    """A numpy Generator for the stream named by ``key`` (strings and ints)."""
+    ss = np.random.SeedSequence(MASTER_SEED, spawn_key=tuple(_key_int(k) for k in key))
+    return np.random.Generator(np.random.PCG64(ss))
+
+
+def seed_int(*key):
+    """A 63-bit integer seed for the stream named by ``key`` (for torch generators)."""
+    ss = np.random.SeedSequence(MASTER_SEED, spawn_key=tuple(_key_int(k) for k in key))
+    return int(ss.generate_state(2, np.uint64)[0] >> np.uint64(1))
+
+
+def expert_mask(shape, *key):
+    """uint8 ``[E]``: ``n_kept`` experts kept (1), chosen uniformly at random."""
+    r = rng("mask", *key)
+    mask = np.zeros(shape.n_experts, np.uint8)
+    mask[r.choice(shape.n_experts, shape.n_kept, replace=False)] = 1
+    return mask
+
+
+def bit_plan(shape, plan, *key):
+    """Per-tensor widths: (routed int32 ``[E, 3]``, shared int32 ``[n_shared, 3]``).
+
+    Plans: ``all2``/``all4``/``all3``; ``gu3_d4_sh4`` (routed gate/up 3, routed
+    down 4, shared 4); ``p234_<pppppp>`` (each tensor drawn from {2,3,4} with
+    the given percentages); ``mixed`` (shared 4-bit, routed 2-bit)."""
+    E, S = shape.n_experts, shape.n_shared
+    if plan.startswith("all"):
+        b = int(plan[3:])
+        return np.full((E, 3), b, np.int32), np.full((S, 3), b, np.int32)
+    if plan == "gu3_d4_sh4":
+        routed = np.tile(np.array([3, 3, 4], np.int32), (E, 1))
+        return routed, np.full((S, 3), 4, np.int32)
+    if plan == "mixed":
+        return np.full((E, 3), 2, np.int32), np.full((S, 3), 4, np.int32)
+    if plan.startswith("p234_"):
+        pct = plan[5:]
+        p = np.array([int(pct[0:2]), int(pct[2:4]), int(pct[4:6])], np.float64) / 100.0
+        r = rng("bits", plan, *key)
+        routed = r.choice(np.array([2, 3, 4], np.int32), size=(E, 3), p=p).astype(np.int32)
+        shared = r.choice(np.array([2, 3, 4], np.int32), size=(S, 3), p=p).astype(np.int32)
+        return routed, shared
+    raise ValueError(f"unknown bit plan {plan!r}")
+
+
+def normal_weights(rows, K, *key, std=0.02):
+    """float32 ``[rows, K]`` drawn from N(0, std)."""
+    return (rng("w", *key).standard_normal((rows, K), dtype=np.float32) * np.float32(std))
+
+
+def random_packed(rows, K, bits, *key):
+    """A random tensor already in the packed layout: (codes uint8 ``[rows, K*bits/8]``,
+    scales uint16 ``[rows, K/32]``).
+
+    Every byte string is a valid packing, so codes are uniform random bytes.
+    Scales are binary16 values spread over [0.5, 1.5) times the typical scale
+    of N(0, 0.02) weights at this width (about 0.06 / (2**(bits-1) - 1))."""
+    r = rng("packed", *key)
+    codes = r.integers(0, 256, size=(rows, K * bits // 8), dtype=np.uint8)
+    typical = 0.06 / max(1, (1 << (bits - 1)) - 1)
+    scales = (r.uniform(0.5, 1.5, size=(rows, K // 32)) * typical).astype(np.float16)
+    return codes, scales.view(np.uint16)
+
+
+def bf16_from_f32(a):
+    """Round float32 to the nearest bfloat16 (ties to even); returns uint16 bit patterns."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def activations(n, H, *key):
+    """bfloat16 bit patterns ``[n, H]`` of N(0, 1) draws."""
+    return bf16_from_f32(rng("x", *key).standard_normal((n, H), dtype=np.float32))
+
+
+def normal_logits(n, E, *key):
+    """float32 ``[n, E]`` router logits drawn from N(0, 1)."""
+    return rng("logits", *key).standard_normal((n, E), dtype=np.float32)
+
+
+def zipf_logits(n, mask, *key, s=1.1):
+    """float32 ``[n, E]``: ``log p_{pi(e)} + Gumbel(0, 1)`` for kept experts.
+
+    ``p`` is Zipf(s) over the kept experts under a seeded permutation ``pi``,
+    so the Gumbel-max top-k draws experts without replacement in proportion to
+    ``p``.  Pruned experts get the most popular expert's law, so the router's
+    masking is exercised."""
+    mask = np.asarray(mask).astype(bool)
+    E = mask.shape[0]
+    r = rng("zipf", *key)
+    kept = np.nonzero(mask)[0]
+    ranks = np.empty(E, np.float64)
+    ranks[kept] = r.permutation(len(kept)) + 1.0
+    ranks[~mask] = 1.0
+    logp = -s * np.log(ranks)
+    logp -= np.log(np.sum(np.arange(1, len(kept) + 1, dtype=np.float64) ** -s))
+    gumbel = r.gumbel(0.0, 1.0, size=(n, E))
+    return (logp[None, :] + gumbel).astype(np.float32)
