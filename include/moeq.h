@@ -1,0 +1,207 @@
+/*
+ * moeq -- forward pass of one pruned, mixed-precision, block-quantized
+ * Mixture-of-Experts layer on an AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the compressed DeepSeek MoE block of "Collaborative
+ * Compression for Large-Scale MoE Deployment on Edge" (arXiv 2509.25689):
+ *
+ *   - expert pruning (Section 3.1) leaves a subset of the routed experts; the
+ *     survivors are given here as a mask over the original expert ids;
+ *   - activation adjustment (Section 3.2) sets how many experts each token
+ *     activates (top_k) and how grouped routing restricts them (topk_group);
+ *   - mixed-precision quantization (Section 3.3) gives every weight tensor
+ *     its own low bit width.  This library stores tensors in a symmetric
+ *     block format (32 weights per binary16 scale, 2/3/4-bit codes) instead
+ *     of the paper's llama.cpp formats;
+ *   - each expert is a SwiGLU feed-forward network and the layer output is
+ *     the routing-weighted sum of the chosen experts plus the shared
+ *     expert(s) (Fig. 1, middle).
+ *
+ * Weight format ("canonical packing", the only layout callers ever see):
+ *   a tensor is a row-major [rows x K] matrix, K a multiple of 32.  Every run
+ *   of 32 consecutive weights in a row (a block) has one scale d (binary16 bit
+ *   pattern) and every weight a b-bit code c; the weight's value is
+ *   d * (c - 2^(b-1)).  The 32 codes of a block form one little-endian bit
+ *   string of 32*b bits: code i occupies bits [i*b, i*b + b).  Blocks follow
+ *   each other along the row, rows follow each other; scales are a separate
+ *   row-major [rows x K/32] array.  Projections: 0 = gate [inter x hidden],
+ *   1 = up [inter x hidden], 2 = down [hidden x inter].
+ *
+ * Conventions for every entry point:
+ *   - return value: MOEQ_OK or a negative moeq_status; nothing is thrown
+ *     across this interface.  moeq_last_error() gives the calling thread's
+ *     text for its last failing call;
+ *   - every argument and configuration check happens on the host before any
+ *     HIP runtime call, so all validation errors are reported the same way on
+ *     a machine without a GPU;
+ *   - "DEVICE" pointers are HIP device memory on the device the layer was
+ *     created on (that device must be current when calling); "HOST" pointers
+ *     are ordinary host memory;
+ *   - stream arguments are hipStream_t values passed as void*; NULL means the
+ *     default stream.  Work is enqueued asynchronously; no entry point except
+ *     moeq_layer_create and moeq_destroy synchronizes the host;
+ *   - a layer handle owns one workspace, so calls on one handle must not run
+ *     concurrently on different streams.
+ */
+#ifndef MOEQ_H
+#define MOEQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOEQ_OK = 0,
+  MOEQ_ERR_INVALID_ARG = -1,   /* a NULL pointer, an out-of-range value, an inconsistent config */
+  MOEQ_ERR_UNSUPPORTED = -2,   /* valid in the format but not supported by these kernels */
+  MOEQ_ERR_OUT_OF_MEMORY = -3, /* a device allocation failed */
+  MOEQ_ERR_DEVICE = -4,        /* a HIP runtime call or a kernel launch failed */
+  MOEQ_ERR_CAPACITY = -5       /* n_tokens exceeds the layer's max_tokens */
+} moeq_status;
+
+enum { MOEQ_PROJ_GATE = 0, MOEQ_PROJ_UP = 1, MOEQ_PROJ_DOWN = 2 };
+enum { MOEQ_WEIGHTS_HOST = 0, MOEQ_WEIGHTS_DEVICE = 1 };
+enum { MOEQ_PATH_AUTO = 0, MOEQ_PATH_DECODE = 1, MOEQ_PATH_PREFILL = 2 };
+
+typedef struct moeq_layer moeq_layer; /* opaque; owns every device buffer it allocates */
+
+/* Layer configuration.
+ *   hidden, inter   H and I; both multiples of 128 (the format needs 32, the
+ *                   kernels' 128-weight units need 128: else UNSUPPORTED)
+ *   n_experts       E, routed experts before pruning (= mask length), 1..1024,
+ *                   a multiple of n_group
+ *   n_shared        shared experts, 0..4; always active, weight 1
+ *   n_group         routing groups: experts [g*E/G, (g+1)*E/G) form group g
+ *   topk_group      groups each token may draw from (Section 3.2), 1..n_group
+ *   top_k           experts per token (num_experts_per_tok), 1..32
+ *   group_topn      best scores summed into a group's score, >= 1 (V3: 2)
+ *   norm_topk       1: weights are the chosen sigmoid scores renormalised to
+ *                   sum to 1, then times routed_scale; 0: scores times routed_scale
+ *   routed_scale    the routed scaling factor (V3: 2.5), finite
+ *   max_tokens      largest n_tokens a forward may use; sizes the workspace
+ *   decode_max_tokens  forward takes the decode path (dequant-GEMV) for
+ *                   n_tokens <= this and the prefill path (grouped GEMM on
+ *                   MFMA) above it; 0 selects the library default (32)
+ */
+typedef struct {
+  int32_t hidden;
+  int32_t inter;
+  int32_t n_experts;
+  int32_t n_shared;
+  int32_t n_group;
+  int32_t topk_group;
+  int32_t top_k;
+  int32_t group_topn;
+  int32_t norm_topk;
+  float routed_scale;
+  int32_t max_tokens;
+  int32_t decode_max_tokens;
+} moeq_config;
+
+/* One quantized tensor in the canonical packing described above.
+ *   bits    2, 3 or 4
+ *   codes   rows * K * bits / 8 bytes
+ *   scales  rows * K / 32 binary16 bit patterns */
+typedef struct {
+  int32_t bits;
+  const void* codes;
+  const void* scales;
+} moeq_qtensor;
+
+/* Build a layer (Sections 3.1-3.3: the pruned expert set, the routing
+ * hyper-parameters and the per-tensor bit widths).
+ *   cfg          HOST; copied
+ *   expert_mask  HOST uint8 [n_experts]; nonzero = expert kept by pruning
+ *   score_bias   HOST float [n_experts] added to the sigmoid scores for
+ *                selection only, or NULL for zeros
+ *   routed       [n_experts * 3] descriptors, index e*3 + proj; entries of
+ *                pruned experts are ignored (may be zeroed)
+ *   shared       [n_shared * 3] descriptors, index s*3 + proj; NULL if n_shared = 0
+ *   weights_location  MOEQ_WEIGHTS_HOST: codes/scales are HOST pointers;
+ *                MOEQ_WEIGHTS_DEVICE: DEVICE pointers on the current device
+ *   out          receives the handle
+ * The routing must be feasible: topk_group must not exceed the number of
+ * groups with a kept expert, and the topk_group smallest non-empty groups
+ * must hold at least top_k kept experts (else INVALID_ARG).
+ * All weight data is copied and re-laid-out on the device; the caller may
+ * free its buffers when this returns.  Synchronizes the device.
+ * Errors: INVALID_ARG, UNSUPPORTED (widths or shapes), OUT_OF_MEMORY, DEVICE;
+ * on error *out is set to NULL and nothing is leaked. */
+moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask,
+                              const float* score_bias, const moeq_qtensor* routed,
+                              const moeq_qtensor* shared, int32_t weights_location,
+                              moeq_layer** out);
+
+/* The layer forward (the whole hot path: route, bucket, expert products,
+ * SwiGLU, weighted combine, shared expert).
+ *   x        DEVICE bfloat16 [n_tokens x hidden], row-major
+ *   logits   DEVICE float32 [n_tokens x n_experts] router logits (finite)
+ *   n_tokens 0..max_tokens; 0 enqueues nothing and returns OK
+ *   y        DEVICE float32 [n_tokens x hidden]; fully overwritten
+ * Borrowed pointers must stay valid until the stream work completes.  No
+ * allocation, no memset, no host synchronization: safe to capture in a HIP
+ * graph.  Deterministic: identical inputs give bitwise-identical y.
+ * Errors: INVALID_ARG, CAPACITY (n_tokens > max_tokens), DEVICE. */
+moeq_status moeq_forward(moeq_layer* layer, const void* x, const float* logits,
+                         int32_t n_tokens, float* y, void* stream);
+
+/* Frees everything the layer owns after synchronizing the device.  NULL-safe. */
+void moeq_destroy(moeq_layer* layer);
+
+/* Text for the calling thread's last failing call ("" if none). */
+const char* moeq_last_error(void);
+
+/* Choose the forward path: MOEQ_PATH_AUTO (by decode_max_tokens),
+ * MOEQ_PATH_DECODE or MOEQ_PATH_PREFILL (any n_tokens).  INVALID_ARG otherwise. */
+moeq_status moeq_set_path(moeq_layer* layer, int32_t path);
+
+/* Diagnostic: the router stage of the forward alone (Section 3.2 grouped
+ * top-k over the experts kept by Section 3.1).  Runs the same device code
+ * the forward would run for this n_tokens.
+ *   logits  DEVICE float32 [n_tokens x n_experts]
+ *   idx     DEVICE int32 [n_tokens x top_k]: chosen experts, best first
+ *   w       DEVICE float32 [n_tokens x top_k]: their combine weights */
+moeq_status moeq_route(moeq_layer* layer, const float* logits, int32_t n_tokens,
+                       int32_t* idx, float* w, void* stream);
+
+/* Diagnostic: the bucketing stage alone, on given expert ids.
+ *   idx      DEVICE int32 [n_tokens x top_k]; every id a kept expert, ids of
+ *            one token distinct (as the router produces)
+ *   offsets  DEVICE int32 [n_experts + 1]: exclusive prefix sum of counts
+ *   perm     DEVICE int32 [n_tokens * top_k]: value t*top_k + j, ordered by
+ *            expert, then token */
+moeq_status moeq_bucket(moeq_layer* layer, const int32_t* idx, int32_t n_tokens,
+                        int32_t* offsets, int32_t* perm, void* stream);
+
+/* Diagnostic: one stored tensor decoded to float32 (exact: d * (c - 2^(b-1))).
+ *   expert   0..n_experts-1 (a kept expert) or -1 - s for shared expert s
+ *   proj     MOEQ_PROJ_*
+ *   out      DEVICE float32 [rows x K] */
+moeq_status moeq_dequant(moeq_layer* layer, int32_t expert, int32_t proj, float* out,
+                         void* stream);
+
+/* Quantize a float32 matrix into the canonical format (Section 3.3's
+ * "quantize to the base precision" step, in this library's block format):
+ * per block d = binary16(max|w| / (2^(b-1)-1)) rounded to nearest even from
+ * the exact quotient, codes clamp(rint(w/d)) + 2^(b-1) (ties to even; all
+ * codes 2^(b-1) when d = 0).
+ *   w       DEVICE float32 [rows x K], K a multiple of 32, finite
+ *   bits    2, 3 or 4
+ *   codes   DEVICE [rows * K * bits / 8] bytes
+ *   scales  DEVICE uint16 [rows * K / 32] */
+moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits,
+                          void* codes, uint16_t* scales, void* stream);
+
+/* Sizes: weight bytes as stored (codes plus scales of every kept expert and
+ * shared expert) and workspace bytes.  Either pointer may be NULL. */
+moeq_status moeq_layer_bytes(const moeq_layer* layer, uint64_t* weight_bytes,
+                             uint64_t* workspace_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOEQ_H */

@@ -96,13 +96,16 @@ def pack(codes, bits):
 
 
 def unpack(packed, bits, K):
-    """packed bytes ``[R, K*bits/8]`` -> codes uint8 ``[R, K]``."""
+    """packed bytes ``[R, K*bits/8]`` -> codes uint8 ``[R, K]``.
+
+    Bit ``j`` of code ``i`` is bit ``i*bits + j`` of the row's bit string."""
     packed = np.asarray(packed, dtype=np.uint8)
     R = packed.shape[0]
     bitstr = np.unpackbits(packed, axis=1, bitorder="little")[:, : K * bits]
-    bitstr = bitstr.reshape(R, K, bits).astype(np.uint16)
-    weights = (1 << np.arange(bits, dtype=np.uint16))
-    return (bitstr * weights).sum(axis=2).astype(np.uint8)
+    codes = np.zeros((R, K), np.uint8)
+    for j in range(bits):
+        codes |= bitstr[:, j::bits] << np.uint8(j)
+    return codes
 
 
 def tensor_bytes(rows, K, bits):

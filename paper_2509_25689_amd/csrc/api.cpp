@@ -1,0 +1,484 @@
+// Host runtime of the C interface declared in include/moeq.h: validation,
+// the device weight store, the workspace and the per-forward dispatch.
+//
+// Every argument check runs before the first HIP runtime call of an entry
+// point, so validation behaves identically without a GPU.  Device memory is
+// owned by the layer and released by moeq_destroy (or on a failed create).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace moeq;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+moeq_status fail(moeq_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+moeq_status ok() { return MOEQ_OK; }
+
+moeq_status hip_fail(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? MOEQ_ERR_OUT_OF_MEMORY : MOEQ_ERR_DEVICE, "%s: %s", what,
+              hipGetErrorString(e));
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct TensorPlan {
+  size_t codes_off, scales_off;
+  int rows, K, bits;
+};
+
+}  // namespace
+
+struct moeq_layer {
+  moeq_config cfg{};
+  int device = 0;
+  int path = MOEQ_PATH_AUTO;
+  int decode_max = kDefaultDecodeMax;
+  int n_kept = 0;
+  uint64_t weight_bytes = 0;   // codes + scales as stored
+  uint64_t ws_bytes = 0;
+  std::vector<TensorDev> desc_host;  // [(E + S) * 3]
+  void* store = nullptr;
+  TensorDev* desc = nullptr;
+  uint8_t* mask = nullptr;
+  float* bias = nullptr;
+  void* ws_mem = nullptr;
+  Workspace ws{};
+};
+
+namespace {
+
+void release(moeq_layer* L) {
+  if (!L) return;
+  hipFree(L->store);
+  hipFree(L->desc);
+  hipFree(L->mask);
+  hipFree(L->bias);
+  hipFree(L->ws_mem);
+  delete L;
+}
+
+moeq_status check_config(const moeq_config* c) {
+  if (!c) return fail(MOEQ_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->hidden <= 0 || c->inter <= 0 || c->hidden % kBlock || c->inter % kBlock)
+    return fail(MOEQ_ERR_INVALID_ARG, "hidden (%d) and inter (%d) must be positive multiples of 32",
+                c->hidden, c->inter);
+  if (c->hidden % kUnit || c->inter % kUnit)
+    return fail(MOEQ_ERR_UNSUPPORTED, "hidden (%d) and inter (%d) must be multiples of 128",
+                c->hidden, c->inter);
+  if (c->hidden > 8192 || c->inter > 8192)
+    return fail(MOEQ_ERR_UNSUPPORTED, "hidden and inter are limited to 8192 (got %d, %d)", c->hidden,
+                c->inter);
+  if (c->n_experts < 1 || c->n_experts > kMaxExperts)
+    return fail(MOEQ_ERR_INVALID_ARG, "n_experts %d outside 1..%d", c->n_experts, kMaxExperts);
+  if (c->n_group < 1 || c->n_group > 64 || c->n_experts % c->n_group)
+    return fail(MOEQ_ERR_INVALID_ARG, "n_group %d must be 1..64 and divide n_experts %d", c->n_group,
+                c->n_experts);
+  if (c->topk_group < 1 || c->topk_group > c->n_group)
+    return fail(MOEQ_ERR_INVALID_ARG, "topk_group %d outside 1..n_group", c->topk_group);
+  if (c->top_k < 1 || c->top_k > kMaxTopK || c->top_k > c->n_experts)
+    return fail(MOEQ_ERR_INVALID_ARG, "top_k %d outside 1..%d", c->top_k, kMaxTopK);
+  if (c->group_topn < 1 || c->group_topn > c->n_experts / c->n_group)
+    return fail(MOEQ_ERR_INVALID_ARG, "group_topn %d outside 1..experts per group", c->group_topn);
+  if (c->norm_topk != 0 && c->norm_topk != 1)
+    return fail(MOEQ_ERR_INVALID_ARG, "norm_topk must be 0 or 1");
+  if (!isfinite(c->routed_scale))
+    return fail(MOEQ_ERR_INVALID_ARG, "routed_scale must be finite");
+  if (c->n_shared < 0 || c->n_shared > kMaxShared)
+    return fail(MOEQ_ERR_INVALID_ARG, "n_shared %d outside 0..%d", c->n_shared, kMaxShared);
+  if (c->max_tokens < 1 || c->max_tokens > (1 << 20))
+    return fail(MOEQ_ERR_INVALID_ARG, "max_tokens %d outside 1..2^20", c->max_tokens);
+  if (c->decode_max_tokens < 0 || c->decode_max_tokens > kDecodeMaxTokens)
+    return fail(MOEQ_ERR_INVALID_ARG, "decode_max_tokens %d outside 0..%d", c->decode_max_tokens,
+                kDecodeMaxTokens);
+  return ok();
+}
+
+moeq_status check_tensor(const moeq_qtensor& t, const char* who, int e, int p) {
+  if (t.bits < 2 || t.bits > 4)
+    return fail(t.bits == 5 || t.bits == 6 || t.bits == 8 ? MOEQ_ERR_UNSUPPORTED : MOEQ_ERR_INVALID_ARG,
+                "%s %d proj %d: bits %d not in {2,3,4}", who, e, p, t.bits);
+  if (!t.codes || !t.scales) return fail(MOEQ_ERR_INVALID_ARG, "%s %d proj %d: NULL codes or scales", who, e, p);
+  return ok();
+}
+
+// Worst case of the grouped selection: the topk_group non-empty groups with
+// the fewest kept experts must still hold top_k of them.
+moeq_status check_routing(const moeq_config* c, const uint8_t* mask, int* n_kept) {
+  const int per = c->n_experts / c->n_group;
+  std::vector<int> counts;
+  int kept = 0;
+  for (int g = 0; g < c->n_group; ++g) {
+    int n = 0;
+    for (int e = g * per; e < (g + 1) * per; ++e) n += mask[e] != 0;
+    kept += n;
+    if (n > 0) counts.push_back(n);
+  }
+  *n_kept = kept;
+  if ((int)counts.size() < c->topk_group)
+    return fail(MOEQ_ERR_INVALID_ARG, "only %d groups have kept experts; topk_group is %d",
+                (int)counts.size(), c->topk_group);
+  std::sort(counts.begin(), counts.end());
+  int worst = 0;
+  for (int i = 0; i < c->topk_group; ++i) worst += counts[i];
+  if (worst < c->top_k)
+    return fail(MOEQ_ERR_INVALID_ARG,
+                "the %d smallest non-empty groups hold %d kept experts, fewer than top_k %d",
+                c->topk_group, worst, c->top_k);
+  return ok();
+}
+
+RouterParams router_params(const moeq_layer* L, const float* logits) {
+  RouterParams rp;
+  rp.logits = logits;
+  rp.mask = L->mask;
+  rp.bias = L->bias;
+  rp.E = L->cfg.n_experts;
+  rp.G = L->cfg.n_group;
+  rp.TG = L->cfg.topk_group;
+  rp.k = L->cfg.top_k;
+  rp.topn = L->cfg.group_topn;
+  rp.norm = L->cfg.norm_topk;
+  rp.scale = L->cfg.routed_scale;
+  return rp;
+}
+
+moeq_status check_device(const moeq_layer* L) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != L->device)
+    return fail(MOEQ_ERR_INVALID_ARG, "layer lives on device %d but device %d is current", L->device, dev);
+  return ok();
+}
+
+// Route (+ bucket) n tokens into the workspace: the first stage of a forward.
+hipError_t route_and_bucket(moeq_layer* L, const float* logits, int n, hipStream_t s) {
+  const RouterParams rp = router_params(L, logits);
+  if (n <= kDecodeMaxTokens) return launch_route_bucket_small(rp, nullptr, n, L->ws, s);
+  hipError_t e = launch_route_tokens(rp, n, L->ws.idx, L->ws.w, s);
+  if (e != hipSuccess) return e;
+  return launch_bucket_chunked(L->ws.idx, n, L->cfg.top_k, L->cfg.n_experts, L->ws, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* moeq_last_error(void) { return g_last_error.c_str(); }
+
+moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask,
+                              const float* score_bias, const moeq_qtensor* routed,
+                              const moeq_qtensor* shared, int32_t weights_location,
+                              moeq_layer** out) {
+  if (!out) return fail(MOEQ_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  moeq_status st = check_config(cfg);
+  if (st != MOEQ_OK) return st;
+  if (!expert_mask) return fail(MOEQ_ERR_INVALID_ARG, "expert_mask is NULL");
+  if (weights_location != MOEQ_WEIGHTS_HOST && weights_location != MOEQ_WEIGHTS_DEVICE)
+    return fail(MOEQ_ERR_INVALID_ARG, "weights_location %d is neither HOST nor DEVICE", weights_location);
+  const int E = cfg->n_experts, S = cfg->n_shared, H = cfg->hidden, I = cfg->inter;
+  int n_kept = 0;
+  st = check_routing(cfg, expert_mask, &n_kept);
+  if (st != MOEQ_OK) return st;
+  if (score_bias)
+    for (int e = 0; e < E; ++e)
+      if (!isfinite(score_bias[e]) || fabsf(score_bias[e]) > 1e30f)
+        return fail(MOEQ_ERR_INVALID_ARG, "score_bias[%d] is not a finite value of magnitude <= 1e30", e);
+  if (!routed) return fail(MOEQ_ERR_INVALID_ARG, "routed is NULL");
+  if (S > 0 && !shared) return fail(MOEQ_ERR_INVALID_ARG, "shared is NULL but n_shared = %d", S);
+  for (int e = 0; e < E; ++e)
+    if (expert_mask[e])
+      for (int p = 0; p < 3; ++p)
+        if ((st = check_tensor(routed[e * 3 + p], "expert", e, p)) != MOEQ_OK) return st;
+  for (int s = 0; s < S; ++s)
+    for (int p = 0; p < 3; ++p)
+      if ((st = check_tensor(shared[s * 3 + p], "shared expert", s, p)) != MOEQ_OK) return st;
+
+  // ---- plan the weight store: one allocation, 256-byte aligned tensors ----
+  std::vector<TensorPlan> plan((size_t)(E + S) * 3);
+  size_t off = 0, max_codes = 0;
+  uint64_t wbytes = 0;
+  auto plan_tensor = [&](int slot, int p, const moeq_qtensor& t) {
+    TensorPlan& tp = plan[(size_t)slot * 3 + p];
+    tp.rows = p == MOEQ_PROJ_DOWN ? H : I;
+    tp.K = p == MOEQ_PROJ_DOWN ? I : H;
+    tp.bits = t.bits;
+    const size_t cb = (size_t)tp.rows * tp.K * t.bits / 8, sb = (size_t)tp.rows * (tp.K / kBlock) * 2;
+    tp.codes_off = off;
+    off = align_up(off + cb, 256);
+    tp.scales_off = off;
+    off = align_up(off + sb, 256);
+    max_codes = cb > max_codes ? cb : max_codes;
+    wbytes += cb + sb;
+  };
+  for (int e = 0; e < E; ++e)
+    if (expert_mask[e])
+      for (int p = 0; p < 3; ++p) plan_tensor(e, p, routed[e * 3 + p]);
+  for (int s = 0; s < S; ++s)
+    for (int p = 0; p < 3; ++p) plan_tensor(E + s, p, shared[s * 3 + p]);
+
+  // ---- workspace sizes ----
+  const int T = cfg->max_tokens, k = cfg->top_k;
+  const size_t nk = (size_t)T * k, rows_h = nk + (size_t)T * S;
+  const size_t chunks = (T + kChunk - 1) / kChunk;
+  size_t wo = 0;
+  auto ws_take = [&](size_t bytes) {
+    const size_t at = wo;
+    wo = align_up(wo + bytes, 256);
+    return at;
+  };
+  const size_t o_idx = ws_take(nk * 4), o_w = ws_take(nk * 4), o_off = ws_take((size_t)(E + 1) * 4),
+               o_perm = ws_take(nk * 4), o_act = ws_take((size_t)(E + 1) * 4),
+               o_cc = ws_take(chunks * E * 4), o_rank = ws_take(nk * 4),
+               o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4);
+
+  // ---- device work ----
+  moeq_layer* L = new moeq_layer();
+  L->cfg = *cfg;
+  L->n_kept = n_kept;
+  L->decode_max = cfg->decode_max_tokens ? cfg->decode_max_tokens : kDefaultDecodeMax;
+  L->weight_bytes = wbytes;
+  L->ws_bytes = wo;
+  hipError_t he = hipGetDevice(&L->device);
+  if (he != hipSuccess) {
+    release(L);
+    return hip_fail(he, "hipGetDevice");
+  }
+  uint8_t* staging = nullptr;
+  auto bail = [&](hipError_t e, const char* what) {
+    hipDeviceSynchronize();
+    hipFree(staging);
+    release(L);
+    return hip_fail(e, what);
+  };
+  if ((he = hipMalloc(&L->store, off ? off : 256)) != hipSuccess) return bail(he, "hipMalloc(weights)");
+  if ((he = hipMalloc(&L->ws_mem, wo)) != hipSuccess) return bail(he, "hipMalloc(workspace)");
+  if ((he = hipMalloc((void**)&L->desc, sizeof(TensorDev) * plan.size())) != hipSuccess)
+    return bail(he, "hipMalloc(descriptors)");
+  if ((he = hipMalloc((void**)&L->mask, E)) != hipSuccess) return bail(he, "hipMalloc(mask)");
+  if ((he = hipMalloc((void**)&L->bias, sizeof(float) * E)) != hipSuccess) return bail(he, "hipMalloc(bias)");
+  if (weights_location == MOEQ_WEIGHTS_HOST && max_codes &&
+      (he = hipMalloc((void**)&staging, max_codes)) != hipSuccess)
+    return bail(he, "hipMalloc(staging)");
+
+  uint8_t* base = (uint8_t*)L->store;
+  L->desc_host.assign(plan.size(), TensorDev{nullptr, nullptr, 0, 0, 0, 0});
+  auto upload = [&](int slot, int p, const moeq_qtensor& t) -> hipError_t {
+    const TensorPlan& tp = plan[(size_t)slot * 3 + p];
+    const size_t cb = (size_t)tp.rows * tp.K * tp.bits / 8, sb = (size_t)tp.rows * (tp.K / kBlock) * 2;
+    const uint8_t* src = (const uint8_t*)t.codes;
+    hipError_t e;
+    if (weights_location == MOEQ_WEIGHTS_HOST) {
+      // staging is reused: the null-stream copy waits for the previous repack
+      if ((e = hipMemcpy(staging, src, cb, hipMemcpyHostToDevice)) != hipSuccess) return e;
+      src = staging;
+    }
+    if ((e = launch_repack(src, tp.rows, tp.K, tp.bits, (uint32_t*)(base + tp.codes_off), 0)) != hipSuccess)
+      return e;
+    if ((e = hipMemcpy(base + tp.scales_off, t.scales, sb,
+                       weights_location == MOEQ_WEIGHTS_HOST ? hipMemcpyHostToDevice
+                                                             : hipMemcpyDeviceToDevice)) != hipSuccess)
+      return e;
+    TensorDev& d = L->desc_host[(size_t)slot * 3 + p];
+    d.codes = (const uint32_t*)(base + tp.codes_off);
+    d.scales = (const uint16_t*)(base + tp.scales_off);
+    d.bits = tp.bits;
+    d.rows = tp.rows;
+    d.K = tp.K;
+    return hipSuccess;
+  };
+  for (int e = 0; e < E; ++e)
+    if (expert_mask[e])
+      for (int p = 0; p < 3; ++p)
+        if ((he = upload(e, p, routed[e * 3 + p])) != hipSuccess) return bail(he, "weight upload");
+  for (int s = 0; s < S; ++s)
+    for (int p = 0; p < 3; ++p)
+      if ((he = upload(E + s, p, shared[s * 3 + p])) != hipSuccess) return bail(he, "weight upload");
+
+  std::vector<float> bias_h(E, 0.0f);
+  if (score_bias) memcpy(bias_h.data(), score_bias, sizeof(float) * E);
+  if ((he = hipMemcpy(L->desc, L->desc_host.data(), sizeof(TensorDev) * plan.size(),
+                      hipMemcpyHostToDevice)) != hipSuccess ||
+      (he = hipMemcpy(L->mask, expert_mask, E, hipMemcpyHostToDevice)) != hipSuccess ||
+      (he = hipMemcpy(L->bias, bias_h.data(), sizeof(float) * E, hipMemcpyHostToDevice)) != hipSuccess)
+    return bail(he, "hipMemcpy(tables)");
+  if ((he = hipDeviceSynchronize()) != hipSuccess) return bail(he, "create");
+  hipFree(staging);
+  staging = nullptr;
+
+  uint8_t* w = (uint8_t*)L->ws_mem;
+  L->ws.idx = (int32_t*)(w + o_idx);
+  L->ws.w = (float*)(w + o_w);
+  L->ws.offsets = (int32_t*)(w + o_off);
+  L->ws.perm = (int32_t*)(w + o_perm);
+  L->ws.active = (int32_t*)(w + o_act);
+  L->ws.chunk_cnt = (int32_t*)(w + o_cc);
+  L->ws.rank = (int32_t*)(w + o_rank);
+  L->ws.h = (float*)(w + o_h);
+  L->ws.partial = (float*)(w + o_part);
+  *out = L;
+  return ok();
+}
+
+void moeq_destroy(moeq_layer* L) {
+  if (!L) return;
+  hipDeviceSynchronize();
+  release(L);
+}
+
+moeq_status moeq_set_path(moeq_layer* L, int32_t path) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (path != MOEQ_PATH_AUTO && path != MOEQ_PATH_DECODE && path != MOEQ_PATH_PREFILL)
+    return fail(MOEQ_ERR_INVALID_ARG, "path %d is not AUTO, DECODE or PREFILL", path);
+  L->path = path;
+  return ok();
+}
+
+moeq_status moeq_layer_bytes(const moeq_layer* L, uint64_t* weight_bytes, uint64_t* workspace_bytes) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (weight_bytes) *weight_bytes = L->weight_bytes;
+  if (workspace_bytes) *workspace_bytes = L->ws_bytes;
+  return ok();
+}
+
+moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int32_t n, float* y,
+                         void* stream) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (n < 0) return fail(MOEQ_ERR_INVALID_ARG, "n_tokens %d is negative", n);
+  if (n > L->cfg.max_tokens)
+    return fail(MOEQ_ERR_CAPACITY, "n_tokens %d exceeds max_tokens %d", n, L->cfg.max_tokens);
+  if (n == 0) return ok();
+  if (!x || !logits || !y) return fail(MOEQ_ERR_INVALID_ARG, "x, logits and y must not be NULL");
+  if (!aligned16(x) || !aligned16(y) || !aligned16(logits))
+    return fail(MOEQ_ERR_INVALID_ARG, "x, logits and y must be 16-byte aligned");
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = route_and_bucket(L, logits, n, s);
+  if (e != hipSuccess) return hip_fail(e, "route/bucket launch");
+  DecodeArgs a;
+  a.desc = L->desc;
+  a.x = (const uint16_t*)x;
+  a.active = L->ws.active;
+  a.offsets = L->ws.offsets;
+  a.perm = L->ws.perm;
+  a.w = L->ws.w;
+  a.h = L->ws.h;
+  a.partial = L->ws.partial;
+  a.y = y;
+  a.n = n;
+  a.H = L->cfg.hidden;
+  a.I = L->cfg.inter;
+  a.E = L->cfg.n_experts;
+  a.S = L->cfg.n_shared;
+  a.k = L->cfg.top_k;
+  const long long nk = (long long)n * a.k;
+  a.max_active = (int)(nk < L->n_kept ? nk : L->n_kept);
+  const bool prefill =
+      L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
+  e = prefill ? launch_prefill(a, s) : launch_decode(a, s);
+  if (e != hipSuccess) return hip_fail(e, prefill ? "prefill launch" : "decode launch");
+  return ok();
+}
+
+moeq_status moeq_route(moeq_layer* L, const float* logits, int32_t n, int32_t* idx, float* w,
+                       void* stream) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (n < 0 || n > L->cfg.max_tokens)
+    return fail(n < 0 ? MOEQ_ERR_INVALID_ARG : MOEQ_ERR_CAPACITY, "n_tokens %d outside 0..max_tokens", n);
+  if (n == 0) return ok();
+  if (!logits || !idx || !w) return fail(MOEQ_ERR_INVALID_ARG, "logits, idx and w must not be NULL");
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = route_and_bucket(L, logits, n, s);
+  if (e != hipSuccess) return hip_fail(e, "route launch");
+  const size_t bytes = (size_t)n * L->cfg.top_k * 4;
+  if ((e = hipMemcpyAsync(idx, L->ws.idx, bytes, hipMemcpyDeviceToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(w, L->ws.w, bytes, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return hip_fail(e, "route copy-out");
+  return ok();
+}
+
+moeq_status moeq_bucket(moeq_layer* L, const int32_t* idx, int32_t n, int32_t* offsets, int32_t* perm,
+                        void* stream) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (n < 0 || n > L->cfg.max_tokens)
+    return fail(n < 0 ? MOEQ_ERR_INVALID_ARG : MOEQ_ERR_CAPACITY, "n_tokens %d outside 0..max_tokens", n);
+  if (!idx || !offsets || !perm) return fail(MOEQ_ERR_INVALID_ARG, "idx, offsets and perm must not be NULL");
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const int E = L->cfg.n_experts, k = L->cfg.top_k;
+  hipError_t e;
+  if (n == 0) {
+    e = hipMemsetAsync(offsets, 0, (size_t)(E + 1) * 4, s);
+    return e == hipSuccess ? ok() : hip_fail(e, "bucket");
+  }
+  if (n <= kDecodeMaxTokens)
+    e = launch_route_bucket_small(router_params(L, nullptr), idx, n, L->ws, s);
+  else
+    e = launch_bucket_chunked(idx, n, k, E, L->ws, s);
+  if (e != hipSuccess) return hip_fail(e, "bucket launch");
+  if ((e = hipMemcpyAsync(offsets, L->ws.offsets, (size_t)(E + 1) * 4, hipMemcpyDeviceToDevice, s)) !=
+          hipSuccess ||
+      (e = hipMemcpyAsync(perm, L->ws.perm, (size_t)n * k * 4, hipMemcpyDeviceToDevice, s)) != hipSuccess)
+    return hip_fail(e, "bucket copy-out");
+  return ok();
+}
+
+moeq_status moeq_dequant(moeq_layer* L, int32_t expert, int32_t proj, float* out, void* stream) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (proj < 0 || proj > 2) return fail(MOEQ_ERR_INVALID_ARG, "proj %d outside 0..2", proj);
+  const int E = L->cfg.n_experts, S = L->cfg.n_shared;
+  int slot;
+  if (expert >= 0 && expert < E)
+    slot = expert;
+  else if (expert < 0 && -1 - expert < S)
+    slot = E + (-1 - expert);
+  else
+    return fail(MOEQ_ERR_INVALID_ARG, "expert %d is neither a routed id nor -1-s for a shared expert", expert);
+  const TensorDev& t = L->desc_host[(size_t)slot * 3 + proj];
+  if (!t.codes) return fail(MOEQ_ERR_INVALID_ARG, "expert %d was pruned", expert);
+  if (!out) return fail(MOEQ_ERR_INVALID_ARG, "out is NULL");
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  hipError_t e = launch_dequant(t, out, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
+}
+
+moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits, void* codes,
+                          uint16_t* scales, void* stream) {
+  if (!w || !codes || !scales) return fail(MOEQ_ERR_INVALID_ARG, "w, codes and scales must not be NULL");
+  if (rows < 0 || K < 0 || K % kBlock) return fail(MOEQ_ERR_INVALID_ARG, "rows %d / K %d invalid", rows, K);
+  if (bits < 2 || bits > 4)
+    return fail(bits == 5 || bits == 6 || bits == 8 ? MOEQ_ERR_UNSUPPORTED : MOEQ_ERR_INVALID_ARG,
+                "bits %d not in {2,3,4}", bits);
+  if (rows == 0 || K == 0) return ok();
+  hipError_t e = launch_quantize(w, rows, K, bits, (uint8_t*)codes, scales, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "quantize launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,443 @@
+// Decode path: fused dequantize x matrix-vector products for small batches.
+//
+// Per token the layer (Fig. 1, middle, of arXiv 2509.25689) evaluates the k
+// routed experts it chose and the shared expert(s), each a SwiGLU network
+// h = silu(W_gate x) * (W_up x), o = W_down h, and sums the outputs with the
+// routing weights.  The work per token is about 2 * sum_i k_i P_i FLOPs
+// (Section 3.2), but at batch sizes of a few tokens every weight byte is used
+// once, so the path is bound by streaming the packed weights from HBM.
+//
+// Work decomposition.  A workgroup handles one (expert slot, row tile) pair:
+// the slot is a shared expert or one entry of the device-built list of active
+// experts (no host synchronization: slots beyond the active count exit at
+// once).  Inside, lanes are split into groups of LPR lanes; a group owns one
+// row, each lane one 128-weight unit of it (coalesced 16-byte loads of the
+// packed codes, see layout.h).  The weights of the wave's rows are loaded to
+// registers once and reused for every token of the expert's bucket, whose
+// activations are staged in LDS in chunks of TM tokens together with their
+// per-block sums.  The dot products run on v_dot2_f32_bf16 with float32
+// accumulation; the per-block scale and zero point are applied once per
+// block; the group reduces its partial sums with cross-lane shuffles in a
+// fixed order, so results are deterministic.
+//
+// gate/up kernel: writes h (float32) for every assignment in bucket order.
+// down kernel: the activations h are split into bfloat16 hi + lo parts
+// (about 16 significant bits) and the result, times the token's routing
+// weight, is written as one partial row per (token, slot).
+// combine kernel: y_t = sum_j partial(t, j) (j in slot order) + shared.
+#include "internal.h"
+#include "layout.h"
+
+namespace moeq {
+
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against LDS bank conflicts
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                         __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+// Which expert and tokens a slot covers.
+struct Slot {
+  int desc;     // descriptor row (expert id, or E + s for shared expert s)
+  int M;        // tokens in the bucket
+  int base;     // first activation row (h) of the bucket
+  int shared;   // shared expert index, or -1
+};
+
+__device__ __forceinline__ bool slot_info(const DecodeArgs& a, int slot, Slot& s) {
+  if (slot < a.S) {
+    s.desc = a.E + slot;
+    s.M = a.n;
+    s.base = a.n * a.k + slot * a.n;
+    s.shared = slot;
+    return true;
+  }
+  const int i = slot - a.S;
+  if (i >= a.active[0]) return false;
+  const int e = a.active[1 + i];
+  s.desc = e;
+  s.base = a.offsets[e];
+  s.M = a.offsets[e + 1] - s.base;
+  s.shared = -1;
+  return true;
+}
+
+// One block's contribution for one token: d * sum_i (c_i - z) x_i, from the
+// block's code pairs p, the token's 16 activation dwords at xl (and their lo
+// parts at xl + lo_offset when NX = 2) and the block sum X.
+template <int NX>
+__device__ __forceinline__ float block_dot(const uint32_t (&p)[16], const uint32_t* xl, int lo_offset,
+                                           float ds, float X, float acc_out) {
+  float acc = 0.0f;
+  const u32x4* x4 = reinterpret_cast<const u32x4*>(xl);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const u32x4 xv = x4[c];
+    acc = dot2(p[4 * c + 0], xv.x, acc);
+    acc = dot2(p[4 * c + 1], xv.y, acc);
+    acc = dot2(p[4 * c + 2], xv.z, acc);
+    acc = dot2(p[4 * c + 3], xv.w, acc);
+  }
+  if constexpr (NX == 2) {
+    const u32x4* l4 = reinterpret_cast<const u32x4*>(xl + lo_offset);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const u32x4 xv = l4[c];
+      acc = dot2(p[4 * c + 0], xv.x, acc);
+      acc = dot2(p[4 * c + 1], xv.y, acc);
+      acc = dot2(p[4 * c + 2], xv.z, acc);
+      acc = dot2(p[4 * c + 3], xv.w, acc);
+    }
+  }
+  return fmaf(ds, fmaf(-192.0f, X, acc), acc_out);
+}
+
+// block q's scale (binary16, 4 per unit in sc) times 2^(b-7)
+template <int B>
+__device__ __forceinline__ float block_scale(uint2 sc, int q) {
+  const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
+  return half_to_float(s16) * (1.0f / (float)(1 << (7 - B)));
+}
+
+template <int LPR>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+  for (int off = LPR / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+__device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
+
+// An empty asm statement that "modifies" the registers: keeps the compiler
+// from hoisting the per-chunk unpacking of loop-invariant weights out of the
+// token-chunk loop (which would hold every unpacked pair in registers).
+template <int N>
+__device__ __forceinline__ void opaque(uint32_t (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+}
+
+// ---------------------------------------------------------------------------
+// gate/up + SwiGLU for one (slot, row tile), gate/up widths BG/BU.
+template <int BG, int BU, int LPR, int TM, int RP>
+__device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl, const TensorDev& tg,
+                                            const TensorDev& tu, uint32_t* smem) {
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const int xts = U * kXStride, sts = U * 4;  // per-token LDS strides (dwords, floats)
+  uint32_t* xl = smem;
+  float* xs = reinterpret_cast<float*>(smem + TM * xts);
+
+  constexpr int GPW = 64 / LPR;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int grp = lane / LPR, u = lane % LPR;
+  const bool uok = u < U;
+  int row[RP];
+  bool ok[RP];
+  uint32_t wg[RP][4 * BG], wu[RP][4 * BU];
+  uint2 sg[RP], su[RP];
+#pragma unroll
+  for (int r = 0; r < RP; ++r) {
+    row[r] = blockIdx.x * (4 * GPW * RP) + (wave * RP + r) * GPW + grp;
+    ok[r] = row[r] < I;
+    if (ok[r] && uok) {
+      load_unit<BG>(tg.codes + (size_t)row[r] * BG * U * 4, U, u, wg[r]);
+      load_unit<BU>(tu.codes + (size_t)row[r] * BU * U * 4, U, u, wu[r]);
+      sg[r] = *reinterpret_cast<const uint2*>(tg.scales + (size_t)row[r] * (H / kBlock) + 4 * u);
+      su[r] = *reinterpret_cast<const uint2*>(tu.scales + (size_t)row[r] * (H / kBlock) + 4 * u);
+    }
+  }
+
+  for (int m0 = 0; m0 < sl.M; m0 += TM) {
+    const int mc = min(TM, sl.M - m0);
+    __syncthreads();
+    // stage the chunk's x rows: 16-byte pieces, 4 per block of 32
+    for (int m = 0; m < mc; ++m) {
+      const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
+      const u32x4* src = reinterpret_cast<const u32x4*>(a.x + (size_t)t * H);
+      for (int q = threadIdx.x; q < H / 8; q += 256) {
+        const u32x4 v = src[q];
+        float s = 0.0f;
+        s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
+        s += bf16_lo(v.z); s += bf16_hi(v.z); s += bf16_lo(v.w); s += bf16_hi(v.w);
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        const int uu = q >> 4, cq = q & 15;
+        *reinterpret_cast<u32x4*>(xl + m * xts + uu * kXStride + cq * 4) = v;
+        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RP; ++r) {
+      opaque(wg[r]);
+      opaque(wu[r]);
+    }
+    float g[RP][TM], up[RP][TM];
+#pragma unroll
+    for (int r = 0; r < RP; ++r)
+#pragma unroll
+      for (int m = 0; m < TM; ++m) g[r][m] = up[r][m] = 0.0f;
+    if (uok) {
+      const uint32_t* xu = xl + u * kXStride;
+      const float* su4 = xs + u * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int r = 0; r < RP; ++r) {
+          if (!ok[r]) continue;
+          uint32_t p[16];
+          block_pairs<BG>(wg[r] + q * BG, p);
+          const float dg = block_scale<BG>(sg[r], q);
+#pragma unroll
+          for (int m = 0; m < TM; ++m)
+            if (m < mc) g[r][m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, dg, su4[m * sts + q], g[r][m]);
+          block_pairs<BU>(wu[r] + q * BU, p);
+          const float du = block_scale<BU>(su[r], q);
+#pragma unroll
+          for (int m = 0; m < TM; ++m)
+            if (m < mc) up[r][m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, du, su4[m * sts + q], up[r][m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RP; ++r) {
+      if (!ok[r]) continue;  // uniform across the lane group
+#pragma unroll
+      for (int m = 0; m < TM; ++m) {
+        if (m < mc) {
+          const float gs = group_sum<LPR>(g[r][m]), us = group_sum<LPR>(up[r][m]);
+          if (u == 0) a.h[(size_t)(sl.base + m0 + m) * I + row[r]] = silu(gs) * us;
+        }
+      }
+    }
+  }
+}
+
+// grid = (row tiles of I, S + max_active), 256 threads
+template <int LPR, int TM, int RP>
+__global__ __launch_bounds__(256) void gateup_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  Slot sl;
+  if (!slot_info(a, blockIdx.y, sl)) return;
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  switch (tg.bits * 8 + tu.bits) {
+    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    default: break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down x routing weight for one (slot, row tile), down width BD.
+template <int BD, int LPR, int TM, int RP>
+__device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, const TensorDev& td,
+                                          uint32_t* smem) {
+  const int H = a.H, I = a.I, U = I / kUnit;
+  const int xts = 2 * U * kXStride, sts = U * 4, lo = U * kXStride;
+  uint32_t* xl = smem;
+  float* xs = reinterpret_cast<float*>(smem + TM * xts);
+
+  constexpr int GPW = 64 / LPR;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int grp = lane / LPR, u = lane % LPR;
+  const bool uok = u < U;
+  int row[RP];
+  bool ok[RP];
+  uint32_t wd[RP][4 * BD];
+  uint2 sd[RP];
+#pragma unroll
+  for (int r = 0; r < RP; ++r) {
+    row[r] = blockIdx.x * (4 * GPW * RP) + (wave * RP + r) * GPW + grp;
+    ok[r] = row[r] < H;
+    if (ok[r] && uok) {
+      load_unit<BD>(td.codes + (size_t)row[r] * BD * U * 4, U, u, wd[r]);
+      sd[r] = *reinterpret_cast<const uint2*>(td.scales + (size_t)row[r] * (I / kBlock) + 4 * u);
+    }
+  }
+
+  for (int m0 = 0; m0 < sl.M; m0 += TM) {
+    const int mc = min(TM, sl.M - m0);
+    __syncthreads();
+    // stage h rows as bfloat16 hi + lo pairs; block sums of hi + lo
+    for (int m = 0; m < mc; ++m) {
+      const float4* src = reinterpret_cast<const float4*>(a.h + (size_t)(sl.base + m0 + m) * I);
+      for (int q = threadIdx.x; q < I / 8; q += 256) {
+        const float4 v0 = src[2 * q], v1 = src[2 * q + 1];
+        const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        uint32_t hi[4], lw[4];
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t h0 = bf16_rne(f[2 * i]), h1 = bf16_rne(f[2 * i + 1]);
+          const uint32_t l0 = bf16_rne(f[2 * i] - __uint_as_float(h0 << 16));
+          const uint32_t l1 = bf16_rne(f[2 * i + 1] - __uint_as_float(h1 << 16));
+          hi[i] = h0 | h1 << 16;
+          lw[i] = l0 | l1 << 16;
+          s += __uint_as_float(h0 << 16) + __uint_as_float(l0 << 16);
+          s += __uint_as_float(h1 << 16) + __uint_as_float(l1 << 16);
+        }
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        const int uu = q >> 4, cq = q & 15;
+        uint32_t* dst = xl + m * xts + uu * kXStride + cq * 4;
+        *reinterpret_cast<u32x4*>(dst) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+        *reinterpret_cast<u32x4*>(dst + lo) = u32x4{lw[0], lw[1], lw[2], lw[3]};
+        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < RP; ++r) opaque(wd[r]);
+    float o[RP][TM];
+#pragma unroll
+    for (int r = 0; r < RP; ++r)
+#pragma unroll
+      for (int m = 0; m < TM; ++m) o[r][m] = 0.0f;
+    if (uok) {
+      const uint32_t* xu = xl + u * kXStride;
+      const float* su4 = xs + u * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int r = 0; r < RP; ++r) {
+          if (!ok[r]) continue;
+          uint32_t p[16];
+          block_pairs<BD>(wd[r] + q * BD, p);
+          const float dd = block_scale<BD>(sd[r], q);
+#pragma unroll
+          for (int m = 0; m < TM; ++m)
+            if (m < mc) o[r][m] = block_dot<2>(p, xu + m * xts + 16 * q, lo, dd, su4[m * sts + q], o[r][m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RP; ++r) {
+      if (!ok[r]) continue;
+#pragma unroll
+      for (int m = 0; m < TM; ++m) {
+        if (m < mc) {
+          const float os = group_sum<LPR>(o[r][m]);
+          if (u == 0) {
+            int prow;
+            float wv;
+            if (sl.shared >= 0) {
+              prow = a.n * a.k + sl.shared * a.n + m0 + m;
+              wv = 1.0f;
+            } else {
+              prow = a.perm[sl.base + m0 + m];
+              wv = a.w[prow];
+            }
+            a.partial[(size_t)prow * H + row[r]] = wv * os;
+          }
+        }
+      }
+    }
+  }
+}
+
+// grid = (row tiles of H, S + max_active), 256 threads
+template <int LPR, int TM, int RP>
+__global__ __launch_bounds__(256) void down_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  Slot sl;
+  if (!slot_info(a, blockIdx.y, sl)) return;
+  const TensorDev td = a.desc[sl.desc * 3 + 2];
+  if (!td.codes) return;
+  switch (td.bits) {
+    case 2: down_body<2, LPR, TM, RP>(a, sl, td, smem); break;
+    case 3: down_body<3, LPR, TM, RP>(a, sl, td, smem); break;
+    case 4: down_body<4, LPR, TM, RP>(a, sl, td, smem); break;
+    default: break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// y_t = sum_j partial(t*k + j) + sum_s partial(n*k + s*n + t), fixed order.
+__global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
+  const int H4 = a.H / 4;
+  const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (long long)a.n * H4) return;
+  const int t = (int)(i / H4), c = (int)(i % H4);
+  const float4* p = reinterpret_cast<const float4*>(a.partial);
+  float4 acc = p[(size_t)(t * a.k) * H4 + c];
+  for (int j = 1; j < a.k; ++j) {
+    const float4 v = p[(size_t)(t * a.k + j) * H4 + c];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  for (int s = 0; s < a.S; ++s) {
+    const float4 v = p[(size_t)(a.n * a.k + s * a.n + t) * H4 + c];
+    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  }
+  reinterpret_cast<float4*>(a.y)[i] = acc;
+}
+
+template <int LPR, int TM>
+hipError_t launch_lpr_tm(const DecodeArgs& a, hipStream_t s) {
+  constexpr int RP = 2;
+  const int slots = a.S + a.max_active;
+  {  // gate/up over rows of I, K = H
+    const int U = a.H / kUnit;
+    const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
+    const int rows_wg = 4 * (64 / LPR) * RP;
+    dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
+    gateup_kernel<LPR, TM, RP><<<grid, 256, lds, s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <int LPR, int TM>
+hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
+  constexpr int RP = 2;
+  const int slots = a.S + a.max_active;
+  const int U = a.I / kUnit;
+  const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
+  const int rows_wg = 4 * (64 / LPR) * RP;
+  dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);
+  down_kernel<LPR, TM, RP><<<grid, 256, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int TM>
+hipError_t launch_gateup_tm(const DecodeArgs& a, hipStream_t s) {
+  const int U = a.H / kUnit;
+  if (U > 32) return launch_lpr_tm<64, TM>(a, s);
+  if (U > 16) return launch_lpr_tm<32, TM>(a, s);
+  return launch_lpr_tm<16, TM>(a, s);
+}
+
+template <int TM>
+hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
+  const int U = a.I / kUnit;
+  if (U > 32) return launch_down_lpr_tm<64, TM>(a, s);
+  if (U > 16) return launch_down_lpr_tm<32, TM>(a, s);
+  return launch_down_lpr_tm<16, TM>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t s) {
+  hipError_t e = a.n == 1 ? launch_gateup_tm<1>(a, s) : launch_gateup_tm<4>(a, s);
+  if (e != hipSuccess) return e;
+  e = a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
+  if (e != hipSuccess) return e;
+  const long long items = (long long)a.n * (a.H / 4);
+  combine_kernel<<<(int)((items + 255) / 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace moeq

@@ -1,0 +1,93 @@
+// Internal declarations shared by the host runtime (api.cpp) and the HIP
+// kernel files.  Not part of the public interface (include/moeq.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "moeq.h"
+
+namespace moeq {
+
+// Weights per device unit: four blocks of 32.  A lane of a GEMV wave owns one
+// unit of a row at a time; hidden and inter must be multiples of this.
+constexpr int kUnit = 128;
+constexpr int kBlock = 32;
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxTopK = 32;
+constexpr int kMaxShared = 4;
+constexpr int kChunk = 64;          // tokens per bucketing chunk (one bit per token in a 64-bit mask)
+constexpr int kDecodeMaxTokens = 64;
+constexpr int kDefaultDecodeMax = 32;
+
+// One stored tensor in the device layout.
+//   codes:  rows * (K/128) units of 16*bits bytes.  Row r's unit u, 16-byte
+//           chunk j lives at byte ((r*bits + j) * U + u) * 16 with U = K/128,
+//           so that chunk j of consecutive units is contiguous (one coalesced
+//           load per wave per chunk).  Inside a unit, block q (q = 0..3) is the
+//           dwords [q*bits, q*bits + bits) of the unit's 4*bits dwords, encoded
+//           as in encode_block() (weights.hip).
+//   scales: row-major [rows x K/32] binary16 (the canonical array, unchanged).
+struct TensorDev {
+  const uint32_t* codes;
+  const uint16_t* scales;
+  int32_t bits;
+  int32_t rows;
+  int32_t K;
+  int32_t pad;
+};
+
+struct RouterParams {
+  const float* logits;    // [n x E]
+  const uint8_t* mask;    // [E] device copy
+  const float* bias;      // [E] device copy (zeros when none was given)
+  int32_t E, G, TG, k, topn, norm;
+  float scale;
+};
+
+// Workspace views (device pointers) for one forward.
+struct Workspace {
+  int32_t* idx;        // [T*k]   chosen experts, token-major
+  float* w;            // [T*k]   combine weights
+  int32_t* offsets;    // [E+1]
+  int32_t* perm;       // [T*k]   bucket order -> t*k + j
+  int32_t* active;     // [1+E]   count, then active expert ids ascending
+  int32_t* chunk_cnt;  // [C*E]   per-chunk counts, then per-chunk bucket bases
+  int32_t* rank;       // [T*k]   rank of an assignment inside its chunk and expert
+  float* h;            // [(T*k + T*S) x I] SwiGLU activations, bucket order then shared
+  float* partial;      // [(T*k + T*S) x H] per-assignment expert outputs, t*k + j then shared
+};
+
+// ---- launchers (return hipSuccess or the launch error) ----
+// route.hip
+hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_in, int n,
+                                     const Workspace& ws, hipStream_t s);
+hipError_t launch_route_tokens(const RouterParams& rp, int n, int32_t* idx, float* w,
+                               hipStream_t s);
+hipError_t launch_bucket_chunked(const int32_t* idx, int n, int k, int E, const Workspace& ws,
+                                 hipStream_t s);
+// weights.hip
+hipError_t launch_repack(const uint8_t* canon_codes, int rows, int K, int bits,
+                         uint32_t* dev_codes, hipStream_t s);
+hipError_t launch_dequant(const TensorDev& t, float* out, hipStream_t s);
+hipError_t launch_quantize(const float* w, int rows, int K, int bits, uint8_t* codes,
+                           uint16_t* scales, hipStream_t s);
+// decode.hip
+struct DecodeArgs {
+  const TensorDev* desc;  // [(E + S) * 3]
+  const uint16_t* x;      // bf16 [n x H]
+  const int32_t* active;
+  const int32_t* offsets;
+  const int32_t* perm;
+  const float* w;
+  float* h;
+  float* partial;
+  float* y;
+  int32_t n, H, I, E, S, k;
+  int32_t max_active;     // routed slots launched: min(n*k, kept experts)
+};
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t s);
+// prefill.hip
+hipError_t launch_prefill(const DecodeArgs& a, hipStream_t s);
+
+}  // namespace moeq

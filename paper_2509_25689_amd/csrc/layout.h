@@ -1,0 +1,128 @@
+// Device layout of the quantized weights and the code-to-bfloat16 unpacking
+// shared by the repack, dequantize and matrix-vector kernels.
+//
+// The value of a weight is d * (c - 2^(b-1)) with a binary16 block scale d
+// and a b-bit code c (the symmetric block format this library uses for the
+// per-tensor low bit widths of Section 3.3).  On the device a row is cut into
+// units of 128 weights (four blocks of 32).  A unit is 4*b dwords; block q of
+// the unit is dwords [q*b, q*b + b), encoded so that two codes -- those of
+// weights 2i and 2i+1 -- sit at the same offset of the low and high 16-bit
+// halves of one dword:
+//
+//   b = 4: dword d (0..3) holds weights 8d..8d+7: weight 8d+2s in bits
+//          [4s, 4s+4), weight 8d+2s+1 in bits [16+4s, 20+4s), s = 0..3
+//   b = 2: dword d (0..1) holds weights 16d..16d+15: weight 16d+2s in bits
+//          [2s, 2s+2), weight 16d+2s+1 in bits [16+2s, 18+2s), s = 0..7
+//   b = 3: dword d (0..2) holds weights 10d..10d+9: weight 10d+2f in bits
+//          [3f, 3f+3), weight 10d+2f+1 in bits [16+3f, 19+3f), f = 0..4;
+//          bit q of weight 30 is bit 15 of dword q, bit q of weight 31 is
+//          bit 31 of dword q (q = 0..2)
+//
+// Unpacking moves a code pair to the top of the 7-bit bfloat16 mantissa and
+// ORs in the exponent of 128 (one shift and one v_and_or_b32 per pair): the
+// dword is then two bfloat16 values 128 + c * 2^(7-b), exact, ready for
+// v_dot2_f32_bf16 against a pair of activations.  Since
+//   sum_i (128 + 2^(7-b) c_i) x_i = 2^(7-b) * sum_i (c_i - z) x_i + 192 * sum_i x_i
+// with z = 2^(b-1), a block's contribution is
+//   d * 2^(b-7) * (dot - 192 * X),     X = sum of the block's 32 activations.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moeq {
+
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t c) { return (a & m) | c; }
+
+constexpr uint32_t kBf16Base = 0x43004300u;  // bfloat16 128.0 in both halves
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// shift a dword left (s > 0) or right (s < 0); s is a compile-time constant
+template <int S>
+__device__ __forceinline__ uint32_t shl(uint32_t v) {
+  if constexpr (S >= 0)
+    return v << S;
+  else
+    return v >> (-S);
+}
+
+// The 16 code pairs of one block (P = pair index = weights 2P, 2P+1), each as
+// two bfloat16 values 128 + c * 2^(7-b).
+template <int B>
+__device__ __forceinline__ void block_pairs(const uint32_t* w, uint32_t (&p)[16]);
+
+template <>
+__device__ __forceinline__ void block_pairs<4>(const uint32_t* w, uint32_t (&p)[16]) {
+  constexpr uint32_t m = 0x00780078u;  // bits [3,7) of each half
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    p[4 * d + 0] = and_or(shl<3>(w[d]), m, kBf16Base);
+    p[4 * d + 1] = and_or(shl<-1>(w[d]), m, kBf16Base);
+    p[4 * d + 2] = and_or(shl<-5>(w[d]), m, kBf16Base);
+    p[4 * d + 3] = and_or(shl<-9>(w[d]), m, kBf16Base);
+  }
+}
+
+template <>
+__device__ __forceinline__ void block_pairs<2>(const uint32_t* w, uint32_t (&p)[16]) {
+  constexpr uint32_t m = 0x00600060u;  // bits [5,7) of each half
+#pragma unroll
+  for (int d = 0; d < 2; ++d) {
+    p[8 * d + 0] = and_or(shl<5>(w[d]), m, kBf16Base);
+    p[8 * d + 1] = and_or(shl<3>(w[d]), m, kBf16Base);
+    p[8 * d + 2] = and_or(shl<1>(w[d]), m, kBf16Base);
+    p[8 * d + 3] = and_or(shl<-1>(w[d]), m, kBf16Base);
+    p[8 * d + 4] = and_or(shl<-3>(w[d]), m, kBf16Base);
+    p[8 * d + 5] = and_or(shl<-5>(w[d]), m, kBf16Base);
+    p[8 * d + 6] = and_or(shl<-7>(w[d]), m, kBf16Base);
+    p[8 * d + 7] = and_or(shl<-9>(w[d]), m, kBf16Base);
+  }
+}
+
+template <>
+__device__ __forceinline__ void block_pairs<3>(const uint32_t* w, uint32_t (&p)[16]) {
+  constexpr uint32_t m = 0x00700070u;  // bits [4,7) of each half
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    p[5 * d + 0] = and_or(shl<4>(w[d]), m, kBf16Base);
+    p[5 * d + 1] = and_or(shl<1>(w[d]), m, kBf16Base);
+    p[5 * d + 2] = and_or(shl<-2>(w[d]), m, kBf16Base);
+    p[5 * d + 3] = and_or(shl<-5>(w[d]), m, kBf16Base);
+    p[5 * d + 4] = and_or(shl<-8>(w[d]), m, kBf16Base);
+  }
+  uint32_t t = and_or(shl<-11>(w[0]), 0x00100010u, kBf16Base);
+  t = and_or(shl<-10>(w[1]), 0x00200020u, t);
+  p[15] = and_or(shl<-9>(w[2]), 0x00400040u, t);
+}
+
+// Load unit u of a row (4*B dwords) with B coalesced 16-byte loads.
+//   row: the row's first dword; U: units per row.
+template <int B>
+__device__ __forceinline__ void load_unit(const uint32_t* row, int U, int u, uint32_t (&w)[4 * B]) {
+  const u32x4* r4 = reinterpret_cast<const u32x4*>(row);
+#pragma unroll
+  for (int j = 0; j < B; ++j) {
+    const u32x4 v = __builtin_nontemporal_load(r4 + (size_t)j * U + u);
+    w[4 * j + 0] = v.x;
+    w[4 * j + 1] = v.y;
+    w[4 * j + 2] = v.z;
+    w[4 * j + 3] = v.w;
+  }
+}
+
+__device__ __forceinline__ float half_to_float(uint32_t h16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h16);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+
+// float -> bfloat16 bits, round to nearest even (finite inputs)
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+}  // namespace moeq

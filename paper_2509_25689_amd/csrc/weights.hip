@@ -1,0 +1,165 @@
+// Weight-format kernels: canonical packing -> device layout (repack), device
+// layout -> float32 (dequantize, a diagnostic that runs the same unpacking as
+// the matrix-vector kernels), and float32 -> canonical packing (quantize).
+//
+// The format is the symmetric block format standing in for the paper's
+// per-tensor low-bit formats (Section 3.3): weight = d * (c - 2^(b-1)), one
+// binary16 scale d per 32 weights, b-bit codes packed least significant bit
+// first within each block.
+#include "internal.h"
+#include "layout.h"
+
+namespace moeq {
+
+namespace {
+
+// codes of one block (32 values < 2^b) -> its b device dwords
+template <int B>
+__device__ void encode_block(const uint8_t* c, uint32_t* w) {
+  for (int d = 0; d < B; ++d) w[d] = 0u;
+  if constexpr (B == 4) {
+    for (int d = 0; d < 4; ++d)
+      for (int s = 0; s < 4; ++s)
+        w[d] |= (uint32_t)c[8 * d + 2 * s] << (4 * s) | (uint32_t)c[8 * d + 2 * s + 1] << (16 + 4 * s);
+  } else if constexpr (B == 2) {
+    for (int d = 0; d < 2; ++d)
+      for (int s = 0; s < 8; ++s)
+        w[d] |= (uint32_t)c[16 * d + 2 * s] << (2 * s) |
+                (uint32_t)c[16 * d + 2 * s + 1] << (16 + 2 * s);
+  } else {
+    for (int d = 0; d < 3; ++d)
+      for (int f = 0; f < 5; ++f)
+        w[d] |= (uint32_t)c[10 * d + 2 * f] << (3 * f) |
+                (uint32_t)c[10 * d + 2 * f + 1] << (16 + 3 * f);
+    for (int q = 0; q < 3; ++q)
+      w[q] |= ((uint32_t)(c[30] >> q) & 1u) << 15 | ((uint32_t)(c[31] >> q) & 1u) << 31;
+  }
+}
+
+// one thread per (row, unit): read 4 canonical blocks, write b 16-byte chunks
+template <int B>
+__global__ __launch_bounds__(256) void repack_kernel(const uint8_t* canon, int rows, int K,
+                                                     uint32_t* dev) {
+  const int U = K / kUnit;
+  const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (long long)rows * U) return;
+  const int r = (int)(gid / U), u = (int)(gid % U);
+  const uint8_t* src = canon + ((size_t)r * (K / kBlock) + 4 * u) * 4 * B;  // 16*B bytes
+  uint8_t c[kUnit];
+  for (int i = 0; i < kUnit; ++i) {
+    const int bit = i * B;
+    const uint32_t lo = src[bit >> 3], hi = (bit >> 3) + 1 < 16 * B ? src[(bit >> 3) + 1] : 0u;
+    c[i] = (uint8_t)(((lo | hi << 8) >> (bit & 7)) & ((1u << B) - 1u));
+  }
+  uint32_t w[4 * B];
+  for (int q = 0; q < 4; ++q) encode_block<B>(c + 32 * q, w + q * B);
+  uint32_t* row = dev + (size_t)r * B * U * 4;
+  for (int j = 0; j < B; ++j)
+    for (int e = 0; e < 4; ++e) row[((size_t)j * U + u) * 4 + e] = w[4 * j + e];
+}
+
+// one thread per (row, unit): the matrix-vector kernels' unpacking, then
+// d * (c - 2^(b-1)) exactly
+template <int B>
+__global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {
+  const int U = t.K / kUnit;
+  const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (long long)t.rows * U) return;
+  const int r = (int)(gid / U), u = (int)(gid % U);
+  uint32_t w[4 * B];
+  load_unit<B>(t.codes + (size_t)r * B * U * 4, U, u, w);
+  const uint16_t* sc = t.scales + (size_t)r * (t.K / kBlock) + 4 * u;
+  const float z = (float)(1 << (B - 1)), unit = (float)(1 << (7 - B));
+  float* o = out + (size_t)r * t.K + kUnit * u;
+  for (int q = 0; q < 4; ++q) {
+    uint32_t p[16];
+    block_pairs<B>(w + q * B, p);
+    const float d = half_to_float(sc[q]);
+    for (int P = 0; P < 16; ++P) {
+      const float c0 = (bf16_lo(p[P]) - 128.0f) / unit, c1 = (bf16_hi(p[P]) - 128.0f) / unit;
+      o[32 * q + 2 * P] = d * (c0 - z);
+      o[32 * q + 2 * P + 1] = d * (c1 - z);
+    }
+  }
+}
+
+// float64 -> binary16 bit pattern, round to nearest even; v >= 0
+__device__ uint16_t half_rne_from_double(double v) {
+  if (!(v > 0.0)) return 0;
+  if (v >= 65520.0) return 0x7C00;  // at or above the midpoint to 2^16: infinity
+  int ex;
+  frexp(v, &ex);
+  int e2 = ex - 1;  // v in [2^e2, 2^(e2+1))
+  if (e2 < -14) return (uint16_t)rint(ldexp(v, 24));  // subnormal, units of 2^-24 (1024 = min normal)
+  double m = rint(ldexp(v, 10 - e2));               // in [1024, 2048]
+  if (m == 2048.0) {
+    m = 1024.0;
+    ++e2;
+  }
+  return (uint16_t)(((e2 + 15) << 10) | ((int)m - 1024));
+}
+
+// one thread per block of 32
+__global__ __launch_bounds__(256) void quantize_kernel(const float* w, int rows, int K, int bits,
+                                                       uint8_t* codes, uint16_t* scales) {
+  const int nb = K / kBlock;
+  const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (long long)rows * nb) return;
+  const float* src = w + gid * kBlock;  // row-major, blocks contiguous
+  float amax = 0.0f;
+  for (int i = 0; i < kBlock; ++i) amax = fmaxf(amax, fabsf(src[i]));
+  const int qm = (1 << (bits - 1)) - 1, z = 1 << (bits - 1);
+  const uint16_t hb = half_rne_from_double((double)amax / (double)qm);
+  scales[gid] = hb;
+  const double d = (double)half_to_float(hb);
+  uint32_t acc[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};  // 32 * bits <= 256 bits
+  for (int i = 0; i < kBlock; ++i) {
+    int q = 0;
+    if (d > 0.0) {
+      const double qq = rint((double)src[i] / d);
+      q = (int)fmin(fmax(qq, (double)-qm), (double)qm);
+    }
+    const uint32_t c = (uint32_t)(q + z);
+    const int bit = i * bits;
+    acc[bit >> 5] |= c << (bit & 31);
+    if ((bit & 31) + bits > 32) acc[(bit >> 5) + 1] |= c >> (32 - (bit & 31));
+  }
+  uint8_t* dst = codes + gid * 4 * bits;
+  for (int i = 0; i < 4 * bits; ++i) dst[i] = (uint8_t)(acc[i >> 2] >> (8 * (i & 3)));
+}
+
+}  // namespace
+
+hipError_t launch_repack(const uint8_t* canon, int rows, int K, int bits, uint32_t* dev,
+                         hipStream_t s) {
+  const long long n = (long long)rows * (K / kUnit);
+  const int grid = (int)((n + 255) / 256);
+  switch (bits) {
+    case 2: repack_kernel<2><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    case 3: repack_kernel<3><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    case 4: repack_kernel<4><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant(const TensorDev& t, float* out, hipStream_t s) {
+  const long long n = (long long)t.rows * (t.K / kUnit);
+  const int grid = (int)((n + 255) / 256);
+  switch (t.bits) {
+    case 2: dequant_kernel<2><<<grid, 256, 0, s>>>(t, out); break;
+    case 3: dequant_kernel<3><<<grid, 256, 0, s>>>(t, out); break;
+    case 4: dequant_kernel<4><<<grid, 256, 0, s>>>(t, out); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize(const float* w, int rows, int K, int bits, uint8_t* codes,
+                           uint16_t* scales, hipStream_t s) {
+  const long long n = (long long)rows * (K / kBlock);
+  quantize_kernel<<<(int)((n + 255) / 256), 256, 0, s>>>(w, rows, K, bits, codes, scales);
+  return hipGetLastError();
+}
+
+}  // namespace moeq

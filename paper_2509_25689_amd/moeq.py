@@ -1,0 +1,257 @@
+"""ctypes binding of the moeq C interface (include/moeq.h).
+
+Argument marshalling only: every step of the layer runs in the HIP library
+``libmoeq.so`` next to this file.  Importing fails loudly when the library has
+not been built; nothing here falls back to another implementation.
+
+The functions keep the C names.  Pointers are plain integers (device or host
+addresses); streams are ``hipStream_t`` values as integers (0 = default).
+``Layer`` is a small convenience wrapper that takes numpy arrays (host weights)
+or torch tensors (device weights / activations) and keeps nothing but the
+handle.
+"""
+import ctypes
+import os
+import re
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoeq.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "moeq.h")
+
+MOEQ_OK = 0
+MOEQ_ERR_INVALID_ARG = -1
+MOEQ_ERR_UNSUPPORTED = -2
+MOEQ_ERR_OUT_OF_MEMORY = -3
+MOEQ_ERR_DEVICE = -4
+MOEQ_ERR_CAPACITY = -5
+STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "OUT_OF_MEMORY",
+                -4: "DEVICE", -5: "CAPACITY"}
+
+MOEQ_PROJ_GATE, MOEQ_PROJ_UP, MOEQ_PROJ_DOWN = 0, 1, 2
+MOEQ_WEIGHTS_HOST, MOEQ_WEIGHTS_DEVICE = 0, 1
+MOEQ_PATH_AUTO, MOEQ_PATH_DECODE, MOEQ_PATH_PREFILL = 0, 1, 2
+
+
+class MoeqError(RuntimeError):
+    def __init__(self, status, message):
+        self.status = status
+        super().__init__(f"moeq {STATUS_NAMES.get(status, status)}: {message}")
+
+
+class moeq_config(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("n_shared", ctypes.c_int32),
+                ("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32),
+                ("top_k", ctypes.c_int32), ("group_topn", ctypes.c_int32),
+                ("norm_topk", ctypes.c_int32), ("routed_scale", ctypes.c_float),
+                ("max_tokens", ctypes.c_int32), ("decode_max_tokens", ctypes.c_int32)]
+
+
+class moeq_qtensor(ctypes.Structure):
+    _fields_ = [("bits", ctypes.c_int32), ("codes", ctypes.c_void_p),
+                ("scales", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+    sig = {
+        "moeq_layer_create": [ctypes.POINTER(moeq_config), P, P, P, P, I32, ctypes.POINTER(P)],
+        "moeq_forward": [P, P, P, I32, P, P],
+        "moeq_destroy": [P],
+        "moeq_last_error": [],
+        "moeq_set_path": [P, I32],
+        "moeq_route": [P, P, I32, P, P, P],
+        "moeq_bucket": [P, P, I32, P, P, P],
+        "moeq_dequant": [P, I32, I32, P, P],
+        "moeq_quantize": [P, I32, I32, I32, P, P, P],
+        "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int32
+    lib.moeq_destroy.restype = None
+    lib.moeq_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+lib = _load()
+
+
+def header_functions():
+    """Names of every function the public header declares."""
+    with open(HEADER_PATH) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:moeq_status|void|const char\*)\s+(moeq_\w+)\s*\(",
+                                 text, re.M)))
+
+
+def moeq_last_error():
+    return lib.moeq_last_error().decode()
+
+
+def _check(status):
+    if status != MOEQ_OK:
+        raise MoeqError(status, moeq_last_error())
+
+
+def moeq_layer_create(cfg, expert_mask, score_bias, routed, shared, weights_location):
+    """cfg: moeq_config; expert_mask/score_bias: host addresses (score_bias may be 0);
+    routed/shared: ctypes arrays of moeq_qtensor (shared may be None).  Returns the handle."""
+    out = ctypes.c_void_p()
+    _check(lib.moeq_layer_create(ctypes.byref(cfg), expert_mask, score_bias or None,
+                                 routed, shared, weights_location, ctypes.byref(out)))
+    return out.value
+
+
+def moeq_forward(layer, x, logits, n_tokens, y, stream=0):
+    _check(lib.moeq_forward(layer, x, logits, n_tokens, y, stream or None))
+
+
+def moeq_destroy(layer):
+    lib.moeq_destroy(layer)
+
+
+def moeq_set_path(layer, path):
+    _check(lib.moeq_set_path(layer, path))
+
+
+def moeq_route(layer, logits, n_tokens, idx, w, stream=0):
+    _check(lib.moeq_route(layer, logits, n_tokens, idx, w, stream or None))
+
+
+def moeq_bucket(layer, idx, n_tokens, offsets, perm, stream=0):
+    _check(lib.moeq_bucket(layer, idx, n_tokens, offsets, perm, stream or None))
+
+
+def moeq_dequant(layer, expert, proj, out, stream=0):
+    _check(lib.moeq_dequant(layer, expert, proj, out, stream or None))
+
+
+def moeq_quantize(w, rows, K, bits, codes, scales, stream=0):
+    _check(lib.moeq_quantize(w, rows, K, bits, codes, scales, stream or None))
+
+
+def moeq_layer_bytes(layer):
+    wb, wsb = ctypes.c_uint64(), ctypes.c_uint64()
+    _check(lib.moeq_layer_bytes(layer, ctypes.byref(wb), ctypes.byref(wsb)))
+    return wb.value, wsb.value
+
+
+# ---------------------------------------------------------------------------
+def make_config(shape, max_tokens, decode_max_tokens=0):
+    """A moeq_config from any object with the layer-shape attribute names."""
+    return moeq_config(shape.hidden, shape.inter, shape.n_experts, shape.n_shared, shape.n_group,
+                       shape.topk_group, shape.top_k, shape.group_topn, shape.norm_topk,
+                       shape.routed_scale, max_tokens, decode_max_tokens)
+
+
+def _addr(a):
+    """Address of a numpy array or torch tensor (0 for None)."""
+    if a is None:
+        return 0
+    if hasattr(a, "data_ptr"):
+        return a.data_ptr()
+    return a.ctypes.data
+
+
+class Layer:
+    """Owns one moeq layer handle.
+
+    routed: dict expert -> (gate, up, down), each a dict with ``bits``,
+    ``codes`` and ``scales`` (numpy arrays for host weights, torch device
+    tensors for device weights); shared: list of such triples."""
+
+    def __init__(self, shape, mask, routed, shared, *, max_tokens, bias=None,
+                 decode_max_tokens=0, device_weights=False):
+        import numpy as np
+        self.shape = shape
+        self.cfg = make_config(shape, max_tokens, decode_max_tokens)
+        self._mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        self._bias = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        E, S = shape.n_experts, shape.n_shared
+        r = (moeq_qtensor * (3 * E))()
+        for e, triple in routed.items():
+            for p, t in enumerate(triple):
+                r[3 * e + p] = moeq_qtensor(int(t["bits"]), _addr(t["codes"]), _addr(t["scales"]))
+        s = (moeq_qtensor * max(1, 3 * S))()
+        for i, triple in enumerate(shared):
+            for p, t in enumerate(triple):
+                s[3 * i + p] = moeq_qtensor(int(t["bits"]), _addr(t["codes"]), _addr(t["scales"]))
+        loc = MOEQ_WEIGHTS_DEVICE if device_weights else MOEQ_WEIGHTS_HOST
+        self.handle = moeq_layer_create(self.cfg, self._mask.ctypes.data,
+                                        0 if self._bias is None else self._bias.ctypes.data,
+                                        r, s if S else None, loc)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            moeq_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @staticmethod
+    def _stream(stream):
+        if stream is not None:
+            return stream
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+
+    def forward(self, x, logits, y=None, stream=None):
+        """x: bf16 CUDA tensor [n, H]; logits: float32 CUDA tensor [n, E] -> y float32 [n, H]."""
+        import torch
+        n = x.shape[0]
+        if y is None:
+            y = torch.empty((n, self.shape.hidden), dtype=torch.float32, device=x.device)
+        moeq_forward(self.handle, x.data_ptr(), logits.data_ptr(), n, y.data_ptr(),
+                     self._stream(stream))
+        return y
+
+    def route(self, logits, stream=None):
+        import torch
+        n = logits.shape[0]
+        idx = torch.empty((n, self.shape.top_k), dtype=torch.int32, device=logits.device)
+        w = torch.empty((n, self.shape.top_k), dtype=torch.float32, device=logits.device)
+        moeq_route(self.handle, logits.data_ptr(), n, idx.data_ptr(), w.data_ptr(),
+                   self._stream(stream))
+        return idx, w
+
+    def bucket(self, idx, stream=None):
+        import torch
+        n = idx.shape[0]
+        offsets = torch.empty(self.shape.n_experts + 1, dtype=torch.int32, device=idx.device)
+        perm = torch.empty(n * self.shape.top_k, dtype=torch.int32, device=idx.device)
+        moeq_bucket(self.handle, idx.data_ptr(), n, offsets.data_ptr(), perm.data_ptr(),
+                    self._stream(stream))
+        return offsets, perm
+
+    def dequant(self, expert, proj, stream=None):
+        import torch
+        rows, K = self.shape.rows_cols(proj)
+        out = torch.empty((rows, K), dtype=torch.float32, device="cuda")
+        moeq_dequant(self.handle, expert, proj, out.data_ptr(), self._stream(stream))
+        return out
+
+    def set_path(self, path):
+        moeq_set_path(self.handle, path)
+
+    def bytes(self):
+        return moeq_layer_bytes(self.handle)
+
+
+def quantize(w, bits, stream=None):
+    """float32 CUDA tensor [rows, K] -> (codes uint8 [rows, K*bits/8], scales int16 [rows, K/32])."""
+    import torch
+    rows, K = w.shape
+    codes = torch.empty((rows, K * bits // 8), dtype=torch.uint8, device=w.device)
+    scales = torch.empty((rows, K // 32), dtype=torch.int16, device=w.device)
+    moeq_quantize(w.data_ptr(), rows, K, bits, codes.data_ptr(), scales.data_ptr(),
+                  stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+    return codes, scales

@@ -1,0 +1,172 @@
+"""The C interface on a machine without a GPU: the library loads, exports every
+function its header declares, and rejects invalid arguments on the host
+before any HIP runtime call."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from inputs import synth
+
+moeq = pytest.importorskip("paper_2509_25689_amd.moeq")
+
+
+def test_exports_every_header_function():
+    names = moeq.header_functions()
+    assert "moeq_layer_create" in names and "moeq_forward" in names and "moeq_destroy" in names
+    for name in names:
+        assert hasattr(moeq.lib, name), name
+
+
+def _cfg(**kw):
+    shape = synth.TINY
+    c = moeq.make_config(shape, max_tokens=8)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def _tensors(E, S, bits=4, codes=1, scales=1):
+    r = (moeq.moeq_qtensor * (3 * E))(*[moeq.moeq_qtensor(bits, codes, scales)] * (3 * E))
+    s = (moeq.moeq_qtensor * max(1, 3 * S))(*[moeq.moeq_qtensor(bits, codes, scales)] * max(1, 3 * S))
+    return r, s
+
+
+def _create(cfg, mask=None, bias=None, bits=4, codes=1, scales=1, loc=0, out=True):
+    E = cfg.n_experts
+    if mask is None:
+        mask = np.ones(max(E, 1), np.uint8)
+    r, s = _tensors(max(E, 1), max(cfg.n_shared, 0), bits, codes, scales)
+    handle = ctypes.c_void_p()
+    st = moeq.lib.moeq_layer_create(ctypes.byref(cfg), mask.ctypes.data,
+                                    None if bias is None else bias.ctypes.data, r, s, loc,
+                                    ctypes.byref(handle) if out else None)
+    return st, handle
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("hidden", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("hidden", 500, moeq.MOEQ_ERR_INVALID_ARG),          # not a multiple of 32
+    ("hidden", 544, moeq.MOEQ_ERR_UNSUPPORTED),          # multiple of 32, not of 128
+    ("inter", 96, moeq.MOEQ_ERR_UNSUPPORTED),
+    ("hidden", 16384, moeq.MOEQ_ERR_UNSUPPORTED),
+    ("n_experts", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("n_experts", 2048, moeq.MOEQ_ERR_INVALID_ARG),
+    ("n_group", 3, moeq.MOEQ_ERR_INVALID_ARG),           # 16 % 3 != 0
+    ("topk_group", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("topk_group", 3, moeq.MOEQ_ERR_INVALID_ARG),        # > n_group
+    ("top_k", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("top_k", 33, moeq.MOEQ_ERR_INVALID_ARG),
+    ("group_topn", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("group_topn", 9, moeq.MOEQ_ERR_INVALID_ARG),        # > experts per group
+    ("norm_topk", 2, moeq.MOEQ_ERR_INVALID_ARG),
+    ("routed_scale", float("nan"), moeq.MOEQ_ERR_INVALID_ARG),
+    ("routed_scale", float("inf"), moeq.MOEQ_ERR_INVALID_ARG),
+    ("n_shared", -1, moeq.MOEQ_ERR_INVALID_ARG),
+    ("n_shared", 5, moeq.MOEQ_ERR_INVALID_ARG),
+    ("max_tokens", 0, moeq.MOEQ_ERR_INVALID_ARG),
+    ("decode_max_tokens", 65, moeq.MOEQ_ERR_INVALID_ARG),
+    ("decode_max_tokens", -1, moeq.MOEQ_ERR_INVALID_ARG),
+])
+def test_config_validation(field, value, status):
+    st, h = _create(_cfg(**{field: value}))
+    assert st == status, moeq.moeq_last_error()
+    assert h.value is None
+    assert moeq.moeq_last_error()
+
+
+@pytest.mark.parametrize("bits,status", [(1, moeq.MOEQ_ERR_INVALID_ARG), (5, moeq.MOEQ_ERR_UNSUPPORTED),
+                                         (6, moeq.MOEQ_ERR_UNSUPPORTED), (8, moeq.MOEQ_ERR_UNSUPPORTED),
+                                         (9, moeq.MOEQ_ERR_INVALID_ARG)])
+def test_bit_width_validation(bits, status):
+    st, _ = _create(_cfg(), bits=bits)
+    assert st == status
+
+
+def test_null_pointers():
+    cfg = _cfg()
+    assert _create(cfg, codes=0)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    assert _create(cfg, scales=0)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    assert _create(cfg, out=False)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    assert moeq.lib.moeq_layer_create(None, None, None, None, None, 0, None) == moeq.MOEQ_ERR_INVALID_ARG
+    h = ctypes.c_void_p()
+    assert moeq.lib.moeq_layer_create(ctypes.byref(cfg), None, None, None, None, 0,
+                                      ctypes.byref(h)) == moeq.MOEQ_ERR_INVALID_ARG
+    assert _create(cfg, loc=7)[0] == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_pruned_expert_tensors_are_not_read():
+    """NULL tensors of a pruned expert are fine; a kept expert with NULL tensors is not.
+
+    Real host buffers back every kept tensor, so on a GPU machine the create
+    succeeds (and the layer is destroyed again)."""
+    shape = synth.TINY
+    cfg = _cfg()
+    bufs = []
+    def qt(p):
+        rows, K = shape.rows_cols(p)
+        c = np.zeros(rows * K // 2, np.uint8)
+        s_ = np.zeros(rows * K // 32, np.uint16)
+        bufs.extend([c, s_])
+        return moeq.moeq_qtensor(4, c.ctypes.data, s_.ctypes.data)
+    r = (moeq.moeq_qtensor * 48)(*[qt(i % 3) for i in range(48)])
+    s = (moeq.moeq_qtensor * 3)(*[qt(i) for i in range(3)])
+    mask = np.ones(16, np.uint8)
+    mask[3] = 0
+    for p in range(3):
+        r[9 + p] = moeq.moeq_qtensor(4, 0, 0)
+    h = ctypes.c_void_p()
+    st = moeq.lib.moeq_layer_create(ctypes.byref(cfg), mask.ctypes.data, None, r, s, 0, ctypes.byref(h))
+    assert st in (moeq.MOEQ_OK, moeq.MOEQ_ERR_DEVICE, moeq.MOEQ_ERR_OUT_OF_MEMORY), moeq.moeq_last_error()
+    if h.value:
+        moeq.lib.moeq_destroy(h)
+    mask[3] = 1
+    st = moeq.lib.moeq_layer_create(ctypes.byref(cfg), mask.ctypes.data, None, r, s, 0, ctypes.byref(h))
+    assert st == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_infeasible_routing_rejected():
+    cfg = _cfg(top_k=5)                              # 2 groups of 8, one group per token
+    mask = np.ones(16, np.uint8)
+    mask[:4] = 0                                     # group 0 keeps 4 < top_k
+    assert _create(cfg, mask=mask)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    mask = np.zeros(16, np.uint8)
+    mask[8:] = 1                                     # one non-empty group, topk_group 2
+    assert _create(_cfg(topk_group=2), mask=mask)[0] == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_bias_validation():
+    bias = np.zeros(16, np.float32)
+    bias[2] = np.nan
+    assert _create(_cfg(), bias=bias)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    bias[2] = 1e31
+    assert _create(_cfg(), bias=bias)[0] == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_entry_points_reject_null_layer():
+    L = moeq.lib
+    assert L.moeq_forward(None, 1, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_route(None, 1, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_bucket(None, 1, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_dequant(None, 0, 0, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_set_path(None, 0) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_layer_bytes(None, None, None) == moeq.MOEQ_ERR_INVALID_ARG
+    L.moeq_destroy(None)                             # NULL-safe
+
+
+def test_quantize_validation():
+    L = moeq.lib
+    assert L.moeq_quantize(None, 1, 32, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_quantize(1, 1, 33, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_quantize(1, -1, 32, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_quantize(1, 1, 32, 8, 1, 1, None) == moeq.MOEQ_ERR_UNSUPPORTED
+    assert L.moeq_quantize(1, 1, 32, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_quantize(1, 0, 32, 4, 1, 1, None) == moeq.MOEQ_OK   # empty: nothing to do
+
+
+def test_error_text_is_per_call():
+    _create(_cfg(top_k=0))
+    assert "top_k" in moeq.moeq_last_error()
+    with pytest.raises(moeq.MoeqError) as ei:
+        moeq.moeq_set_path(None, 0)
+    assert ei.value.status == moeq.MOEQ_ERR_INVALID_ARG
