@@ -55,6 +55,13 @@ class moeq_qtensor(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+    # torch ships its own HIP runtime under the same soname; loading torch first
+    # makes libmoeq.so bind to that one instead of starting a second runtime
+    # in the process (which then sees no device).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
     sig = {
