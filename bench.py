@@ -1,0 +1,315 @@
+#!/usr/bin/env python3
+"""Benchmark: one DeepSeek-V3-shape pruned, mixed-precision MoE layer, decode.
+
+Workload (synthetic, seeded): hidden 7168, expert intermediate 2048, 256 routed
+experts pruned to 192 (r = 0.75), 1 shared expert, sigmoid router with 8
+groups / 4 groups per token / 8 experts per token, routed scale 2.5; routed
+gate/up 3-bit, routed down 4-bit, shared expert 4-bit, blocks of 32 with
+binary16 scales; weights N(0, 0.02) generated on the GPU and quantized by the
+library's quantizer; activations bf16 N(0, 1), router logits fp32 N(0, 1);
+batch 1 (one token per forward).
+
+A step is one full layer forward (route, bucket, gate/up + SwiGLU, down,
+combine) on the next of 64 pre-generated input sets, rotating over 4
+independently seeded layers so that neither the routed experts nor the shared
+expert are served from the 256 MB Infinity Cache between uses.  Steps are
+replayed from a HIP graph; every input is resident in HBM before timing.
+
+Reported: tokens/s (the value), effective weight GB/s per step (codes + scales
+of the distinct tensors each step touches), the dominant kernel's roofline
+(gate/up dequant-GEMV, HBM bound, timed with HIP events recorded by the
+library around each stage), and the CPU oracle on a bounded sample.
+"""
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "V3-shape MoE layer decode tokens/s + effective weight GB/s vs HBM peak"
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=6400)
+    p.add_argument("--warmup", type=int, default=640)
+    p.add_argument("--batch", type=int, default=1)
+    p.add_argument("--layers", type=int, default=4, help="independently seeded layers rotated per step")
+    p.add_argument("--sets", type=int, default=64, help="input sets (x, logits) per layer")
+    p.add_argument("--kernel-steps", type=int, default=256, help="eager forwards timed per stage")
+    p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
+    return p.parse_args()
+
+
+class Hip:
+    """The few HIP runtime calls the benchmark needs for events (torch's runtime)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so.7")
+        for name, args in (("hipEventCreate", [ctypes.POINTER(ctypes.c_void_p)]),
+                           ("hipEventDestroy", [ctypes.c_void_p]),
+                           ("hipEventSynchronize", [ctypes.c_void_p]),
+                           ("hipEventElapsedTime", [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                    ctypes.c_void_p])):
+            getattr(self.lib, name).argtypes = args
+            getattr(self.lib, name).restype = ctypes.c_int
+
+    def event(self):
+        e = ctypes.c_void_p()
+        assert self.lib.hipEventCreate(ctypes.byref(e)) == 0
+        return e.value
+
+    def elapsed_ms(self, a, b):
+        assert self.lib.hipEventSynchronize(b) == 0
+        ms = ctypes.c_float()
+        assert self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def destroy(self, e):
+        self.lib.hipEventDestroy(e)
+
+
+def build_layer(torch, moeq, synth, shape, plan, key, max_tokens):
+    """N(0, 0.02) weights drawn on the GPU (seeded per tensor), quantized by
+    moeq_quantize into the canonical packing, handed over as device pointers."""
+    mask = synth.expert_mask(shape, key)
+    bits_r, bits_s = synth.bit_plan(shape, plan, key)
+    gen = torch.Generator(device="cuda")
+
+    def tensor(kind, e, p, bits):
+        rows, K = shape.rows_cols(p)
+        gen.manual_seed(synth.seed_int("bench-w", key, kind, e, p))
+        w = torch.randn((rows, K), generator=gen, device="cuda", dtype=torch.float32) * 0.02
+        codes, scales = moeq.quantize(w, bits)
+        return dict(bits=bits, codes=codes, scales=scales)
+
+    routed = {int(e): tuple(tensor("r", e, p, int(bits_r[e, p])) for p in range(3))
+              for e in range(shape.n_experts) if mask[e]}
+    shared = [tuple(tensor("s", s, p, int(bits_s[s, p])) for p in range(3)) for s in range(shape.n_shared)]
+    torch.cuda.synchronize()
+    layer = moeq.Layer(shape, mask, routed, shared, max_tokens=max_tokens, device_weights=True)
+    return layer, mask, bits_r, bits_s
+
+
+def tensor_bytes(shape, bits, p):
+    rows, K = shape.rows_cols(p)
+    return rows * K * bits // 8 + rows * (K // 32) * 2
+
+
+def cpu_baseline(shape, steps, batch):
+    """The oracle, as it stands, on `steps` forwards of the same workload shape.
+
+    Inputs: a seeded layer whose touched experts hold random packed codes
+    (the oracle's cost does not depend on code values), seeded x and logits.
+    Timed: routing, bucketing, dequantization of every touched tensor and the
+    float64 expert products and combine -- the whole forward."""
+    import numpy as np
+    from inputs import synth
+    from oracle import bucket, moe, router
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = None
+    key = "bench-cpu"
+    mask = synth.expert_mask(shape, key)
+    bits_r, bits_s = synth.bit_plan(shape, "gu3_d4_sh4", key)
+
+    def packed(kind, e, p):
+        rows, K = shape.rows_cols(p)
+        bits = int(bits_r[e, p] if kind == "r" else bits_s[e, p])
+        codes, scales = synth.random_packed(rows, K, bits, key, kind, e, p)
+        return dict(bits=bits, codes=codes, scales=scales)
+
+    xs = [synth.activations(batch, shape.hidden, key, "x", i) for i in range(steps)]
+    lgs = [synth.normal_logits(batch, shape.n_experts, key, "l", i) for i in range(steps)]
+    # untimed: materialise the packed tensors the sample touches
+    need = set()
+    for lg in lgs:
+        idx, _ = router.route(lg, mask, n_group=shape.n_group, topk_group=shape.topk_group,
+                              top_k=shape.top_k, routed_scale=shape.routed_scale)
+        need |= set(int(e) for e in np.unique(idx))
+    store = {e: tuple(packed("r", e, p) for p in range(3)) for e in need}
+    shared_t = [tuple(packed("s", s, p) for p in range(3)) for s in range(shape.n_shared)]
+    Ks = [shape.rows_cols(p)[1] for p in range(3)]
+
+    t0 = time.perf_counter()
+    for i in range(steps):
+        idx, w = router.route(lgs[i], mask, n_group=shape.n_group, topk_group=shape.topk_group,
+                              top_k=shape.top_k, routed_scale=shape.routed_scale)
+        bucket.bucket(idx, shape.n_experts)
+        shared = [tuple(moe.dequant_tensor(t, K) for t, K in zip(tr, Ks)) for tr in shared_t]
+        moe.moe_forward(xs[i], idx, w,
+                        lambda e: tuple(moe.dequant_tensor(t, K) for t, K in zip(store[e], Ks)), shared)
+    dt = time.perf_counter() - t0
+    cores = len(os.sched_getaffinity(0))
+    return {"value": steps * batch / dt, "unit": "tokens/s",
+            "cores": blas_threads if blas_threads else cores, "kind": "oracle",
+            "sample": f"{steps} forwards of {batch} token(s), same V3 shape and bit plan, "
+                      f"random packed codes; {dt:.1f} s; host cores visible {cores}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(every run uses exactly one MI355X); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from inputs import synth
+    from paper_2509_25689_amd import moeq
+
+    shape = synth.V3
+    B, NL, R = args.batch, args.layers, args.sets
+    hip = Hip()
+    torch.cuda.set_device(0)
+
+    layers = []
+    for li in range(NL):
+        layer, mask, bits_r, bits_s = build_layer(torch, moeq, synth, shape, "gu3_d4_sh4",
+                                                  f"bench-layer-{li}", max_tokens=max(B, 1))
+        layers.append((layer, mask, bits_r, bits_s))
+    resident = sum(L.bytes()[0] for L, *_ in layers)
+
+    # inputs resident in HBM; step s uses layer s % NL and set s % R
+    n_sets = R * NL
+    xs, lgs = [], []
+    for i in range(n_sets):
+        xb = synth.activations(B, shape.hidden, "bench-x", i)
+        xs.append(torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16))
+        lgs.append(torch.from_numpy(synth.normal_logits(B, shape.n_experts, "bench-l", i)).cuda())
+    ys = [torch.empty((B, shape.hidden), device="cuda") for _ in range(NL)]
+
+    # algorithmic bytes of each step: distinct tensors it touches
+    gu_bytes, down_bytes = [], []
+    for i in range(n_sets):
+        layer, mask, bits_r, bits_s = layers[i % NL]
+        idx, _ = layer.route(lgs[i])
+        experts = np.unique(idx.cpu().numpy())
+        g = sum(tensor_bytes(shape, int(bits_r[e, 0]), 0) + tensor_bytes(shape, int(bits_r[e, 1]), 1)
+                for e in experts)
+        d = sum(tensor_bytes(shape, int(bits_r[e, 2]), 2) for e in experts)
+        for s in range(shape.n_shared):
+            g += tensor_bytes(shape, int(bits_s[s, 0]), 0) + tensor_bytes(shape, int(bits_s[s, 1]), 1)
+            d += tensor_bytes(shape, int(bits_s[s, 2]), 2)
+        gu_bytes.append(g)
+        down_bytes.append(d)
+    io_bytes = B * (shape.hidden * 2 + shape.n_experts * 4 + shape.hidden * 4)
+    step_bytes = [g + d + io_bytes for g, d in zip(gu_bytes, down_bytes)]
+
+    def run_step(i, stream):
+        layer = layers[i % NL][0]
+        moeq.moeq_forward(layer.handle, xs[i].data_ptr(), lgs[i].data_ptr(), B,
+                          ys[i % NL].data_ptr(), stream)
+
+    # capture all n_sets steps in one graph (plus one for a remainder)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n_sets):
+            run_step(i, side.cuda_stream)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+
+    def capture(count):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            st = torch.cuda.current_stream().cuda_stream
+            for i in range(count):
+                run_step(i, st)
+        return g
+
+    full = capture(n_sets)
+    rem = args.steps % n_sets
+    part = capture(rem) if rem else None
+
+    def run(steps):
+        for _ in range(steps // n_sets):
+            full.replay()
+        if steps % n_sets:
+            (part if steps % n_sets == rem and part is not None else capture(steps % n_sets)).replay()
+
+    run(args.warmup)
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    run(args.steps)
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_per_step = total_ms / args.steps
+    mean_step_bytes = float(np.mean([step_bytes[i % n_sets] for i in range(args.steps)]))
+
+    # per-stage durations: eager forwards with events recorded by the library
+    KT = args.kernel_steps
+    events = [[hip.event() for _ in range(moeq.MOEQ_STAGE_EVENTS)] for _ in range(KT)]
+    stream = torch.cuda.current_stream().cuda_stream
+    for j in range(KT):
+        layer = layers[j % NL][0]
+        moeq.moeq_set_stage_events(layer.handle, events[j])
+        run_step(j % n_sets, stream)
+    for L, *_ in layers:
+        moeq.moeq_set_stage_events(L.handle, None)
+    torch.cuda.synchronize()
+    stage_ms = np.array([[hip.elapsed_ms(ev[s], ev[s + 1]) for s in range(4)] for ev in events])
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    stage_mean = stage_ms.mean(axis=0)
+    gu_launch_bytes = float(np.mean([gu_bytes[j % n_sets] for j in range(KT)]))
+    down_launch_bytes = float(np.mean([down_bytes[j % n_sets] for j in range(KT)]))
+    gu_gbps = gu_launch_bytes / (stage_mean[1] * 1e-3) / 1e9
+    down_gbps = down_launch_bytes / (stage_mean[2] * 1e-3) / 1e9
+
+    tokens_per_s = args.steps * B / (total_ms * 1e-3)
+    step_gbps = mean_step_bytes / (ms_per_step * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"DeepSeek-V3-shape MoE layer decode, batch {B}: hidden 7168, inter 2048, "
+                        "192 of 256 routed experts kept, 1 shared, 8 groups / top-4 groups / top-8, "
+                        "routed gate/up 3-bit, down 4-bit, shared 4-bit, block 32, fp16 scales",
+            "global_batch": B, "seq_len": 1, "parallelism": "none (1 GPU)",
+            "layers_rotated": NL, "input_sets_per_layer": R, "graph_replay": True,
+            "resident_weight_GB": round(resident / 1e9, 3),
+        },
+        "effective_weight_GBps": round(step_gbps, 1),
+        "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+        "bytes_per_step": int(mean_step_bytes),
+        "stage_us": {"route_bucket": round(stage_mean[0] * 1e3, 2), "gate_up": round(stage_mean[1] * 1e3, 2),
+                     "down": round(stage_mean[2] * 1e3, 2), "combine": round(stage_mean[3] * 1e3, 2)},
+        "down_GBps": round(down_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)",
+                     "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "bytes_per_launch": int(gu_launch_bytes)},
+    }
+    for L, *_ in layers:
+        L.close()
+    if args.cpu_steps > 0:
+        out["cpu_baseline"] = cpu_baseline(shape, args.cpu_steps, B)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

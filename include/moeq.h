@@ -200,6 +200,19 @@ moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits,
 moeq_status moeq_layer_bytes(const moeq_layer* layer, uint64_t* weight_bytes,
                              uint64_t* workspace_bytes);
 
+/* Benchmark instrumentation: stage boundaries of moeq_forward.
+ *   events  NULL (count 0) to stop, or MOEQ_STAGE_EVENTS hipEvent_t handles
+ *           (as void*) owned by the caller.  Every following moeq_forward on
+ *           this layer records, on its stream, events[0] before its first
+ *           kernel, events[1] after routing and bucketing, events[2] after the
+ *           gate/up kernel, events[3] after the down kernel and events[4]
+ *           after the combine, so hipEventElapsedTime between neighbours is
+ *           the duration of one stage.
+ * The handles are copied; the caller keeps them alive while they are set.
+ * Errors: INVALID_ARG (count neither 0 nor MOEQ_STAGE_EVENTS, NULL handle). */
+#define MOEQ_STAGE_EVENTS 5
+moeq_status moeq_set_stage_events(moeq_layer* layer, void* const* events, int32_t count);
+
 #ifdef __cplusplus
 }
 #endif

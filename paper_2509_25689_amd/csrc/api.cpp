@@ -64,6 +64,8 @@ struct moeq_layer {
   float* bias = nullptr;
   void* ws_mem = nullptr;
   Workspace ws{};
+  hipEvent_t stage_events[MOEQ_STAGE_EVENTS] = {};
+  bool timing = false;
 };
 
 namespace {
@@ -376,8 +378,6 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   moeq_status st = check_device(L);
   if (st != MOEQ_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = route_and_bucket(L, logits, n, s);
-  if (e != hipSuccess) return hip_fail(e, "route/bucket launch");
   DecodeArgs a;
   a.desc = L->desc;
   a.x = (const uint16_t*)x;
@@ -398,8 +398,35 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.max_active = (int)(nk < L->n_kept ? nk : L->n_kept);
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
-  e = prefill ? launch_prefill(a, s) : launch_decode(a, s);
-  if (e != hipSuccess) return hip_fail(e, prefill ? "prefill launch" : "decode launch");
+  hipError_t e = hipSuccess;
+  auto mark = [&](int i) {
+    if (L->timing && e == hipSuccess) e = hipEventRecord(L->stage_events[i], s);
+  };
+  mark(0);
+  if (e == hipSuccess) e = route_and_bucket(L, logits, n, s);
+  mark(1);
+  if (e == hipSuccess) e = prefill ? launch_gateup_prefill(a, s) : launch_gateup_decode(a, s);
+  mark(2);
+  if (e == hipSuccess) e = prefill ? launch_down_prefill(a, s) : launch_down_decode(a, s);
+  mark(3);
+  if (e == hipSuccess) e = launch_combine(a, s);
+  mark(4);
+  if (e != hipSuccess) return hip_fail(e, prefill ? "forward (prefill path)" : "forward (decode path)");
+  return ok();
+}
+
+moeq_status moeq_set_stage_events(moeq_layer* L, void* const* events, int32_t count) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (count == 0) {
+    L->timing = false;
+    return ok();
+  }
+  if (count != MOEQ_STAGE_EVENTS || !events)
+    return fail(MOEQ_ERR_INVALID_ARG, "need %d events (got %d)", MOEQ_STAGE_EVENTS, count);
+  for (int i = 0; i < MOEQ_STAGE_EVENTS; ++i)
+    if (!events[i]) return fail(MOEQ_ERR_INVALID_ARG, "event %d is NULL", i);
+  for (int i = 0; i < MOEQ_STAGE_EVENTS; ++i) L->stage_events[i] = (hipEvent_t)events[i];
+  L->timing = true;
   return ok();
 }
 

@@ -365,21 +365,32 @@ __global__ __launch_bounds__(256) void down_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// y_t = sum_j partial(t*k + j) + sum_s partial(n*k + s*n + t), fixed order.
+// y_t = sum_j partial(t*k + j) + sum_s partial(n*k + s*n + t), fixed order;
+// the loads of eight partial rows are issued together.
 __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
   const int H4 = a.H / 4;
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= (long long)a.n * H4) return;
   const int t = (int)(i / H4), c = (int)(i % H4);
   const float4* p = reinterpret_cast<const float4*>(a.partial);
-  float4 acc = p[(size_t)(t * a.k) * H4 + c];
-  for (int j = 1; j < a.k; ++j) {
-    const float4 v = p[(size_t)(t * a.k + j) * H4 + c];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-  }
-  for (int s = 0; s < a.S; ++s) {
-    const float4 v = p[(size_t)(a.n * a.k + s * a.n + t) * H4 + c];
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+  const int rows = a.k + a.S;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int j0 = 0; j0 < rows; j0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int j = j0 + q;
+      if (j < rows) {
+        const size_t r = j < a.k ? (size_t)t * a.k + j : (size_t)a.n * a.k + (size_t)(j - a.k) * a.n + t;
+        v[q] = p[r * H4 + c];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (j0 + q < rows) {
+        acc.x += v[q].x; acc.y += v[q].y; acc.z += v[q].z; acc.w += v[q].w;
+      }
+    }
   }
   reinterpret_cast<float4*>(a.y)[i] = acc;
 }
@@ -430,11 +441,15 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t s) {
-  hipError_t e = a.n == 1 ? launch_gateup_tm<1>(a, s) : launch_gateup_tm<4>(a, s);
-  if (e != hipSuccess) return e;
-  e = a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
-  if (e != hipSuccess) return e;
+hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
+  return a.n == 1 ? launch_gateup_tm<1>(a, s) : launch_gateup_tm<4>(a, s);
+}
+
+hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {
+  return a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
+}
+
+hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {
   const long long items = (long long)a.n * (a.H / 4);
   combine_kernel<<<(int)((items + 255) / 256), 256, 0, s>>>(a);
   return hipGetLastError();

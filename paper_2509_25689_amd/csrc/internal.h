@@ -86,8 +86,11 @@ struct DecodeArgs {
   int32_t n, H, I, E, S, k;
   int32_t max_active;     // routed slots launched: min(n*k, kept experts)
 };
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // prefill.hip
-hipError_t launch_prefill(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s);
 
 }  // namespace moeq

@@ -5,6 +5,8 @@
 
 namespace moeq {
 
-hipError_t launch_prefill(const DecodeArgs& a, hipStream_t s) { return launch_decode(a, s); }
+hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) { return launch_gateup_decode(a, s); }
+
+hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) { return launch_down_decode(a, s); }
 
 }  // namespace moeq

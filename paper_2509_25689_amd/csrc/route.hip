@@ -22,7 +22,8 @@ namespace moeq {
 
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;        // tokens per workgroup of the many-token router
+constexpr int kSmallWaves = 16;  // waves of the small-batch route + bucket workgroup
 
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -36,103 +37,155 @@ __device__ __forceinline__ bool before(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-__device__ __forceinline__ void wave_argmax(float& v, int& i) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    float ov = __shfl_xor(v, off, 64);
-    int oi = __shfl_xor(i, off, 64);
-    if (before(ov, oi, v, i)) {
-      v = ov;
-      i = oi;
-    }
-  }
+// Order-preserving float -> uint32 map; keys compare like the selection
+// order: larger score first, then lower id.  0 = no candidate.
+__device__ __forceinline__ uint32_t ord_f32(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ uint64_t sel_key(float v, int e) {
+  return ((uint64_t)ord_f32(v) << 32) | (uint64_t)(~(uint32_t)e);
 }
 
-// Route token t with the calling wavefront.  s_l / b_l: this wave's LDS rows
-// of E floats; gs_l: G floats.  Writes idx/w for the token to idx_g/w_g
-// (global) and, if idx_s is not null, the ids to idx_s (LDS).
-__device__ void route_token_wave(const RouterParams& rp, int t, float* s_l, float* b_l,
-                                 float* gs_l, int32_t* idx_g, float* w_g, int32_t* idx_s) {
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROW_MASK, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROW_MASK, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum of a 64-bit key over the wavefront, returned to every lane:
+// row prefix maxima (row_shr 1, 2, 4, 8), then row broadcasts into lane 63.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  uint64_t t;
+  t = dpp64<0x111, 0xF>(k); k = t > k ? t : k;
+  t = dpp64<0x112, 0xF>(k); k = t > k ? t : k;
+  t = dpp64<0x114, 0xF>(k); k = t > k ? t : k;
+  t = dpp64<0x118, 0xF>(k); k = t > k ? t : k;
+  t = dpp64<0x142, 0xA>(k); k = t > k ? t : k;   // row_bcast:15
+  t = dpp64<0x143, 0xC>(k); k = t > k ? t : k;   // row_bcast:31
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(k >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Route token t with the calling wavefront.  Lane l owns experts
+// [l*EPL, l*EPL + EPL).  gs_l: this wave's LDS row of >= G floats.  Writes
+// idx/w for the token to idx_g/w_g and, if idx_s is not null, the ids to idx_s.
+template <int EPL>
+__device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
+                                 float* w_g, int32_t* idx_s) {
   const int lane = threadIdx.x & 63;
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
   const float* lg = rp.logits + (size_t)t * E;
-  for (int e = lane; e < E; e += 64) {
-    // sigmoid evaluated in double precision, rounded once to float
-    float s = (float)(1.0 / (1.0 + exp(-(double)lg[e])));
-    if (!(s == s)) s = 0.0f;  // a NaN logit must not leave the index range undefined
-    s_l[e] = s;
-    b_l[e] = rp.mask[e] ? s + rp.bias[e] : -INFINITY;
-  }
-  wave_sync();
-
-  // group scores: lane g sums its group's `topn` best kept scores, best first
-  for (int g = lane; g < G; g += 64) {
-    float acc = 0.0f, pv = INFINITY;
-    int pi = -1, taken = 0;
-    for (int r = 0; r < rp.topn; ++r) {
-      float bv = -INFINITY;
-      int bi = INT_MAX;
-      for (int e = g * per; e < (g + 1) * per; ++e) {
-        float v = b_l[e];
-        if (v == -INFINITY) continue;
-        if (before(pv, pi, v, e) && before(v, e, bv, bi)) {
-          bv = v;
-          bi = e;
-        }
-      }
-      if (bi == INT_MAX) break;
-      acc = acc + bv;
-      ++taken;
-      pv = bv;
-      pi = bi;
+  float s[EPL], b[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane * EPL + i;
+    s[i] = 0.0f;
+    b[i] = -INFINITY;
+    if (e < E) {
+      // sigmoid evaluated in double precision, rounded once to float
+      float v = (float)(1.0 / (1.0 + exp(-(double)lg[e])));
+      if (!(v == v)) v = 0.0f;  // a NaN logit must not leave the index range undefined
+      s[i] = v;
+      if (rp.mask[e]) b[i] = v + rp.bias[e];
     }
-    gs_l[g] = taken ? acc : -INFINITY;
   }
-  wave_sync();
 
-  // group selection, computed redundantly by every lane (G <= 64)
-  uint64_t gsel = 0;
-  for (int r = 0; r < rp.TG; ++r) {
-    float bv = 0.0f;
-    int bi = -1;
+  // ---- group scores: float32 sum of each group's topn best kept scores ----
+  const int lpg = per / EPL;  // lanes per group on the fast path
+  const bool fast = per % EPL == 0 && (lpg & (lpg - 1)) == 0 && rp.topn <= 2;
+  if (fast) {
+    float a = -INFINITY, c = -INFINITY;  // best and second best of this lane
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      if (b[i] > a) {
+        c = a;
+        a = b[i];
+      } else if (b[i] > c) {
+        c = b[i];
+      }
+    }
+    for (int off = 1; off < lpg; off <<= 1) {
+      const float oa = __shfl_xor(a, off, 64), oc = __shfl_xor(c, off, 64);
+      const float lo = fminf(a, oa);
+      a = fmaxf(a, oa);
+      c = fmaxf(lo, fmaxf(c, oc));
+    }
+    float gsc = a;
+    if (rp.topn == 2 && c != -INFINITY) gsc = a + c;  // 0 + a + c in float32, best first
+    if (lane % lpg == 0 && lane / lpg < G) gs_l[lane / lpg] = gsc;
+  } else {
+    // any group size and topn: per group, topn rounds of a wave-wide arg-max
     for (int g = 0; g < G; ++g) {
-      if ((gsel >> g) & 1) continue;
-      float v = gs_l[g];
-      if (bi < 0 || before(v, g, bv, bi)) {
-        bv = v;
-        bi = g;
+      float acc = 0.0f;
+      int taken = 0;
+      uint64_t prev = ~0ull;
+      for (int r = 0; r < rp.topn; ++r) {
+        uint64_t kb = 0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) {
+          const int e = lane * EPL + i;
+          const uint64_t kk = (e < E && e / per == g && b[i] != -INFINITY) ? sel_key(b[i], e) : 0ull;
+          if (kk < prev && kk > kb) kb = kk;
+        }
+        kb = wave_max_key(kb);
+        if (kb == 0) break;
+        const int e = (int)~(uint32_t)kb;
+        float bv = 0.0f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+          if (e % EPL == i) bv = b[i];
+        acc = acc + __shfl(bv, e / EPL, 64);
+        ++taken;
+        prev = kb;
       }
+      if (lane == 0) gs_l[g] = taken ? acc : -INFINITY;
     }
-    gsel |= 1ull << bi;
   }
+  wave_sync();
 
-  // expert selection: k rounds of "best remaining" over the kept experts of
-  // the chosen groups; round r finds the r-th element of the sorted order
-  float pv = INFINITY, sum = 0.0f, my_s = 0.0f;
-  int pi = -1, my_i = 0;
+  // ---- group selection: group g is kept if fewer than TG groups precede it ----
+  bool keep = false;
+  if (lane < G) {
+    const float mine = gs_l[lane];
+    int rank = 0;
+    for (int g = 0; g < G; ++g) rank += before(gs_l[g], g, mine, lane);
+    keep = rank < rp.TG;
+  }
+  const uint64_t gsel = __ballot(keep);
+
+  // ---- expert selection: k rounds of "best key below the previous pick" ----
+  uint64_t key[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane * EPL + i;
+    key[i] = (e < E && b[i] != -INFINITY && ((gsel >> (e / per)) & 1)) ? sel_key(b[i], e) : 0ull;
+  }
+  uint64_t prev = ~0ull;
+  float sum = 0.0f, my_s = 0.0f;
+  int my_i = 0, last = -1;
   for (int r = 0; r < rp.k; ++r) {
-    float bv = -INFINITY;
-    int bi = INT_MAX;
-    for (int e = lane; e < E; e += 64) {
-      if (!((gsel >> (e / per)) & 1)) continue;
-      float v = b_l[e];
-      if (v == -INFINITY) continue;
-      if (before(pv, pi, v, e) && before(v, e, bv, bi)) {
-        bv = v;
-        bi = e;
-      }
-    }
-    wave_argmax(bv, bi);
+    uint64_t kb = 0;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (key[i] < prev && key[i] > kb) kb = key[i];
+    kb = wave_max_key(kb);
     // creation checks guarantee k candidates; never leave the index range
-    if (bi == INT_MAX) bi = pi < 0 ? 0 : pi;
-    const float sv = s_l[bi];
+    const int e = kb ? (int)~(uint32_t)kb : (last < 0 ? 0 : last);
+    float sv = 0.0f;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i)
+      if (e % EPL == i) sv = s[i];
+    sv = __shfl(sv, e / EPL, 64);
     sum = sum + sv;
     if (lane == r) {
-      my_i = bi;
+      my_i = e;
       my_s = sv;
     }
-    pv = bv;
-    pi = bi;
+    if (kb) prev = kb;
+    last = e;
   }
   if (lane < rp.k) {
     float wv;
@@ -144,6 +197,22 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* s_l, floa
     w_g[(size_t)t * rp.k + lane] = wv;
     if (idx_s) idx_s[t * rp.k + lane] = my_i;
   }
+  wave_sync();  // gs_l is reused by this wave's next token
+}
+
+// Route token t, choosing the experts-per-lane instantiation from E.
+__device__ __forceinline__ void route_token(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
+                                           float* w_g, int32_t* idx_s) {
+  if (rp.E <= 64)
+    route_token_wave<1>(rp, t, gs_l, idx_g, w_g, idx_s);
+  else if (rp.E <= 128)
+    route_token_wave<2>(rp, t, gs_l, idx_g, w_g, idx_s);
+  else if (rp.E <= 256)
+    route_token_wave<4>(rp, t, gs_l, idx_g, w_g, idx_s);
+  else if (rp.E <= 512)
+    route_token_wave<8>(rp, t, gs_l, idx_g, w_g, idx_s);
+  else
+    route_token_wave<16>(rp, t, gs_l, idx_g, w_g, idx_s);
 }
 
 // Exclusive scan of cnt[0..E) by one wavefront into off[0..E] (off[E] = total),
@@ -184,12 +253,10 @@ __device__ void wave_scan_experts(const int* cnt, int E, int32_t* off_lds, int32
 }
 
 // ---- small batches (n <= 64): route + bucket in one workgroup ----
-__global__ __launch_bounds__(256) void route_bucket_small_kernel(RouterParams rp,
-                                                                 const int32_t* idx_in, int n,
-                                                                 Workspace ws) {
-  __shared__ float s_l[kWaves][kMaxExperts];
-  __shared__ float b_l[kWaves][kMaxExperts];
-  __shared__ float gs_l[kWaves][64];
+__global__ __launch_bounds__(1024) void route_bucket_small_kernel(RouterParams rp,
+                                                                  const int32_t* idx_in, int n,
+                                                                  Workspace ws) {
+  __shared__ float gs_l[kSmallWaves][64];
   __shared__ int32_t idx_l[kDecodeMaxTokens * kMaxTopK];
   __shared__ unsigned long long emask[kMaxExperts];
   __shared__ int32_t cnt[kMaxExperts];
@@ -197,23 +264,22 @@ __global__ __launch_bounds__(256) void route_bucket_small_kernel(RouterParams rp
 
   const int tid = threadIdx.x, wave = tid >> 6;
   const int E = rp.E, k = rp.k, nk = n * k;
-  for (int e = tid; e < E; e += 256) emask[e] = 0ull;
+  for (int e = tid; e < E; e += 1024) emask[e] = 0ull;
   if (idx_in) {
-    for (int a = tid; a < nk; a += 256) idx_l[a] = idx_in[a];
+    for (int a = tid; a < nk; a += 1024) idx_l[a] = idx_in[a];
   } else {
-    for (int t = wave; t < n; t += kWaves)
-      route_token_wave(rp, t, s_l[wave], b_l[wave], gs_l[wave], ws.idx, ws.w, idx_l);
+    for (int t = wave; t < n; t += kSmallWaves) route_token(rp, t, gs_l[wave], ws.idx, ws.w, idx_l);
   }
   __syncthreads();
   // ids outside [0, E) (possible only for caller-provided ids) are ignored
-  for (int a = tid; a < nk; a += 256)
+  for (int a = tid; a < nk; a += 1024)
     if ((unsigned)idx_l[a] < (unsigned)E) atomicOr(&emask[idx_l[a]], 1ull << (a / k));
   __syncthreads();
-  for (int e = tid; e < E; e += 256) cnt[e] = __popcll(emask[e]);
+  for (int e = tid; e < E; e += 1024) cnt[e] = __popcll(emask[e]);
   __syncthreads();
   if (wave == 0) wave_scan_experts(cnt, E, off, ws.offsets, ws.active);
   __syncthreads();
-  for (int a = tid; a < nk; a += 256) {
+  for (int a = tid; a < nk; a += 1024) {
     const int e = idx_l[a], t = a / k;
     if ((unsigned)e >= (unsigned)E) continue;
     const unsigned long long below = (t == 0) ? 0ull : (emask[e] & ((1ull << t) - 1ull));
@@ -224,12 +290,10 @@ __global__ __launch_bounds__(256) void route_bucket_small_kernel(RouterParams rp
 // ---- large batches: one token per wavefront ----
 __global__ __launch_bounds__(256) void route_tokens_kernel(RouterParams rp, int n, int32_t* idx,
                                                            float* w) {
-  __shared__ float s_l[kWaves][kMaxExperts];
-  __shared__ float b_l[kWaves][kMaxExperts];
   __shared__ float gs_l[kWaves][64];
   const int wave = threadIdx.x >> 6;
   const int t = blockIdx.x * kWaves + wave;
-  if (t < n) route_token_wave(rp, t, s_l[wave], b_l[wave], gs_l[wave], idx, w, nullptr);
+  if (t < n) route_token(rp, t, gs_l[wave], idx, w, nullptr);
 }
 
 // chunk c = tokens [64c, 64c+64): per-expert counts and in-chunk ranks
@@ -288,7 +352,7 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const int32_t* idx,
 
 hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_in, int n,
                                      const Workspace& ws, hipStream_t s) {
-  route_bucket_small_kernel<<<1, 256, 0, s>>>(rp, idx_in, n, ws);
+  route_bucket_small_kernel<<<1, 1024, 0, s>>>(rp, idx_in, n, ws);
   return hipGetLastError();
 }
 

@@ -75,6 +75,7 @@ def _load():
         "moeq_dequant": [P, I32, I32, P, P],
         "moeq_quantize": [P, I32, I32, I32, P, P, P],
         "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
+        "moeq_set_stage_events": [P, ctypes.POINTER(P), I32],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -140,6 +141,18 @@ def moeq_dequant(layer, expert, proj, out, stream=0):
 
 def moeq_quantize(w, rows, K, bits, codes, scales, stream=0):
     _check(lib.moeq_quantize(w, rows, K, bits, codes, scales, stream or None))
+
+
+MOEQ_STAGE_EVENTS = 5
+
+
+def moeq_set_stage_events(layer, events):
+    """events: sequence of MOEQ_STAGE_EVENTS hipEvent_t handles (ints), or None to stop."""
+    if not events:
+        _check(lib.moeq_set_stage_events(layer, None, 0))
+        return
+    arr = (ctypes.c_void_p * len(events))(*events)
+    _check(lib.moeq_set_stage_events(layer, arr, len(events)))
 
 
 def moeq_layer_bytes(layer):
