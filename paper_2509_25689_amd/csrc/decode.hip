@@ -36,6 +36,33 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against LDS bank conflicts
 
+// Pipeline shape: each wave walks kGateUpSteps (kDownSteps) row steps with
+// kGateUpBuf (kDownBuf) register buffers, i.e. NBUF - 1 steps of codes in
+// flight while one is reduced; MinBlocks bounds registers for occupancy.
+#ifndef MOEQ_GATEUP_STEPS
+#define MOEQ_GATEUP_STEPS 4
+#endif
+#ifndef MOEQ_GATEUP_BUF
+#define MOEQ_GATEUP_BUF 1
+#endif
+#ifndef MOEQ_DOWN_STEPS
+#define MOEQ_DOWN_STEPS 4
+#endif
+#ifndef MOEQ_DOWN_BUF
+#define MOEQ_DOWN_BUF 1
+#endif
+#ifndef MOEQ_GATEUP_MINBLOCKS
+#define MOEQ_GATEUP_MINBLOCKS 4
+#endif
+#ifndef MOEQ_DOWN_MINBLOCKS
+#define MOEQ_DOWN_MINBLOCKS 4
+#endif
+constexpr int kGateUpSteps = MOEQ_GATEUP_STEPS, kGateUpBuf = MOEQ_GATEUP_BUF;
+static_assert(MOEQ_GATEUP_STEPS % MOEQ_GATEUP_BUF == 0 && MOEQ_DOWN_STEPS % MOEQ_DOWN_BUF == 0,
+              "steps per wave must be a multiple of the pipeline depth");
+constexpr int kDownSteps = MOEQ_DOWN_STEPS, kDownBuf = MOEQ_DOWN_BUF;
+constexpr int kGateUpMinBlocks = MOEQ_GATEUP_MINBLOCKS, kDownMinBlocks = MOEQ_DOWN_MINBLOCKS;
+
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
                                          __builtin_bit_cast(bf16x2, b), c, false);
@@ -99,32 +126,86 @@ __device__ __forceinline__ float block_dot(const uint32_t (&p)[16], const uint32
 
 // block q's scale (binary16, 4 per unit in sc) times 2^(b-7)
 template <int B>
-__device__ __forceinline__ float block_scale(uint2 sc, int q) {
+__device__ __forceinline__ float block_scale(u32x2 sc, int q) {
   const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
   return half_to_float(s16) * (1.0f / (float)(1 << (7 - B)));
 }
 
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
+
+// Sum over a group of LPR lanes (16, 32 or 64) with DPP adds in a fixed order:
+// quad butterflies, row rotations, then row broadcasts.  The group's last
+// lane holds the total.
 template <int LPR>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int off = LPR / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x124>(v);  // row_ror:4
+  v += dpp_f<0x128>(v);  // row_ror:8
+  if constexpr (LPR >= 32) v += dpp_f<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
+  if constexpr (LPR >= 64) v += dpp_f<0x143, 0xC>(v);  // row_bcast:31 into rows 2, 3
   return v;
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
-// An empty asm statement that "modifies" the registers: keeps the compiler
-// from hoisting the per-chunk unpacking of loop-invariant weights out of the
-// token-chunk loop (which would hold every unpacked pair in registers).
-template <int N>
-__device__ __forceinline__ void opaque(uint32_t (&v)[N]) {
-#pragma unroll
-  for (int i = 0; i < N; ++i) asm volatile("" : "+v"(v[i]));
+// ---------------------------------------------------------------------------
+// gate/up + SwiGLU for one (slot, row tile), gate/up widths BG/BU.  Each wave
+// owns RW consecutive row steps (GPW rows each) and walks them with two
+// register buffers: the codes of step i+1 are in flight while step i is
+// reduced, so every wave keeps HBM requests outstanding.
+template <int BG, int BU>
+struct GateUpRows {
+  uint32_t wg[4 * BG], wu[4 * BU];
+  u32x2 sg, su;
+};
+
+template <int BG, int BU>
+__device__ __forceinline__ void load_gateup(GateUpRows<BG, BU>& b, const TensorDev& tg, const TensorDev& tu,
+                                            int row, int U, int u, int H) {
+  load_unit<BG>(tg.codes + (size_t)row * BG * U * 4, U, u, b.wg);
+  load_unit<BU>(tu.codes + (size_t)row * BU * U * 4, U, u, b.wu);
+  b.sg = *gptr(reinterpret_cast<const u32x2*>(tg.scales + (size_t)row * (H / kBlock) + 4 * u));
+  b.su = *gptr(reinterpret_cast<const u32x2*>(tu.scales + (size_t)row * (H / kBlock) + 4 * u));
 }
 
-// ---------------------------------------------------------------------------
-// gate/up + SwiGLU for one (slot, row tile), gate/up widths BG/BU.
-template <int BG, int BU, int LPR, int TM, int RP>
+template <int BG, int BU, int LPR, int TM>
+__device__ __forceinline__ void compute_gateup(const GateUpRows<BG, BU>& b, bool active, const uint32_t* xu,
+                                               const float* su4, int xts, int sts, int mc, int u,
+                                               int hrow0, int row, const DecodeArgs& a) {
+  float g[TM], up[TM];
+#pragma unroll
+  for (int m = 0; m < TM; ++m) g[m] = up[m] = 0.0f;
+  if (active) {
+    const PairConsts pk = pair_consts();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t p[16];
+      block_pairs<BG>(b.wg + q * BG, pk, p);
+      const float dg = block_scale<BG>(b.sg, q);
+#pragma unroll
+      for (int m = 0; m < TM; ++m)
+        if (m < mc) g[m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, dg, su4[m * sts + q], g[m]);
+      block_pairs<BU>(b.wu + q * BU, pk, p);
+      const float du = block_scale<BU>(b.su, q);
+#pragma unroll
+      for (int m = 0; m < TM; ++m)
+        if (m < mc) up[m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, du, su4[m * sts + q], up[m]);
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < TM; ++m) {
+    if (m < mc) {
+      const float gs = group_sum<LPR>(g[m]), us = group_sum<LPR>(up[m]);
+      if (u == LPR - 1) a.h[(size_t)(hrow0 + m) * a.I + row] = silu(gs) * us;
+    }
+  }
+}
+
+template <int BG, int BU, int LPR, int TM, int RW, int NBUF>
 __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl, const TensorDev& tg,
                                             const TensorDev& tu, uint32_t* smem) {
   const int H = a.H, I = a.I, U = H / kUnit;
@@ -136,29 +217,20 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl,
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane / LPR, u = lane % LPR;
   const bool uok = u < U;
-  int row[RP];
-  bool ok[RP];
-  uint32_t wg[RP][4 * BG], wu[RP][4 * BU];
-  uint2 sg[RP], su[RP];
-#pragma unroll
-  for (int r = 0; r < RP; ++r) {
-    row[r] = blockIdx.x * (4 * GPW * RP) + (wave * RP + r) * GPW + grp;
-    ok[r] = row[r] < I;
-    if (ok[r] && uok) {
-      load_unit<BG>(tg.codes + (size_t)row[r] * BG * U * 4, U, u, wg[r]);
-      load_unit<BU>(tu.codes + (size_t)row[r] * BU * U * 4, U, u, wu[r]);
-      sg[r] = *reinterpret_cast<const uint2*>(tg.scales + (size_t)row[r] * (H / kBlock) + 4 * u);
-      su[r] = *reinterpret_cast<const uint2*>(tu.scales + (size_t)row[r] * (H / kBlock) + 4 * u);
-    }
-  }
+  const int row0 = blockIdx.x * (4 * GPW * RW) + wave * (GPW * RW) + grp;  // + step * GPW
 
+  GateUpRows<BG, BU> buf[NBUF];
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
     const int mc = min(TM, sl.M - m0);
+    asm volatile("" ::: "memory");  // weight loads stay inside the chunk loop
+#pragma unroll
+    for (int st = 0; st < NBUF - 1; ++st)
+      if (st < RW && uok && row0 + st * GPW < I) load_gateup(buf[st], tg, tu, row0 + st * GPW, U, u, H);
     __syncthreads();
     // stage the chunk's x rows: 16-byte pieces, 4 per block of 32
     for (int m = 0; m < mc; ++m) {
       const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
-      const u32x4* src = reinterpret_cast<const u32x4*>(a.x + (size_t)t * H);
+      const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
       for (int q = threadIdx.x; q < H / 8; q += 256) {
         const u32x4 v = src[q];
         float s = 0.0f;
@@ -172,77 +244,101 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl,
       }
     }
     __syncthreads();
+    const uint32_t* xu = xl + u * kXStride;
+    const float* su4 = xs + u * 4;
+    // groups of NBUF steps: buffer indices are static inside a group
+#pragma unroll 1
+    for (int g0 = 0; g0 < RW; g0 += NBUF) {
+      asm volatile("" ::: "memory");
 #pragma unroll
-    for (int r = 0; r < RP; ++r) {
-      opaque(wg[r]);
-      opaque(wu[r]);
-    }
-    float g[RP][TM], up[RP][TM];
-#pragma unroll
-    for (int r = 0; r < RP; ++r)
-#pragma unroll
-      for (int m = 0; m < TM; ++m) g[r][m] = up[r][m] = 0.0f;
-    if (uok) {
-      const uint32_t* xu = xl + u * kXStride;
-      const float* su4 = xs + u * 4;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-#pragma unroll
-        for (int r = 0; r < RP; ++r) {
-          if (!ok[r]) continue;
-          uint32_t p[16];
-          block_pairs<BG>(wg[r] + q * BG, p);
-          const float dg = block_scale<BG>(sg[r], q);
-#pragma unroll
-          for (int m = 0; m < TM; ++m)
-            if (m < mc) g[r][m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, dg, su4[m * sts + q], g[r][m]);
-          block_pairs<BU>(wu[r] + q * BU, p);
-          const float du = block_scale<BU>(su[r], q);
-#pragma unroll
-          for (int m = 0; m < TM; ++m)
-            if (m < mc) up[r][m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, du, su4[m * sts + q], up[r][m]);
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < RP; ++r) {
-      if (!ok[r]) continue;  // uniform across the lane group
-#pragma unroll
-      for (int m = 0; m < TM; ++m) {
-        if (m < mc) {
-          const float gs = group_sum<LPR>(g[r][m]), us = group_sum<LPR>(up[r][m]);
-          if (u == 0) a.h[(size_t)(sl.base + m0 + m) * I + row[r]] = silu(gs) * us;
-        }
+      for (int b = 0; b < NBUF; ++b) {
+        const int st = g0 + b;
+        const int rn = row0 + (st + NBUF - 1) * GPW;
+        if (st + NBUF - 1 < RW && uok && rn < I) load_gateup(buf[(b + NBUF - 1) % NBUF], tg, tu, rn, U, u, H);
+        const int r = row0 + st * GPW;
+        if (r < I) compute_gateup<BG, BU, LPR, TM>(buf[b], uok, xu, su4, xts, sts, mc, u, sl.base + m0, r, a);
       }
     }
   }
 }
 
 // grid = (row tiles of I, S + max_active), 256 threads
-template <int LPR, int TM, int RP>
-__global__ __launch_bounds__(256) void gateup_kernel(DecodeArgs a) {
+template <int LPR, int TM, int RW, int NBUF>
+__global__ __launch_bounds__(256, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   Slot sl;
   if (!slot_info(a, blockIdx.y, sl)) return;
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   switch (tg.bits * 8 + tu.bits) {
-    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RP>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RP>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
     default: break;
   }
 }
 
 // ---------------------------------------------------------------------------
-// down x routing weight for one (slot, row tile), down width BD.
-template <int BD, int LPR, int TM, int RP>
+// down x routing weight for one (slot, row tile), down width BD; the same
+// two-buffer walk over each wave's row steps.
+template <int BD>
+struct DownRows {
+  uint32_t w[4 * BD];
+  u32x2 s;
+};
+
+template <int BD>
+__device__ __forceinline__ void load_down(DownRows<BD>& b, const TensorDev& td, int row, int U, int u, int I) {
+  load_unit<BD>(td.codes + (size_t)row * BD * U * 4, U, u, b.w);
+  b.s = *gptr(reinterpret_cast<const u32x2*>(td.scales + (size_t)row * (I / kBlock) + 4 * u));
+}
+
+template <int BD, int LPR, int TM>
+__device__ __forceinline__ void compute_down(const DownRows<BD>& b, bool active, const uint32_t* xu,
+                                             const float* su4, int xts, int sts, int lo, int mc, int u,
+                                             const Slot& sl, int m0, int row, const DecodeArgs& a) {
+  float o[TM];
+#pragma unroll
+  for (int m = 0; m < TM; ++m) o[m] = 0.0f;
+  if (active) {
+    const PairConsts pk = pair_consts();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t p[16];
+      block_pairs<BD>(b.w + q * BD, pk, p);
+      const float dd = block_scale<BD>(b.s, q);
+#pragma unroll
+      for (int m = 0; m < TM; ++m)
+        if (m < mc) o[m] = block_dot<2>(p, xu + m * xts + 16 * q, lo, dd, su4[m * sts + q], o[m]);
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < TM; ++m) {
+    if (m < mc) {
+      const float os = group_sum<LPR>(o[m]);
+      if (u == LPR - 1) {
+        int prow;
+        float wv;
+        if (sl.shared >= 0) {
+          prow = a.n * a.k + sl.shared * a.n + m0 + m;
+          wv = 1.0f;
+        } else {
+          prow = a.perm[sl.base + m0 + m];
+          wv = a.w[prow];
+        }
+        a.partial[(size_t)prow * a.H + row] = wv * os;
+      }
+    }
+  }
+}
+
+template <int BD, int LPR, int TM, int RW, int NBUF>
 __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, const TensorDev& td,
                                           uint32_t* smem) {
   const int H = a.H, I = a.I, U = I / kUnit;
@@ -254,28 +350,21 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, c
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane / LPR, u = lane % LPR;
   const bool uok = u < U;
-  int row[RP];
-  bool ok[RP];
-  uint32_t wd[RP][4 * BD];
-  uint2 sd[RP];
-#pragma unroll
-  for (int r = 0; r < RP; ++r) {
-    row[r] = blockIdx.x * (4 * GPW * RP) + (wave * RP + r) * GPW + grp;
-    ok[r] = row[r] < H;
-    if (ok[r] && uok) {
-      load_unit<BD>(td.codes + (size_t)row[r] * BD * U * 4, U, u, wd[r]);
-      sd[r] = *reinterpret_cast<const uint2*>(td.scales + (size_t)row[r] * (I / kBlock) + 4 * u);
-    }
-  }
+  const int row0 = blockIdx.x * (4 * GPW * RW) + wave * (GPW * RW) + grp;  // + step * GPW
 
+  DownRows<BD> buf[NBUF];
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
     const int mc = min(TM, sl.M - m0);
+    asm volatile("" ::: "memory");  // weight loads stay inside the chunk loop
+#pragma unroll
+    for (int st = 0; st < NBUF - 1; ++st)
+      if (st < RW && uok && row0 + st * GPW < H) load_down(buf[st], td, row0 + st * GPW, U, u, I);
     __syncthreads();
     // stage h rows as bfloat16 hi + lo pairs; block sums of hi + lo
     for (int m = 0; m < mc; ++m) {
-      const float4* src = reinterpret_cast<const float4*>(a.h + (size_t)(sl.base + m0 + m) * I);
+      const MOEQ_GLOBAL f32x4* src = gptr(reinterpret_cast<const f32x4*>(a.h + (size_t)(sl.base + m0 + m) * I));
       for (int q = threadIdx.x; q < I / 8; q += 256) {
-        const float4 v0 = src[2 * q], v1 = src[2 * q + 1];
+        const f32x4 v0 = src[2 * q], v1 = src[2 * q + 1];
         const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
         uint32_t hi[4], lw[4];
         float s = 0.0f;
@@ -299,67 +388,36 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, c
       }
     }
     __syncthreads();
+    const uint32_t* xu = xl + u * kXStride;
+    const float* su4 = xs + u * 4;
+    // groups of NBUF steps: buffer indices are static inside a group
+#pragma unroll 1
+    for (int g0 = 0; g0 < RW; g0 += NBUF) {
+      asm volatile("" ::: "memory");
 #pragma unroll
-    for (int r = 0; r < RP; ++r) opaque(wd[r]);
-    float o[RP][TM];
-#pragma unroll
-    for (int r = 0; r < RP; ++r)
-#pragma unroll
-      for (int m = 0; m < TM; ++m) o[r][m] = 0.0f;
-    if (uok) {
-      const uint32_t* xu = xl + u * kXStride;
-      const float* su4 = xs + u * 4;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-#pragma unroll
-        for (int r = 0; r < RP; ++r) {
-          if (!ok[r]) continue;
-          uint32_t p[16];
-          block_pairs<BD>(wd[r] + q * BD, p);
-          const float dd = block_scale<BD>(sd[r], q);
-#pragma unroll
-          for (int m = 0; m < TM; ++m)
-            if (m < mc) o[r][m] = block_dot<2>(p, xu + m * xts + 16 * q, lo, dd, su4[m * sts + q], o[r][m]);
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < RP; ++r) {
-      if (!ok[r]) continue;
-#pragma unroll
-      for (int m = 0; m < TM; ++m) {
-        if (m < mc) {
-          const float os = group_sum<LPR>(o[r][m]);
-          if (u == 0) {
-            int prow;
-            float wv;
-            if (sl.shared >= 0) {
-              prow = a.n * a.k + sl.shared * a.n + m0 + m;
-              wv = 1.0f;
-            } else {
-              prow = a.perm[sl.base + m0 + m];
-              wv = a.w[prow];
-            }
-            a.partial[(size_t)prow * H + row[r]] = wv * os;
-          }
-        }
+      for (int b = 0; b < NBUF; ++b) {
+        const int st = g0 + b;
+        const int rn = row0 + (st + NBUF - 1) * GPW;
+        if (st + NBUF - 1 < RW && uok && rn < H) load_down(buf[(b + NBUF - 1) % NBUF], td, rn, U, u, I);
+        const int r = row0 + st * GPW;
+        if (r < H) compute_down<BD, LPR, TM>(buf[b], uok, xu, su4, xts, sts, lo, mc, u, sl, m0, r, a);
       }
     }
   }
 }
 
 // grid = (row tiles of H, S + max_active), 256 threads
-template <int LPR, int TM, int RP>
-__global__ __launch_bounds__(256) void down_kernel(DecodeArgs a) {
+template <int LPR, int TM, int RW, int NBUF>
+__global__ __launch_bounds__(256, TM == 1 ? kDownMinBlocks : 2) void down_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   Slot sl;
   if (!slot_info(a, blockIdx.y, sl)) return;
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
   switch (td.bits) {
-    case 2: down_body<2, LPR, TM, RP>(a, sl, td, smem); break;
-    case 3: down_body<3, LPR, TM, RP>(a, sl, td, smem); break;
-    case 4: down_body<4, LPR, TM, RP>(a, sl, td, smem); break;
+    case 2: down_body<2, LPR, TM, RW, NBUF>(a, sl, td, smem); break;
+    case 3: down_body<3, LPR, TM, RW, NBUF>(a, sl, td, smem); break;
+    case 4: down_body<4, LPR, TM, RW, NBUF>(a, sl, td, smem); break;
     default: break;
   }
 }
@@ -395,40 +453,37 @@ __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
   reinterpret_cast<float4*>(a.y)[i] = acc;
 }
 
+// Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
+// rows of one slot.
+
 template <int LPR, int TM>
-hipError_t launch_lpr_tm(const DecodeArgs& a, hipStream_t s) {
-  constexpr int RP = 2;
+hipError_t launch_gateup_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const int slots = a.S + a.max_active;
-  {  // gate/up over rows of I, K = H
-    const int U = a.H / kUnit;
-    const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
-    const int rows_wg = 4 * (64 / LPR) * RP;
-    dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
-    gateup_kernel<LPR, TM, RP><<<grid, 256, lds, s>>>(a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
+  const int U = a.H / kUnit;
+  const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
+  const int rows_wg = 4 * (64 / LPR) * kGateUpSteps;
+  dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
+  gateup_kernel<LPR, TM, kGateUpSteps, kGateUpBuf><<<grid, 256, lds, s>>>(a);
+  return hipGetLastError();
 }
 
 template <int LPR, int TM>
 hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
-  constexpr int RP = 2;
   const int slots = a.S + a.max_active;
   const int U = a.I / kUnit;
   const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
-  const int rows_wg = 4 * (64 / LPR) * RP;
+  const int rows_wg = 4 * (64 / LPR) * kDownSteps;
   dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);
-  down_kernel<LPR, TM, RP><<<grid, 256, lds, s>>>(a);
+  down_kernel<LPR, TM, kDownSteps, kDownBuf><<<grid, 256, lds, s>>>(a);
   return hipGetLastError();
 }
 
 template <int TM>
 hipError_t launch_gateup_tm(const DecodeArgs& a, hipStream_t s) {
   const int U = a.H / kUnit;
-  if (U > 32) return launch_lpr_tm<64, TM>(a, s);
-  if (U > 16) return launch_lpr_tm<32, TM>(a, s);
-  return launch_lpr_tm<16, TM>(a, s);
+  if (U > 32) return launch_gateup_lpr_tm<64, TM>(a, s);
+  if (U > 16) return launch_gateup_lpr_tm<32, TM>(a, s);
+  return launch_gateup_lpr_tm<16, TM>(a, s);
 }
 
 template <int TM>

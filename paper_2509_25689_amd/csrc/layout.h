@@ -32,11 +32,46 @@
 
 namespace moeq {
 
-__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t c) { return (a & m) | c; }
-
 constexpr uint32_t kBf16Base = 0x43004300u;  // bfloat16 128.0 in both halves
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Global (not generic) address space: pointers read from the descriptor
+// table would otherwise become flat loads, which also count against the LDS
+// wait counter and serialize HBM streaming with LDS reads.
+#define MOEQ_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const MOEQ_GLOBAL T* gptr(const T* p) {
+  return (const MOEQ_GLOBAL T*)p;
+}
+
+// (a & m) | c as one v_and_or_b32.  gfx9 VOP3 cannot encode literals, so the
+// constants are passed in VGPRs (see the masks below) and the instruction is
+// written out; the compiler otherwise splits it into v_and + v_or.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t c) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(m), "v"(c));
+  return r;
+}
+
+// Masks and the bfloat16 base held in registers for and_or.
+struct PairConsts {
+  uint32_t base, m2, m3, m4, b30, b31, b32;
+};
+__device__ __forceinline__ PairConsts pair_consts() {
+  PairConsts k;
+  // opaque moves keep the constants in VGPRs
+  asm("v_mov_b32 %0, 0x43004300" : "=v"(k.base));
+  asm("v_mov_b32 %0, 0x00600060" : "=v"(k.m2));
+  asm("v_mov_b32 %0, 0x00700070" : "=v"(k.m3));
+  asm("v_mov_b32 %0, 0x00780078" : "=v"(k.m4));
+  asm("v_mov_b32 %0, 0x00100010" : "=v"(k.b30));
+  asm("v_mov_b32 %0, 0x00200020" : "=v"(k.b31));
+  asm("v_mov_b32 %0, 0x00400040" : "=v"(k.b32));
+  return k;
+}
 
 // shift a dword left (s > 0) or right (s < 0); s is a compile-time constant
 template <int S>
@@ -50,57 +85,57 @@ __device__ __forceinline__ uint32_t shl(uint32_t v) {
 // The 16 code pairs of one block (P = pair index = weights 2P, 2P+1), each as
 // two bfloat16 values 128 + c * 2^(7-b).
 template <int B>
-__device__ __forceinline__ void block_pairs(const uint32_t* w, uint32_t (&p)[16]);
+__device__ __forceinline__ void block_pairs(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]);
 
 template <>
-__device__ __forceinline__ void block_pairs<4>(const uint32_t* w, uint32_t (&p)[16]) {
-  constexpr uint32_t m = 0x00780078u;  // bits [3,7) of each half
+__device__ __forceinline__ void block_pairs<4>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m4: bits [3,7) of each half
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
-    p[4 * d + 0] = and_or(shl<3>(w[d]), m, kBf16Base);
-    p[4 * d + 1] = and_or(shl<-1>(w[d]), m, kBf16Base);
-    p[4 * d + 2] = and_or(shl<-5>(w[d]), m, kBf16Base);
-    p[4 * d + 3] = and_or(shl<-9>(w[d]), m, kBf16Base);
+    p[4 * d + 0] = and_or(shl<3>(w[d]), k.m4, k.base);
+    p[4 * d + 1] = and_or(shl<-1>(w[d]), k.m4, k.base);
+    p[4 * d + 2] = and_or(shl<-5>(w[d]), k.m4, k.base);
+    p[4 * d + 3] = and_or(shl<-9>(w[d]), k.m4, k.base);
   }
 }
 
 template <>
-__device__ __forceinline__ void block_pairs<2>(const uint32_t* w, uint32_t (&p)[16]) {
-  constexpr uint32_t m = 0x00600060u;  // bits [5,7) of each half
+__device__ __forceinline__ void block_pairs<2>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m2: bits [5,7) of each half
 #pragma unroll
   for (int d = 0; d < 2; ++d) {
-    p[8 * d + 0] = and_or(shl<5>(w[d]), m, kBf16Base);
-    p[8 * d + 1] = and_or(shl<3>(w[d]), m, kBf16Base);
-    p[8 * d + 2] = and_or(shl<1>(w[d]), m, kBf16Base);
-    p[8 * d + 3] = and_or(shl<-1>(w[d]), m, kBf16Base);
-    p[8 * d + 4] = and_or(shl<-3>(w[d]), m, kBf16Base);
-    p[8 * d + 5] = and_or(shl<-5>(w[d]), m, kBf16Base);
-    p[8 * d + 6] = and_or(shl<-7>(w[d]), m, kBf16Base);
-    p[8 * d + 7] = and_or(shl<-9>(w[d]), m, kBf16Base);
+    p[8 * d + 0] = and_or(shl<5>(w[d]), k.m2, k.base);
+    p[8 * d + 1] = and_or(shl<3>(w[d]), k.m2, k.base);
+    p[8 * d + 2] = and_or(shl<1>(w[d]), k.m2, k.base);
+    p[8 * d + 3] = and_or(shl<-1>(w[d]), k.m2, k.base);
+    p[8 * d + 4] = and_or(shl<-3>(w[d]), k.m2, k.base);
+    p[8 * d + 5] = and_or(shl<-5>(w[d]), k.m2, k.base);
+    p[8 * d + 6] = and_or(shl<-7>(w[d]), k.m2, k.base);
+    p[8 * d + 7] = and_or(shl<-9>(w[d]), k.m2, k.base);
   }
 }
 
 template <>
-__device__ __forceinline__ void block_pairs<3>(const uint32_t* w, uint32_t (&p)[16]) {
-  constexpr uint32_t m = 0x00700070u;  // bits [4,7) of each half
+__device__ __forceinline__ void block_pairs<3>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m3: bits [4,7) of each half
 #pragma unroll
   for (int d = 0; d < 3; ++d) {
-    p[5 * d + 0] = and_or(shl<4>(w[d]), m, kBf16Base);
-    p[5 * d + 1] = and_or(shl<1>(w[d]), m, kBf16Base);
-    p[5 * d + 2] = and_or(shl<-2>(w[d]), m, kBf16Base);
-    p[5 * d + 3] = and_or(shl<-5>(w[d]), m, kBf16Base);
-    p[5 * d + 4] = and_or(shl<-8>(w[d]), m, kBf16Base);
+    p[5 * d + 0] = and_or(shl<4>(w[d]), k.m3, k.base);
+    p[5 * d + 1] = and_or(shl<1>(w[d]), k.m3, k.base);
+    p[5 * d + 2] = and_or(shl<-2>(w[d]), k.m3, k.base);
+    p[5 * d + 3] = and_or(shl<-5>(w[d]), k.m3, k.base);
+    p[5 * d + 4] = and_or(shl<-8>(w[d]), k.m3, k.base);
   }
-  uint32_t t = and_or(shl<-11>(w[0]), 0x00100010u, kBf16Base);
-  t = and_or(shl<-10>(w[1]), 0x00200020u, t);
-  p[15] = and_or(shl<-9>(w[2]), 0x00400040u, t);
+  uint32_t t = and_or(shl<-11>(w[0]), k.b30, k.base);
+  t = and_or(shl<-10>(w[1]), k.b31, t);
+  p[15] = and_or(shl<-9>(w[2]), k.b32, t);
 }
 
 // Load unit u of a row (4*B dwords) with B coalesced 16-byte loads.
 //   row: the row's first dword; U: units per row.
 template <int B>
 __device__ __forceinline__ void load_unit(const uint32_t* row, int U, int u, uint32_t (&w)[4 * B]) {
-  const u32x4* r4 = reinterpret_cast<const u32x4*>(row);
+  const MOEQ_GLOBAL u32x4* r4 = gptr(reinterpret_cast<const u32x4*>(row));
 #pragma unroll
   for (int j = 0; j < B; ++j) {
     const u32x4 v = __builtin_nontemporal_load(r4 + (size_t)j * U + u);

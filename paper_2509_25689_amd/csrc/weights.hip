@@ -71,9 +71,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {
   const uint16_t* sc = t.scales + (size_t)r * (t.K / kBlock) + 4 * u;
   const float z = (float)(1 << (B - 1)), unit = (float)(1 << (7 - B));
   float* o = out + (size_t)r * t.K + kUnit * u;
+  const PairConsts pk = pair_consts();
   for (int q = 0; q < 4; ++q) {
     uint32_t p[16];
-    block_pairs<B>(w + q * B, p);
+    block_pairs<B>(w + q * B, pk, p);
     const float d = half_to_float(sc[q]);
     for (int P = 0; P < 16; ++P) {
       const float c0 = (bf16_lo(p[P]) - 128.0f) / unit, c1 = (bf16_hi(p[P]) - 128.0f) / unit;
