@@ -150,8 +150,11 @@ moeq_status check_routing(const moeq_config* c, const uint8_t* mask, int* n_kept
   return ok();
 }
 
-RouterParams router_params(const moeq_layer* L, const float* logits) {
+RouterParams router_params(const moeq_layer* L, const float* logits, const void* x = nullptr) {
   RouterParams rp;
+  rp.x = (const uint16_t*)x;
+  rp.H = L->cfg.hidden;
+  rp.xexp = L->ws.xexp;
   rp.logits = logits;
   rp.mask = L->mask;
   rp.bias = L->bias;
@@ -175,8 +178,10 @@ moeq_status check_device(const moeq_layer* L) {
 }
 
 // Route (+ bucket) n tokens into the workspace: the first stage of a forward.
-hipError_t route_and_bucket(moeq_layer* L, const float* logits, int n, hipStream_t s) {
-  const RouterParams rp = router_params(L, logits);
+// With x given, the router also records each token's binary16 prescale.
+hipError_t route_and_bucket(moeq_layer* L, const float* logits, int n, hipStream_t s,
+                            const void* x = nullptr) {
+  const RouterParams rp = router_params(L, logits, x);
   if (n <= kDecodeMaxTokens) return launch_route_bucket_small(rp, nullptr, n, L->ws, s);
   hipError_t e = launch_route_tokens(rp, n, L->ws.idx, L->ws.w, s);
   if (e != hipSuccess) return e;
@@ -251,10 +256,13 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     wo = align_up(wo + bytes, 256);
     return at;
   };
+  const int max_mtiles = prefill_max_mtiles(T, k, S, n_kept);
   const size_t o_idx = ws_take(nk * 4), o_w = ws_take(nk * 4), o_off = ws_take((size_t)(E + 1) * 4),
                o_perm = ws_take(nk * 4), o_act = ws_take((size_t)(E + 1) * 4),
                o_cc = ws_take(chunks * E * 4), o_rank = ws_take(nk * 4),
-               o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4);
+               o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4),
+               o_xexp = ws_take((size_t)T * 4), o_rmax = ws_take(rows_h * 4),
+               o_tiles = ws_take((size_t)(1 + 2 * max_mtiles) * 4);
 
   // ---- device work ----
   moeq_layer* L = new moeq_layer();
@@ -340,6 +348,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->ws.rank = (int32_t*)(w + o_rank);
   L->ws.h = (float*)(w + o_h);
   L->ws.partial = (float*)(w + o_part);
+  L->ws.xexp = (int32_t*)(w + o_xexp);
+  L->ws.rowmax = (uint32_t*)(w + o_rmax);
+  L->ws.tiles = (int32_t*)(w + o_tiles);
   *out = L;
   return ok();
 }
@@ -396,6 +407,10 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.k = L->cfg.top_k;
   const long long nk = (long long)n * a.k;
   a.max_active = (int)(nk < L->n_kept ? nk : L->n_kept);
+  a.xexp = L->ws.xexp;
+  a.rowmax = L->ws.rowmax;
+  a.tiles = L->ws.tiles;
+  a.max_mtiles = prefill_max_mtiles(n, a.k, a.S, L->n_kept);
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
   hipError_t e = hipSuccess;
@@ -403,7 +418,7 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
     if (L->timing && e == hipSuccess) e = hipEventRecord(L->stage_events[i], s);
   };
   mark(0);
-  if (e == hipSuccess) e = route_and_bucket(L, logits, n, s);
+  if (e == hipSuccess) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
   mark(1);
   if (e == hipSuccess) e = prefill ? launch_gateup_prefill(a, s) : launch_gateup_decode(a, s);
   mark(2);

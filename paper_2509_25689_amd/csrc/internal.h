@@ -43,6 +43,11 @@ struct RouterParams {
   const float* bias;      // [E] device copy (zeros when none was given)
   int32_t E, G, TG, k, topn, norm;
   float scale;
+  // optional (many-token path): activations whose per-token binary exponent
+  // prescale for half precision is written to xexp
+  const uint16_t* x;      // bf16 [n x H] or null
+  int32_t H;
+  int32_t* xexp;          // [n]
 };
 
 // Workspace views (device pointers) for one forward.
@@ -56,6 +61,9 @@ struct Workspace {
   int32_t* rank;       // [T*k]   rank of an assignment inside its chunk and expert
   float* h;            // [(T*k + T*S) x I] SwiGLU activations, bucket order then shared
   float* partial;      // [(T*k + T*S) x H] per-assignment expert outputs, t*k + j then shared
+  int32_t* xexp;       // [T]     per-token exponent e: x * 2^-e fits binary16
+  uint32_t* rowmax;    // [T*k + T*S] max |h| of each activation row (float bits)
+  int32_t* tiles;      // [1 + 2*max_mtiles] count, then (slot, first row) per m-tile
 };
 
 // ---- launchers (return hipSuccess or the launch error) ----
@@ -85,11 +93,18 @@ struct DecodeArgs {
   float* y;
   int32_t n, H, I, E, S, k;
   int32_t max_active;     // routed slots launched: min(n*k, kept experts)
+  // many-token path
+  const int32_t* xexp;
+  uint32_t* rowmax;
+  int32_t* tiles;
+  int32_t max_mtiles;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // prefill.hip
+constexpr int kGemmBM = 128;  // tokens per grouped-GEMM m-tile
+int prefill_max_mtiles(int n, int k, int S, int n_kept);
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s);
 

@@ -76,6 +76,14 @@ template <int EPL>
 __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
                                  float* w_g, int32_t* idx_s) {
   const int lane = threadIdx.x & 63;
+  if (rp.x) {
+    // binary exponent prescale for half precision: x * 2^-e < 2^15
+    uint32_t mx = 0;
+    for (int i = lane; i < rp.H; i += 64) mx = max(mx, (uint32_t)(rp.x[(size_t)t * rp.H + i] & 0x7FFFu));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
+    if (lane == 0) rp.xexp[t] = max(0, (int)((mx >> 7) & 0xFFu) - 127 - 14);
+  }
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
   const float* lg = rp.logits + (size_t)t * E;
   float s[EPL], b[EPL];
