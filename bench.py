@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 
 METRIC = "V3-shape MoE layer decode tokens/s + effective weight GB/s vs HBM peak"
 HBM_PEAK_GBPS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 
 
 def parse():
@@ -45,6 +46,7 @@ def parse():
     p.add_argument("--sets", type=int, default=64, help="input sets (x, logits) per layer")
     p.add_argument("--kernel-steps", type=int, default=256, help="eager forwards timed per stage")
     p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
+    p.add_argument("--prefill-steps", type=int, default=10, help="2048-token prefill forwards timed (0 = skip)")
     return p.parse_args()
 
 
@@ -101,6 +103,49 @@ def build_layer(torch, moeq, synth, shape, plan, key, max_tokens):
 def tensor_bytes(shape, bits, p):
     rows, K = shape.rows_cols(p)
     return rows * K * bits // 8 + rows * (K // 32) * 2
+
+
+def prefill_bench(torch, np, moeq, synth, hip, steps, n=2048):
+    """The 2048-token prefill: Zipf(1.1)-routed, per-tensor widths from {2,3,4}
+    (p = 0.6, 0.2, 0.2), grouped GEMM path.  Returns a dict of measurements."""
+    shape = synth.V3
+    layer, mask, _, _ = build_layer(torch, moeq, synth, shape, "p234_602020", "bench-prefill", max_tokens=n)
+    sets = 4
+    xs = [torch.from_numpy(synth.activations(n, shape.hidden, "bench-pf-x", i).view(np.int16)).cuda()
+          .view(torch.bfloat16) for i in range(sets)]
+    lgs = [torch.from_numpy(synth.zipf_logits(n, mask, "bench-pf-l", i)).cuda() for i in range(sets)]
+    y = torch.empty((n, shape.hidden), device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    for i in range(2):
+        moeq.moeq_forward(layer.handle, xs[i % sets].data_ptr(), lgs[i % sets].data_ptr(), n, y.data_ptr(), stream)
+    torch.cuda.synchronize()
+    events = [[hip.event() for _ in range(moeq.MOEQ_STAGE_EVENTS)] for _ in range(steps)]
+    for j in range(steps):
+        moeq.moeq_set_stage_events(layer.handle, events[j])
+        moeq.moeq_forward(layer.handle, xs[j % sets].data_ptr(), lgs[j % sets].data_ptr(), n, y.data_ptr(), stream)
+    moeq.moeq_set_stage_events(layer.handle, None)
+    torch.cuda.synchronize()
+    st = np.array([[hip.elapsed_ms(ev[s], ev[s + 1]) for s in range(4)] for ev in events]).mean(axis=0)
+    total = np.array([hip.elapsed_ms(ev[0], ev[4]) for ev in events]).mean()
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    layer.close()
+    rows = n * (shape.top_k + shape.n_shared)
+    f_gu = 2.0 * 2 * shape.hidden * shape.inter * rows
+    f_dn = 2.0 * shape.hidden * shape.inter * rows
+    tf = lambda f, ms: f / (ms * 1e-3) / 1e12
+    return {"workload": f"DeepSeek-V3-shape layer prefill, {n} tokens, Zipf(1.1) routing over 192 kept experts, "
+                        "per-tensor widths from {2,3,4} (p=0.6,0.2,0.2)",
+            "tokens_per_s": round(n / (total * 1e-3), 1), "ms_per_step": round(total, 4),
+            "useful_tflop_per_step": round((f_gu + f_dn) / 1e12, 4),
+            "tflops": round(tf(f_gu + f_dn, total), 1),
+            "mfma_frac": round(tf(f_gu + f_dn, total) / MFMA_F16_PEAK_TFLOPS, 4),
+            "stage_ms": {"route_bucket": round(st[0], 4), "gate_up": round(st[1], 4), "down": round(st[2], 4),
+                         "combine": round(st[3], 4)},
+            "gate_up_tflops": round(tf(f_gu, st[1]), 1), "down_tflops": round(tf(f_dn, st[2]), 1),
+            "gate_up_mfma_frac": round(tf(f_gu, st[1]) / MFMA_F16_PEAK_TFLOPS, 4),
+            "steps": steps, "dtype": "fp16 MFMA, fp32 accumulate"}
 
 
 def cpu_baseline(shape, steps, batch):
@@ -306,6 +351,8 @@ def main():
     }
     for L, *_ in layers:
         L.close()
+    if args.prefill_steps > 0:
+        out["prefill"] = prefill_bench(torch, np, moeq, synth, hip, args.prefill_steps)
     if args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_steps, B)
     print(json.dumps(out), flush=True)

@@ -155,6 +155,7 @@ RouterParams router_params(const moeq_layer* L, const float* logits, const void*
   rp.x = (const uint16_t*)x;
   rp.H = L->cfg.hidden;
   rp.xexp = L->ws.xexp;
+  rp.x16 = L->ws.x16;
   rp.logits = logits;
   rp.mask = L->mask;
   rp.bias = L->bias;
@@ -262,7 +263,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
                o_cc = ws_take(chunks * E * 4), o_rank = ws_take(nk * 4),
                o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4),
                o_xexp = ws_take((size_t)T * 4), o_rmax = ws_take(rows_h * 4),
-               o_tiles = ws_take((size_t)(1 + 2 * max_mtiles) * 4);
+               o_tiles = ws_take((size_t)(1 + 2 * max_mtiles) * 4),
+               o_x16 = ws_take((size_t)T * H * 2), o_h16 = ws_take(rows_h * I * 2);
 
   // ---- device work ----
   moeq_layer* L = new moeq_layer();
@@ -351,6 +353,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->ws.xexp = (int32_t*)(w + o_xexp);
   L->ws.rowmax = (uint32_t*)(w + o_rmax);
   L->ws.tiles = (int32_t*)(w + o_tiles);
+  L->ws.x16 = (uint16_t*)(w + o_x16);
+  L->ws.h16 = (uint16_t*)(w + o_h16);
   *out = L;
   return ok();
 }
@@ -411,6 +415,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.rowmax = L->ws.rowmax;
   a.tiles = L->ws.tiles;
   a.max_mtiles = prefill_max_mtiles(n, a.k, a.S, L->n_kept);
+  a.x16 = L->ws.x16;
+  a.h16 = L->ws.h16;
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
   hipError_t e = hipSuccess;

@@ -44,10 +44,12 @@ struct RouterParams {
   int32_t E, G, TG, k, topn, norm;
   float scale;
   // optional (many-token path): activations whose per-token binary exponent
-  // prescale for half precision is written to xexp
+  // prescale for half precision is written to xexp, and the prescaled
+  // binary16 copy x * 2^-xexp to x16
   const uint16_t* x;      // bf16 [n x H] or null
   int32_t H;
   int32_t* xexp;          // [n]
+  uint16_t* x16;          // binary16 [n x H]
 };
 
 // Workspace views (device pointers) for one forward.
@@ -64,6 +66,8 @@ struct Workspace {
   int32_t* xexp;       // [T]     per-token exponent e: x * 2^-e fits binary16
   uint32_t* rowmax;    // [T*k + T*S] max |h| of each activation row (float bits)
   int32_t* tiles;      // [1 + 2*max_mtiles] count, then (slot, first row) per m-tile
+  uint16_t* x16;       // [T x H]  binary16 x * 2^-xexp (many-token path)
+  uint16_t* h16;       // [(T*k + T*S) x I] binary16 h * 2^-(row exponent) (many-token path)
 };
 
 // ---- launchers (return hipSuccess or the launch error) ----
@@ -98,6 +102,8 @@ struct DecodeArgs {
   uint32_t* rowmax;
   int32_t* tiles;
   int32_t max_mtiles;
+  const uint16_t* x16;
+  uint16_t* h16;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);

@@ -17,6 +17,7 @@
 // counts and every assignment's rank inside its expert; a scan over chunks and
 // experts turns those into global positions.  Integer-only and deterministic.
 #include "internal.h"
+#include "layout.h"
 
 namespace moeq {
 
@@ -77,12 +78,36 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
                                  float* w_g, int32_t* idx_s) {
   const int lane = threadIdx.x & 63;
   if (rp.x) {
-    // binary exponent prescale for half precision: x * 2^-e < 2^15
+    // binary exponent prescale for half precision: x * 2^-e < 2^15, and the
+    // prescaled binary16 copy of the row (exact unless it falls below the
+    // binary16 normal range, then rounded to nearest even)
+    const MOEQ_GLOBAL u32x4* xr = gptr(reinterpret_cast<const u32x4*>(rp.x + (size_t)t * rp.H));
+    const int C = rp.H / 8;
     uint32_t mx = 0;
-    for (int i = lane; i < rp.H; i += 64) mx = max(mx, (uint32_t)(rp.x[(size_t)t * rp.H + i] & 0x7FFFu));
+    for (int c = lane; c < C; c += 64) {
+      const u32x4 v = xr[c];
+      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) mx = max(mx, max(q[j] & 0x7FFFu, (q[j] >> 16) & 0x7FFFu));
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
-    if (lane == 0) rp.xexp[t] = max(0, (int)((mx >> 7) & 0xFFu) - 127 - 14);
+    const int e = max(0, (int)((mx >> 7) & 0xFFu) - 127 - 14);
+    if (lane == 0) rp.xexp[t] = e;
+    const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
+    MOEQ_GLOBAL u32x4* hr = (MOEQ_GLOBAL u32x4*)(rp.x16 + (size_t)t * rp.H);
+    for (int c = lane; c < C; c += 64) {
+      const u32x4 v = xr[c];
+      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float lo = __uint_as_float(q[j] << 16) * sc, hi = __uint_as_float(q[j] & 0xFFFF0000u) * sc;
+        o[j] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+               ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+      }
+      hr[c] = u32x4{o[0], o[1], o[2], o[3]};
+    }
   }
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
   const float* lg = rp.logits + (size_t)t * E;
