@@ -47,6 +47,10 @@ def parse():
     p.add_argument("--kernel-steps", type=int, default=256, help="eager forwards timed per stage")
     p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
     p.add_argument("--prefill-steps", type=int, default=10, help="2048-token prefill forwards timed (0 = skip)")
+    p.add_argument("--mode", choices=("all", "decode", "prefill", "copy"), default="all",
+                   help="all: decode line with prefill and CPU legs; decode / prefill: one leg only "
+                        "(for profiling); copy: a plain 1 GiB device copy whose HBM counters "
+                        "calibrate the profiler's byte counts")
     return p.parse_args()
 
 
@@ -58,6 +62,7 @@ class Hip:
         for name, args in (("hipEventCreate", [ctypes.POINTER(ctypes.c_void_p)]),
                            ("hipEventDestroy", [ctypes.c_void_p]),
                            ("hipEventSynchronize", [ctypes.c_void_p]),
+                           ("hipEventRecord", [ctypes.c_void_p, ctypes.c_void_p]),
                            ("hipEventElapsedTime", [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                     ctypes.c_void_p])):
             getattr(self.lib, name).argtypes = args
@@ -67,6 +72,9 @@ class Hip:
         e = ctypes.c_void_p()
         assert self.lib.hipEventCreate(ctypes.byref(e)) == 0
         return e.value
+
+    def record(self, e, stream):
+        assert self.lib.hipEventRecord(e, stream) == 0
 
     def elapsed_ms(self, a, b):
         assert self.lib.hipEventSynchronize(b) == 0
@@ -148,6 +156,27 @@ def prefill_bench(torch, np, moeq, synth, hip, steps, n=2048):
             "steps": steps, "dtype": "fp16 MFMA, fp32 accumulate"}
 
 
+def copy_calibration(torch, hip, nbytes=1 << 30, reps=4):
+    """A plain device-to-device copy of known size: under rocprofv3 --pmc its
+    FETCH_SIZE / WRITE_SIZE per dispatch give the factor that turns those
+    counters into bytes."""
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    e0, e1 = hip.event(), hip.event()
+    stream = torch.cuda.current_stream().cuda_stream
+    hip.record(e0, stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    hip.record(e1, stream)
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(e0, e1) / reps
+    hip.destroy(e0)
+    hip.destroy(e1)
+    return {"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps, "ms_per_copy": round(ms, 4),
+            "GBps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def cpu_baseline(shape, steps, batch):
     """The oracle, as it stands, on `steps` forwards of the same workload shape.
 
@@ -216,6 +245,13 @@ def main():
     B, NL, R = args.batch, args.layers, args.sets
     hip = Hip()
     torch.cuda.set_device(0)
+    if args.mode == "copy":
+        print(json.dumps(copy_calibration(torch, hip)), flush=True)
+        return
+    if args.mode == "prefill":
+        print(json.dumps({"prefill": prefill_bench(torch, np, moeq, synth, hip, max(1, args.prefill_steps))}),
+              flush=True)
+        return
 
     layers = []
     for li in range(NL):
@@ -351,9 +387,9 @@ def main():
     }
     for L, *_ in layers:
         L.close()
-    if args.prefill_steps > 0:
+    if args.mode == "all" and args.prefill_steps > 0:
         out["prefill"] = prefill_bench(torch, np, moeq, synth, hip, args.prefill_steps)
-    if args.cpu_steps > 0:
+    if args.mode == "all" and args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_steps, B)
     print(json.dumps(out), flush=True)
 

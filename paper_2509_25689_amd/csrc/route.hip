@@ -24,7 +24,6 @@ namespace moeq {
 namespace {
 
 constexpr int kWaves = 4;        // tokens per workgroup of the many-token router
-constexpr int kSmallWaves = 16;  // waves of the small-batch route + bucket workgroup
 
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -68,6 +67,29 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)k, 63);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(k >> 32), 63);
   return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum of an unsigned key over the wavefront, returned to every lane
+// (0 is the identity, so each step folds into one v_max_u32 with DPP).
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false));  // row_shr:1
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false));  // row_shr:2
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false));  // row_shr:4
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false));  // row_shr:8
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));  // row_bcast:15
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Inclusive prefix sum over the wavefront.
+__device__ __forceinline__ int wave_incl_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return v;
 }
 
 // Route token t with the calling wavefront.  Lane l owns experts
@@ -189,35 +211,62 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
   }
   const uint64_t gsel = __ballot(keep);
 
-  // ---- expert selection: k rounds of "best key below the previous pick" ----
-  uint64_t key[EPL];
+  // ---- expert selection ----
+  // Each lane sorts its own candidates (biased score descending, lower id
+  // first); then k rounds of: wave-wide float max of every lane's current
+  // head, the lowest lane holding it wins (lane l owns ids [l*EPL, l*EPL+EPL),
+  // so that is the lowest id among equal scores), the winner drops its head.
+  float cv[EPL], cs[EPL];
+  int ci[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
-    key[i] = (e < E && b[i] != -INFINITY && ((gsel >> (e / per)) & 1)) ? sel_key(b[i], e) : 0ull;
+    const bool ok = e < E && b[i] != -INFINITY && ((gsel >> (e / per)) & 1);
+    cv[i] = ok ? b[i] : -INFINITY;
+    cs[i] = s[i];
+    ci[i] = i;
   }
-  uint64_t prev = ~0ull;
+#pragma unroll
+  for (int i = 1; i < EPL; ++i)
+#pragma unroll
+    for (int j = i; j > 0; --j) {
+      // insertion step: move element j up while it comes before element j-1
+      const bool sw = cv[j] > cv[j - 1] || (cv[j] == cv[j - 1] && ci[j] < ci[j - 1]);
+      const float tv = cv[j], ts = cs[j];
+      const int ti = ci[j];
+      cv[j] = sw ? cv[j - 1] : cv[j];
+      cs[j] = sw ? cs[j - 1] : cs[j];
+      ci[j] = sw ? ci[j - 1] : ci[j];
+      cv[j - 1] = sw ? tv : cv[j - 1];
+      cs[j - 1] = sw ? ts : cs[j - 1];
+      ci[j - 1] = sw ? ti : ci[j - 1];
+    }
+  // keys: order-preserving map of the head score, 0 = no candidate left
+  auto head_key = [](float v) { return v == -INFINITY ? 0u : ord_f32(v); };
+  uint32_t hk = head_key(cv[0]);
   float sum = 0.0f, my_s = 0.0f;
-  int my_i = 0, last = -1;
+  int my_i = 0, last = 0;
   for (int r = 0; r < rp.k; ++r) {
-    uint64_t kb = 0;
-#pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if (key[i] < prev && key[i] > kb) kb = key[i];
-    kb = wave_max_key(kb);
+    const uint32_t m = wave_max_u32(hk);
+    const uint64_t hold = __ballot(hk == m) & (m ? ~0ull : 0ull);
     // creation checks guarantee k candidates; never leave the index range
-    const int e = kb ? (int)~(uint32_t)kb : (last < 0 ? 0 : last);
-    float sv = 0.0f;
+    const int wl = hold ? __builtin_ctzll(hold) : 0;
+    const int e = hold ? wl * EPL + __builtin_amdgcn_readlane(ci[0], wl) : last;
+    const float sv = hold ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cs[0]), wl)) : 0.0f;
+    const bool win = hold && lane == wl;
 #pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      if (e % EPL == i) sv = s[i];
-    sv = __shfl(sv, e / EPL, 64);
+    for (int i = 0; i + 1 < EPL; ++i) {
+      cv[i] = win ? cv[i + 1] : cv[i];
+      cs[i] = win ? cs[i + 1] : cs[i];
+      ci[i] = win ? ci[i + 1] : ci[i];
+    }
+    cv[EPL - 1] = win ? -INFINITY : cv[EPL - 1];
+    hk = win ? head_key(cv[0]) : hk;
     sum = sum + sv;
     if (lane == r) {
       my_i = e;
       my_s = sv;
     }
-    if (kb) prev = kb;
     last = e;
   }
   if (lane < rp.k) {
@@ -233,50 +282,36 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
   wave_sync();  // gs_l is reused by this wave's next token
 }
 
-// Route token t, choosing the experts-per-lane instantiation from E.
-__device__ __forceinline__ void route_token(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
-                                           float* w_g, int32_t* idx_s) {
-  if (rp.E <= 64)
-    route_token_wave<1>(rp, t, gs_l, idx_g, w_g, idx_s);
-  else if (rp.E <= 128)
-    route_token_wave<2>(rp, t, gs_l, idx_g, w_g, idx_s);
-  else if (rp.E <= 256)
-    route_token_wave<4>(rp, t, gs_l, idx_g, w_g, idx_s);
-  else if (rp.E <= 512)
-    route_token_wave<8>(rp, t, gs_l, idx_g, w_g, idx_s);
-  else
-    route_token_wave<16>(rp, t, gs_l, idx_g, w_g, idx_s);
-}
+// Experts per lane for E experts (the kernels are instantiated per value).
+int experts_per_lane(int E) { return E <= 64 ? 1 : E <= 128 ? 2 : E <= 256 ? 4 : E <= 512 ? 8 : 16; }
 
 // Exclusive scan of cnt[0..E) by one wavefront into off[0..E] (off[E] = total),
 // plus the ascending list of experts with cnt > 0 into active[1..], count in
-// active[0].  Each lane owns a contiguous run of experts.
+// active[0].  Lane l owns experts [l*EPL, l*EPL + EPL), EPL*64 >= E.
+template <int EPL>
 __device__ void wave_scan_experts(const int* cnt, int E, int32_t* off_lds, int32_t* off_g,
                                   int32_t* active_g) {
   const int lane = threadIdx.x & 63;
-  const int epl = (E + 63) / 64;
-  const int e0 = lane * epl, e1 = min(E, e0 + epl);
+  int c[EPL];
   int local = 0, nact = 0;
-  for (int e = e0; e < e1; ++e) {
-    local += cnt[e];
-    nact += cnt[e] > 0;
-  }
-  int incl = local, iact = nact;
 #pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    int v = __shfl_up(incl, d, 64);
-    int a = __shfl_up(iact, d, 64);
-    if (lane >= d) {
-      incl += v;
-      iact += a;
-    }
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane * EPL + i;
+    c[i] = e < E ? cnt[e] : 0;
+    local += c[i];
+    nact += c[i] > 0;
   }
+  const int incl = wave_incl_sum(local), iact = wave_incl_sum(nact);
   int run = incl - local, arun = iact - nact;
-  for (int e = e0; e < e1; ++e) {
-    if (off_lds) off_lds[e] = run;
-    off_g[e] = run;
-    if (cnt[e] > 0) active_g[1 + arun++] = e;
-    run += cnt[e];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane * EPL + i;
+    if (e < E) {
+      if (off_lds) off_lds[e] = run;
+      off_g[e] = run;
+      if (c[i] > 0) active_g[1 + arun++] = e;
+      run += c[i];
+    }
   }
   if (lane == 63) {
     off_g[E] = incl;
@@ -286,10 +321,16 @@ __device__ void wave_scan_experts(const int* cnt, int E, int32_t* off_lds, int32
 }
 
 // ---- small batches (n <= 64): route + bucket in one workgroup ----
-__global__ __launch_bounds__(1024) void route_bucket_small_kernel(RouterParams rp,
+// threads of the small-batch workgroup: fewer for wide lanes (register room)
+template <int EPL>
+constexpr int small_threads() { return EPL >= 8 ? 512 : 1024; }
+
+template <int EPL>
+__global__ __launch_bounds__(small_threads<EPL>()) void route_bucket_small_kernel(RouterParams rp,
                                                                   const int32_t* idx_in, int n,
                                                                   Workspace ws) {
-  __shared__ float gs_l[kSmallWaves][64];
+  constexpr int NT = small_threads<EPL>(), NW = NT / 64;
+  __shared__ float gs_l[NW][64];
   __shared__ int32_t idx_l[kDecodeMaxTokens * kMaxTopK];
   __shared__ unsigned long long emask[kMaxExperts];
   __shared__ int32_t cnt[kMaxExperts];
@@ -297,22 +338,22 @@ __global__ __launch_bounds__(1024) void route_bucket_small_kernel(RouterParams r
 
   const int tid = threadIdx.x, wave = tid >> 6;
   const int E = rp.E, k = rp.k, nk = n * k;
-  for (int e = tid; e < E; e += 1024) emask[e] = 0ull;
+  for (int e = tid; e < E; e += NT) emask[e] = 0ull;
   if (idx_in) {
-    for (int a = tid; a < nk; a += 1024) idx_l[a] = idx_in[a];
+    for (int a = tid; a < nk; a += NT) idx_l[a] = idx_in[a];
   } else {
-    for (int t = wave; t < n; t += kSmallWaves) route_token(rp, t, gs_l[wave], ws.idx, ws.w, idx_l);
+    for (int t = wave; t < n; t += NW) route_token_wave<EPL>(rp, t, gs_l[wave], ws.idx, ws.w, idx_l);
   }
   __syncthreads();
   // ids outside [0, E) (possible only for caller-provided ids) are ignored
-  for (int a = tid; a < nk; a += 1024)
+  for (int a = tid; a < nk; a += NT)
     if ((unsigned)idx_l[a] < (unsigned)E) atomicOr(&emask[idx_l[a]], 1ull << (a / k));
   __syncthreads();
-  for (int e = tid; e < E; e += 1024) cnt[e] = __popcll(emask[e]);
+  for (int e = tid; e < E; e += NT) cnt[e] = __popcll(emask[e]);
   __syncthreads();
-  if (wave == 0) wave_scan_experts(cnt, E, off, ws.offsets, ws.active);
+  if (wave == 0) wave_scan_experts<EPL>(cnt, E, off, ws.offsets, ws.active);
   __syncthreads();
-  for (int a = tid; a < nk; a += 1024) {
+  for (int a = tid; a < nk; a += NT) {
     const int e = idx_l[a], t = a / k;
     if ((unsigned)e >= (unsigned)E) continue;
     const unsigned long long below = (t == 0) ? 0ull : (emask[e] & ((1ull << t) - 1ull));
@@ -321,12 +362,13 @@ __global__ __launch_bounds__(1024) void route_bucket_small_kernel(RouterParams r
 }
 
 // ---- large batches: one token per wavefront ----
+template <int EPL>
 __global__ __launch_bounds__(256) void route_tokens_kernel(RouterParams rp, int n, int32_t* idx,
                                                            float* w) {
   __shared__ float gs_l[kWaves][64];
   const int wave = threadIdx.x >> 6;
   const int t = blockIdx.x * kWaves + wave;
-  if (t < n) route_token(rp, t, gs_l[wave], idx, w, nullptr);
+  if (t < n) route_token_wave<EPL>(rp, t, gs_l[wave], idx, w, nullptr);
 }
 
 // chunk c = tokens [64c, 64c+64): per-expert counts and in-chunk ranks
@@ -350,6 +392,7 @@ __global__ __launch_bounds__(256) void bucket_count_kernel(const int32_t* idx, i
 }
 
 // one workgroup: per-expert scan over chunks, then over experts
+template <int EPL>
 __global__ __launch_bounds__(1024) void bucket_scan_kernel(int n_chunks, int E, int32_t* chunk_cnt,
                                                            int32_t* offsets, int32_t* active) {
   __shared__ int32_t total[kMaxExperts];
@@ -365,7 +408,7 @@ __global__ __launch_bounds__(1024) void bucket_scan_kernel(int n_chunks, int E, 
     total[e] = run;
   }
   __syncthreads();
-  if (tid < 64) wave_scan_experts(total, E, off, offsets, active);
+  if (tid < 64) wave_scan_experts<EPL>(total, E, off, offsets, active);
   __syncthreads();
   for (int e = tid; e < E; e += 1024)
     for (int c = 0; c < n_chunks; ++c) chunk_cnt[(size_t)c * E + e] += off[e];
@@ -385,13 +428,26 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const int32_t* idx,
 
 hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_in, int n,
                                      const Workspace& ws, hipStream_t s) {
-  route_bucket_small_kernel<<<1, 1024, 0, s>>>(rp, idx_in, n, ws);
+  switch (experts_per_lane(rp.E)) {
+    case 1: route_bucket_small_kernel<1><<<1, small_threads<1>(), 0, s>>>(rp, idx_in, n, ws); break;
+    case 2: route_bucket_small_kernel<2><<<1, small_threads<2>(), 0, s>>>(rp, idx_in, n, ws); break;
+    case 4: route_bucket_small_kernel<4><<<1, small_threads<4>(), 0, s>>>(rp, idx_in, n, ws); break;
+    case 8: route_bucket_small_kernel<8><<<1, small_threads<8>(), 0, s>>>(rp, idx_in, n, ws); break;
+    default: route_bucket_small_kernel<16><<<1, small_threads<16>(), 0, s>>>(rp, idx_in, n, ws); break;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_route_tokens(const RouterParams& rp, int n, int32_t* idx, float* w,
                                hipStream_t s) {
-  route_tokens_kernel<<<(n + kWaves - 1) / kWaves, 256, 0, s>>>(rp, n, idx, w);
+  const int grid = (n + kWaves - 1) / kWaves;
+  switch (experts_per_lane(rp.E)) {
+    case 1: route_tokens_kernel<1><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
+    case 2: route_tokens_kernel<2><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
+    case 4: route_tokens_kernel<4><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
+    case 8: route_tokens_kernel<8><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
+    default: route_tokens_kernel<16><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
+  }
   return hipGetLastError();
 }
 
@@ -401,7 +457,13 @@ hipError_t launch_bucket_chunked(const int32_t* idx, int n, int k, int E, const 
   bucket_count_kernel<<<chunks, 256, 0, s>>>(idx, n, k, E, ws.chunk_cnt, ws.rank);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  bucket_scan_kernel<<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active);
+  switch (experts_per_lane(E)) {
+    case 1: bucket_scan_kernel<1><<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active); break;
+    case 2: bucket_scan_kernel<2><<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active); break;
+    case 4: bucket_scan_kernel<4><<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active); break;
+    case 8: bucket_scan_kernel<8><<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active); break;
+    default: bucket_scan_kernel<16><<<1, 1024, 0, s>>>(chunks, E, ws.chunk_cnt, ws.offsets, ws.active); break;
+  }
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   bucket_scatter_kernel<<<(n * k + 255) / 256, 256, 0, s>>>(idx, n, k, E, ws.chunk_cnt, ws.rank,
