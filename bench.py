@@ -47,10 +47,12 @@ def parse():
     p.add_argument("--kernel-steps", type=int, default=256, help="eager forwards timed per stage")
     p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
     p.add_argument("--prefill-steps", type=int, default=10, help="2048-token prefill forwards timed (0 = skip)")
-    p.add_argument("--mode", choices=("all", "decode", "prefill", "copy"), default="all",
-                   help="all: decode line with prefill and CPU legs; decode / prefill: one leg only "
-                        "(for profiling); copy: a plain 1 GiB device copy whose HBM counters "
-                        "calibrate the profiler's byte counts")
+    p.add_argument("--b16-steps", type=int, default=2560, help="16-token decode steps timed (0 = skip)")
+    p.add_argument("--mode", choices=("all", "decode", "prefill", "copy", "stack", "sweep"), default="all",
+                   help="all: batch-1 decode line with 16-token, prefill and CPU legs; decode / prefill: "
+                        "one leg only (for profiling); copy: a plain 1 GiB device copy whose HBM counters "
+                        "calibrate the profiler's byte counts; stack: 58 independent layers; sweep: kept "
+                        "experts x widths x tokens x routing on the decode path")
     return p.parse_args()
 
 
@@ -60,6 +62,7 @@ class Hip:
     def __init__(self):
         self.lib = ctypes.CDLL("libamdhip64.so.7")
         for name, args in (("hipEventCreate", [ctypes.POINTER(ctypes.c_void_p)]),
+                           ("hipEventCreateWithFlags", [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]),
                            ("hipEventDestroy", [ctypes.c_void_p]),
                            ("hipEventSynchronize", [ctypes.c_void_p]),
                            ("hipEventRecord", [ctypes.c_void_p, ctypes.c_void_p]),
@@ -68,18 +71,27 @@ class Hip:
             getattr(self.lib, name).argtypes = args
             getattr(self.lib, name).restype = ctypes.c_int
 
+    # timing-only events: no system-scope fence (cache writeback and
+    # invalidation) when they are recorded, so they barely perturb the kernels
+    # they bracket
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
     def event(self):
         e = ctypes.c_void_p()
-        assert self.lib.hipEventCreate(ctypes.byref(e)) == 0
+        assert self.lib.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE) == 0
         return e.value
 
     def record(self, e, stream):
         assert self.lib.hipEventRecord(e, stream) == 0
 
-    def elapsed_ms(self, a, b):
+    def elapsed_ms(self, a, b, strict=True):
         assert self.lib.hipEventSynchronize(b) == 0
         ms = ctypes.c_float()
-        assert self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        rc = self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if rc != 0:
+            if strict:
+                raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+            return None
         return ms.value
 
     def destroy(self, e):
@@ -230,6 +242,188 @@ def cpu_baseline(shape, steps, batch):
                       f"random packed codes; {dt:.1f} s; host cores visible {cores}"}
 
 
+def random_layer(torch, moeq, synth, shape, plan, key, max_tokens):
+    """A layer whose codes are uniform random bytes and whose scales are near the
+    block quantizer's typical d for N(0, 0.02) weights (about 2.2 sigma /
+    qmax, times U(0.8, 1.2)), generated directly on the GPU: used where
+    quantizing real draws would take too long (the 58-layer stack)."""
+    mask = synth.expert_mask(shape, key)
+    bits_r, bits_s = synth.bit_plan(shape, plan, key)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(synth.seed_int("bench-rand", key))
+
+    def tensor(bits, p):
+        rows, K = shape.rows_cols(p)
+        codes = torch.randint(0, 256, (rows, K * bits // 8), generator=gen, device="cuda", dtype=torch.uint8)
+        qmax = (1 << (bits - 1)) - 1
+        d = (0.02 * 2.2 / qmax) * (0.8 + 0.4 * torch.rand((rows, K // 32), generator=gen, device="cuda"))
+        return dict(bits=bits, codes=codes, scales=d.to(torch.float16).view(torch.int16))
+
+    routed = {int(e): tuple(tensor(int(bits_r[e, p]), p) for p in range(3))
+              for e in range(shape.n_experts) if mask[e]}
+    shared = [tuple(tensor(int(bits_s[s, p]), p) for p in range(3)) for s in range(shape.n_shared)]
+    torch.cuda.synchronize()
+    layer = moeq.Layer(shape, mask, routed, shared, max_tokens=max_tokens, device_weights=True)
+    del routed, shared
+    return layer, mask, bits_r, bits_s
+
+
+def step_bytes_of(np, shape, layer, bits_r, bits_s, logits):
+    """Algorithmic bytes of one forward: codes + scales of every distinct
+    tensor it touches (routed experts chosen by any token, plus the shared
+    experts), and of each kind (gate/up, down)."""
+    idx, _ = layer.route(logits)
+    experts = np.unique(idx.cpu().numpy())
+    g = sum(tensor_bytes(shape, int(bits_r[e, 0]), 0) + tensor_bytes(shape, int(bits_r[e, 1]), 1) for e in experts)
+    d = sum(tensor_bytes(shape, int(bits_r[e, 2]), 2) for e in experts)
+    for s in range(shape.n_shared):
+        g += tensor_bytes(shape, int(bits_s[s, 0]), 0) + tensor_bytes(shape, int(bits_s[s, 1]), 1)
+        d += tensor_bytes(shape, int(bits_s[s, 2]), 2)
+    return g, d, len(experts)
+
+
+def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, kernel_steps, key,
+               zipf=False, path=None):
+    """Batch-B decode over the given layers (step s uses layer s % NL and
+    input set s), replayed from one HIP graph with inputs resident in HBM.
+    Returns timing, bytes and per-stage kernel durations."""
+    NL = len(layers)
+    n_sets = R * NL
+    if path is not None:
+        for L, *_ in layers:
+            L.set_path(path)
+    xs, lgs = [], []
+    for i in range(n_sets):
+        xb = synth.activations(B, shape.hidden, key, "x", i)
+        xs.append(torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16))
+        mask = layers[i % NL][1]
+        lg = synth.zipf_logits(B, mask, key, "l", i) if zipf else synth.normal_logits(B, shape.n_experts, key, "l", i)
+        lgs.append(torch.from_numpy(lg).cuda())
+    ys = [torch.empty((B, shape.hidden), device="cuda") for _ in range(NL)]
+    gu_bytes, down_bytes, n_exp = [], [], []
+    for i in range(n_sets):
+        layer, mask, bits_r, bits_s = layers[i % NL]
+        g, d, ne = step_bytes_of(np, shape, layer, bits_r, bits_s, lgs[i])
+        gu_bytes.append(g)
+        down_bytes.append(d)
+        n_exp.append(ne)
+    io_bytes = B * (shape.hidden * 2 + shape.n_experts * 4 + shape.hidden * 4)
+
+    def run_step(i, stream):
+        layer = layers[i % NL][0]
+        moeq.moeq_forward(layer.handle, xs[i].data_ptr(), lgs[i].data_ptr(), B, ys[i % NL].data_ptr(), stream)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n_sets):
+            run_step(i, side.cuda_stream)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+
+    def capture(count):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            st = torch.cuda.current_stream().cuda_stream
+            for i in range(count):
+                run_step(i % n_sets, st)
+        return g
+
+    full = capture(n_sets)
+    reps = max(1, steps // n_sets)
+    steps = reps * n_sets
+    for _ in range(max(1, warmup // n_sets)):
+        full.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        full.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    ms_per_step = total_ms / steps
+
+    # per-stage kernel durations: timing-only events recorded by the library
+    # between its kernels, over kernel_steps eager forwards
+    KT = min(kernel_steps, n_sets)
+    events = [[hip.event() for _ in range(moeq.MOEQ_STAGE_EVENTS)] for _ in range(KT)]
+    stream = torch.cuda.current_stream().cuda_stream
+    for j in range(KT):
+        moeq.moeq_set_stage_events(layers[j % NL][0].handle, events[j])
+        run_step(j, stream)
+    for L, *_ in layers:
+        moeq.moeq_set_stage_events(L.handle, None)
+    torch.cuda.synchronize()
+    stage_ms = np.array([[hip.elapsed_ms(ev[q], ev[q + 1]) for q in range(4)] for ev in events])
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    if path is not None:
+        for L, *_ in layers:
+            L.set_path(moeq.MOEQ_PATH_AUTO)
+    stage_mean = stage_ms.mean(axis=0)
+    mean_step_bytes = float(np.mean(gu_bytes) + np.mean(down_bytes) + io_bytes)
+    gu_launch = float(np.mean(gu_bytes[:KT]))
+    dn_launch = float(np.mean(down_bytes[:KT]))
+    return {
+        "tokens_per_s": steps * B / (total_ms * 1e-3), "ms_per_step": ms_per_step, "steps": steps,
+        "bytes_per_step": mean_step_bytes, "GBps": mean_step_bytes / (ms_per_step * 1e-3) / 1e9,
+        "distinct_experts_per_step": float(np.mean(n_exp)),
+        "stage_ms": stage_mean,
+        "gu_launch_bytes": gu_launch, "dn_launch_bytes": dn_launch,
+        "gu_GBps": gu_launch / (stage_mean[1] * 1e-3) / 1e9, "dn_GBps": dn_launch / (stage_mean[2] * 1e-3) / 1e9,
+    }
+
+
+def stack_leg(torch, np, moeq, synth, hip, steps, n_layers=58):
+    """58 independent layers of the V3 decode shape (per-tensor widths from
+    {2,3,4} with p = 0.7, 0.1, 0.2), batch 1: one step is the 58 layer
+    forwards in sequence, each on its own x and logits."""
+    shape = synth.V3
+    t0 = time.perf_counter()
+    layers = [random_layer(torch, moeq, synth, shape, "p234_701020", f"bench-stack-{li}", max_tokens=1)
+              for li in range(n_layers)]
+    build_s = time.perf_counter() - t0
+    resident = sum(L.bytes()[0] for L, *_ in layers)
+    r = decode_leg(torch, np, moeq, synth, hip, shape, layers, 1, 2, max(steps, 2 * n_layers), n_layers,
+                   n_layers, "bench-stack")
+    per_stack_ms = r["ms_per_step"] * n_layers
+    out = {"workload": f"{n_layers} independent V3-shape layers (192 of 256 experts kept each), batch 1, "
+                       "per-tensor widths from {2,3,4} with p = (0.7, 0.1, 0.2), random codes",
+           "resident_weight_GB": round(resident / 1e9, 2), "build_s": round(build_s, 1),
+           "ms_per_stack_step": round(per_stack_ms, 4), "tokens_per_s": round(1e3 / per_stack_ms, 1),
+           "bytes_per_stack_step_GB": round(r["bytes_per_step"] * n_layers / 1e9, 3),
+           "GBps": round(r["GBps"], 1), "hbm_frac": round(r["GBps"] / HBM_PEAK_GBPS, 4),
+           "layer_forwards_timed": r["steps"]}
+    for L, *_ in layers:
+        L.close()
+    return out
+
+
+def sweep_leg(torch, np, moeq, synth, hip, steps):
+    """Decode-path sweep: kept experts {256, 192, 128} x widths {uniform 2,
+    uniform 4, mixed (shared 4-bit, routed 2-bit)} x tokens {1, 16, 64} x
+    routing {N(0,1) logits, Zipf(1.1)}."""
+    import dataclasses
+    rows = []
+    for kept in (256, 192, 128):
+        shape = dataclasses.replace(synth.V3, n_kept=kept)
+        for plan in ("all2", "all4", "mixed"):
+            layer = random_layer(torch, moeq, synth, shape, plan, f"bench-sweep-{kept}-{plan}", max_tokens=64)
+            for n in (1, 16, 64):
+                for zipf in (False, True):
+                    r = decode_leg(torch, np, moeq, synth, hip, shape, [layer], n, 32, steps, 32, 32,
+                                   f"bench-sweep-{kept}-{plan}-{n}-{int(zipf)}", zipf=zipf,
+                                   path=moeq.MOEQ_PATH_DECODE)
+                    rows.append({"kept": kept, "bits": plan, "tokens": n, "routing": "zipf" if zipf else "normal",
+                                 "tokens_per_s": round(r["tokens_per_s"], 1), "us_per_step": round(r["ms_per_step"] * 1e3, 2),
+                                 "distinct_experts": round(r["distinct_experts_per_step"], 1),
+                                 "GBps": round(r["GBps"], 1), "hbm_frac": round(r["GBps"] / HBM_PEAK_GBPS, 4)})
+            layer[0].close()
+    return rows
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -252,115 +446,27 @@ def main():
         print(json.dumps({"prefill": prefill_bench(torch, np, moeq, synth, hip, max(1, args.prefill_steps))}),
               flush=True)
         return
+    if args.mode == "stack":
+        print(json.dumps({"stack": stack_leg(torch, np, moeq, synth, hip, args.steps)}), flush=True)
+        return
+    if args.mode == "sweep":
+        print(json.dumps({"sweep": sweep_leg(torch, np, moeq, synth, hip, args.steps)}), flush=True)
+        return
 
-    layers = []
-    for li in range(NL):
-        layer, mask, bits_r, bits_s = build_layer(torch, moeq, synth, shape, "gu3_d4_sh4",
-                                                  f"bench-layer-{li}", max_tokens=max(B, 1))
-        layers.append((layer, mask, bits_r, bits_s))
+    layers = [build_layer(torch, moeq, synth, shape, "gu3_d4_sh4", f"bench-layer-{li}", max_tokens=64)
+              for li in range(NL)]
     resident = sum(L.bytes()[0] for L, *_ in layers)
-
-    # inputs resident in HBM; step s uses layer s % NL and set s % R
-    n_sets = R * NL
-    xs, lgs = [], []
-    for i in range(n_sets):
-        xb = synth.activations(B, shape.hidden, "bench-x", i)
-        xs.append(torch.from_numpy(xb.view(np.int16)).cuda().view(torch.bfloat16))
-        lgs.append(torch.from_numpy(synth.normal_logits(B, shape.n_experts, "bench-l", i)).cuda())
-    ys = [torch.empty((B, shape.hidden), device="cuda") for _ in range(NL)]
-
-    # algorithmic bytes of each step: distinct tensors it touches
-    gu_bytes, down_bytes = [], []
-    for i in range(n_sets):
-        layer, mask, bits_r, bits_s = layers[i % NL]
-        idx, _ = layer.route(lgs[i])
-        experts = np.unique(idx.cpu().numpy())
-        g = sum(tensor_bytes(shape, int(bits_r[e, 0]), 0) + tensor_bytes(shape, int(bits_r[e, 1]), 1)
-                for e in experts)
-        d = sum(tensor_bytes(shape, int(bits_r[e, 2]), 2) for e in experts)
-        for s in range(shape.n_shared):
-            g += tensor_bytes(shape, int(bits_s[s, 0]), 0) + tensor_bytes(shape, int(bits_s[s, 1]), 1)
-            d += tensor_bytes(shape, int(bits_s[s, 2]), 2)
-        gu_bytes.append(g)
-        down_bytes.append(d)
-    io_bytes = B * (shape.hidden * 2 + shape.n_experts * 4 + shape.hidden * 4)
-    step_bytes = [g + d + io_bytes for g, d in zip(gu_bytes, down_bytes)]
-
-    def run_step(i, stream):
-        layer = layers[i % NL][0]
-        moeq.moeq_forward(layer.handle, xs[i].data_ptr(), lgs[i].data_ptr(), B,
-                          ys[i % NL].data_ptr(), stream)
-
-    # capture all n_sets steps in one graph (plus one for a remainder)
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        for i in range(n_sets):
-            run_step(i, side.cuda_stream)
-    torch.cuda.current_stream().wait_stream(side)
-    torch.cuda.synchronize()
-
-    def capture(count):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            st = torch.cuda.current_stream().cuda_stream
-            for i in range(count):
-                run_step(i, st)
-        return g
-
-    full = capture(n_sets)
-    rem = args.steps % n_sets
-    part = capture(rem) if rem else None
-
-    def run(steps):
-        for _ in range(steps // n_sets):
-            full.replay()
-        if steps % n_sets:
-            (part if steps % n_sets == rem and part is not None else capture(steps % n_sets)).replay()
-
-    run(args.warmup)
-    torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record()
-    run(args.steps)
-    t1.record()
-    torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
-    ms_per_step = total_ms / args.steps
-    mean_step_bytes = float(np.mean([step_bytes[i % n_sets] for i in range(args.steps)]))
-
-    # per-stage durations: eager forwards with events recorded by the library
-    KT = args.kernel_steps
-    events = [[hip.event() for _ in range(moeq.MOEQ_STAGE_EVENTS)] for _ in range(KT)]
-    stream = torch.cuda.current_stream().cuda_stream
-    for j in range(KT):
-        layer = layers[j % NL][0]
-        moeq.moeq_set_stage_events(layer.handle, events[j])
-        run_step(j % n_sets, stream)
-    for L, *_ in layers:
-        moeq.moeq_set_stage_events(L.handle, None)
-    torch.cuda.synchronize()
-    stage_ms = np.array([[hip.elapsed_ms(ev[s], ev[s + 1]) for s in range(4)] for ev in events])
-    for ev in events:
-        for e in ev:
-            hip.destroy(e)
-    stage_mean = stage_ms.mean(axis=0)
-    gu_launch_bytes = float(np.mean([gu_bytes[j % n_sets] for j in range(KT)]))
-    down_launch_bytes = float(np.mean([down_bytes[j % n_sets] for j in range(KT)]))
-    gu_gbps = gu_launch_bytes / (stage_mean[1] * 1e-3) / 1e9
-    down_gbps = down_launch_bytes / (stage_mean[2] * 1e-3) / 1e9
-
-    tokens_per_s = args.steps * B / (total_ms * 1e-3)
-    step_gbps = mean_step_bytes / (ms_per_step * 1e-3) / 1e9
+    r = decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, args.steps, args.warmup,
+                   args.kernel_steps, "bench")
+    st = r["stage_ms"]
     out = {
         "metric": METRIC,
-        "value": round(tokens_per_s, 1),
+        "value": round(r["tokens_per_s"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": r["steps"],
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": round(r["ms_per_step"], 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -374,17 +480,24 @@ def main():
             "layers_rotated": NL, "input_sets_per_layer": R, "graph_replay": True,
             "resident_weight_GB": round(resident / 1e9, 3),
         },
-        "effective_weight_GBps": round(step_gbps, 1),
-        "hbm_frac": round(step_gbps / HBM_PEAK_GBPS, 4),
-        "bytes_per_step": int(mean_step_bytes),
-        "stage_us": {"route_bucket": round(stage_mean[0] * 1e3, 2), "gate_up": round(stage_mean[1] * 1e3, 2),
-                     "down": round(stage_mean[2] * 1e3, 2), "combine": round(stage_mean[3] * 1e3, 2)},
-        "down_GBps": round(down_gbps, 1),
+        "effective_weight_GBps": round(r["GBps"], 1),
+        "hbm_frac": round(r["GBps"] / HBM_PEAK_GBPS, 4),
+        "bytes_per_step": int(r["bytes_per_step"]),
+        "stage_us": {"route_bucket": round(st[0] * 1e3, 2), "gate_up": round(st[1] * 1e3, 2),
+                     "down": round(st[2] * 1e3, 2), "combine": round(st[3] * 1e3, 2)},
+        "down_GBps": round(r["dn_GBps"], 1),
         "roofline": {"bound": "hbm", "kernel": "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)",
-                     "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "bytes_per_launch": int(gu_launch_bytes)},
+                     "achieved": round(r["gu_GBps"], 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "bytes_per_launch": int(r["gu_launch_bytes"])},
     }
+    if args.mode == "all" and args.b16_steps > 0:
+        r16 = decode_leg(torch, np, moeq, synth, hip, shape, layers, 16, 16, args.b16_steps, 64, 64, "bench-b16")
+        out["decode_b16"] = {"tokens_per_s": round(r16["tokens_per_s"], 1),
+                             "us_per_step": round(r16["ms_per_step"] * 1e3, 2),
+                             "distinct_experts_per_step": round(r16["distinct_experts_per_step"], 1),
+                             "bytes_per_step": int(r16["bytes_per_step"]), "GBps": round(r16["GBps"], 1),
+                             "hbm_frac": round(r16["GBps"] / HBM_PEAK_GBPS, 4)}
     for L, *_ in layers:
         L.close()
     if args.mode == "all" and args.prefill_steps > 0:

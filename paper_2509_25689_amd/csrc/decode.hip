@@ -76,22 +76,29 @@ struct Slot {
   int shared;   // shared expert index, or -1
 };
 
-__device__ __forceinline__ bool slot_info(const DecodeArgs& a, int slot, Slot& s) {
+// The slot's bucket; M = -1 for a slot beyond the active count.
+__device__ __forceinline__ Slot slot_info(const DecodeArgs& a, int slot) {
+  Slot s;
   if (slot < a.S) {
     s.desc = a.E + slot;
     s.M = a.n;
     s.base = a.n * a.k + slot * a.n;
     s.shared = slot;
-    return true;
+    return s;
   }
   const int i = slot - a.S;
-  if (i >= a.active[0]) return false;
+  s.shared = -1;
+  if (i >= a.active[0]) {
+    s.desc = 0;
+    s.M = -1;
+    s.base = 0;
+    return s;
+  }
   const int e = a.active[1 + i];
   s.desc = e;
   s.base = a.offsets[e];
   s.M = a.offsets[e + 1] - s.base;
-  s.shared = -1;
-  return true;
+  return s;
 }
 
 // One block's contribution for one token: d * sum_i (c_i - z) x_i, from the
@@ -206,7 +213,7 @@ __device__ __forceinline__ void compute_gateup(const GateUpRows<BG, BU>& b, bool
 }
 
 template <int BG, int BU, int LPR, int TM, int RW, int NBUF>
-__device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl, const TensorDev& tg,
+__device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
                                             const TensorDev& tu, uint32_t* smem) {
   const int H = a.H, I = a.I, U = H / kUnit;
   const int xts = U * kXStride, sts = U * 4;  // per-token LDS strides (dwords, floats)
@@ -223,8 +230,10 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl,
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
     const int mc = min(TM, sl.M - m0);
     asm volatile("" ::: "memory");  // weight loads stay inside the chunk loop
+    // the first NBUF row steps are requested before x is staged, so the
+    // staging latency overlaps the weight traffic
 #pragma unroll
-    for (int st = 0; st < NBUF - 1; ++st)
+    for (int st = 0; st < NBUF; ++st)
       if (st < RW && uok && row0 + st * GPW < I) load_gateup(buf[st], tg, tu, row0 + st * GPW, U, u, H);
     __syncthreads();
     // stage the chunk's x rows: 16-byte pieces, 4 per block of 32
@@ -246,17 +255,18 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl,
     __syncthreads();
     const uint32_t* xu = xl + u * kXStride;
     const float* su4 = xs + u * 4;
-    // groups of NBUF steps: buffer indices are static inside a group
+    // groups of NBUF steps: buffer indices are static inside a group; step st
+    // is reduced from buffer st % NBUF, which then takes step st + NBUF
 #pragma unroll 1
     for (int g0 = 0; g0 < RW; g0 += NBUF) {
       asm volatile("" ::: "memory");
 #pragma unroll
       for (int b = 0; b < NBUF; ++b) {
         const int st = g0 + b;
-        const int rn = row0 + (st + NBUF - 1) * GPW;
-        if (st + NBUF - 1 < RW && uok && rn < I) load_gateup(buf[(b + NBUF - 1) % NBUF], tg, tu, rn, U, u, H);
         const int r = row0 + st * GPW;
         if (r < I) compute_gateup<BG, BU, LPR, TM>(buf[b], uok, xu, su4, xts, sts, mc, u, sl.base + m0, r, a);
+        const int rn = row0 + (st + NBUF) * GPW;
+        if (st + NBUF < RW && uok && rn < I) load_gateup(buf[b], tg, tu, rn, U, u, H);
       }
     }
   }
@@ -266,8 +276,8 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot& sl,
 template <int LPR, int TM, int RW, int NBUF>
 __global__ __launch_bounds__(256, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
-  Slot sl;
-  if (!slot_info(a, blockIdx.y, sl)) return;
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   switch (tg.bits * 8 + tu.bits) {
@@ -302,7 +312,7 @@ __device__ __forceinline__ void load_down(DownRows<BD>& b, const TensorDev& td, 
 template <int BD, int LPR, int TM>
 __device__ __forceinline__ void compute_down(const DownRows<BD>& b, bool active, const uint32_t* xu,
                                              const float* su4, int xts, int sts, int lo, int mc, int u,
-                                             const Slot& sl, int m0, int row, const DecodeArgs& a) {
+                                             const Slot sl, int m0, int row, const DecodeArgs& a) {
   float o[TM];
 #pragma unroll
   for (int m = 0; m < TM; ++m) o[m] = 0.0f;
@@ -339,7 +349,7 @@ __device__ __forceinline__ void compute_down(const DownRows<BD>& b, bool active,
 }
 
 template <int BD, int LPR, int TM, int RW, int NBUF>
-__device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, const TensorDev& td,
+__device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot sl, const TensorDev& td,
                                           uint32_t* smem) {
   const int H = a.H, I = a.I, U = I / kUnit;
   const int xts = 2 * U * kXStride, sts = U * 4, lo = U * kXStride;
@@ -357,7 +367,7 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, c
     const int mc = min(TM, sl.M - m0);
     asm volatile("" ::: "memory");  // weight loads stay inside the chunk loop
 #pragma unroll
-    for (int st = 0; st < NBUF - 1; ++st)
+    for (int st = 0; st < NBUF; ++st)
       if (st < RW && uok && row0 + st * GPW < H) load_down(buf[st], td, row0 + st * GPW, U, u, I);
     __syncthreads();
     // stage h rows as bfloat16 hi + lo pairs; block sums of hi + lo
@@ -390,17 +400,16 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, c
     __syncthreads();
     const uint32_t* xu = xl + u * kXStride;
     const float* su4 = xs + u * 4;
-    // groups of NBUF steps: buffer indices are static inside a group
 #pragma unroll 1
     for (int g0 = 0; g0 < RW; g0 += NBUF) {
       asm volatile("" ::: "memory");
 #pragma unroll
       for (int b = 0; b < NBUF; ++b) {
         const int st = g0 + b;
-        const int rn = row0 + (st + NBUF - 1) * GPW;
-        if (st + NBUF - 1 < RW && uok && rn < H) load_down(buf[(b + NBUF - 1) % NBUF], td, rn, U, u, I);
         const int r = row0 + st * GPW;
         if (r < H) compute_down<BD, LPR, TM>(buf[b], uok, xu, su4, xts, sts, lo, mc, u, sl, m0, r, a);
+        const int rn = row0 + (st + NBUF) * GPW;
+        if (st + NBUF < RW && uok && rn < H) load_down(buf[b], td, rn, U, u, I);
       }
     }
   }
@@ -410,8 +419,8 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot& sl, c
 template <int LPR, int TM, int RW, int NBUF>
 __global__ __launch_bounds__(256, TM == 1 ? kDownMinBlocks : 2) void down_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
-  Slot sl;
-  if (!slot_info(a, blockIdx.y, sl)) return;
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
   switch (td.bits) {
