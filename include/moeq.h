@@ -200,6 +200,34 @@ moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits,
 moeq_status moeq_layer_bytes(const moeq_layer* layer, uint64_t* weight_bytes,
                              uint64_t* workspace_bytes);
 
+/* Expert importance and the pruning mask (Section 3.1): the statistics of the
+ * unpruned router over calibration tokens.  Every expert is kept for routing;
+ * cfg's grouped top-k fields and score_bias apply as in a forward.  For each
+ * expert e:
+ *   f_e    = (tokens that selected e) / n_tokens            (float32)
+ *   sbar_e = mean sigmoid score of e over those tokens, 0 if none (float32;
+ *            the scores are summed in float32 in token order)
+ *   I_e    = alpha * f_e + (1 - alpha) * sbar_e              (float64, two
+ *            products and one sum, each rounded)
+ * and mask_e = 1 for the ceil(retain * E) experts with the largest I_e (ties:
+ * lower id first; the product is taken with a 1e-9 tolerance so that e.g.
+ * 0.7 * 10 keeps 7).  The result is deterministic.
+ *   cfg         HOST; a valid layer configuration (its routing fields are used)
+ *   score_bias  HOST float [n_experts] or NULL (zeros); copied before return
+ *   logits      DEVICE float32 [n_tokens x n_experts], finite
+ *   n_tokens    1..2^24
+ *   alpha       in [0, 1]; retain in (0, 1]
+ *   importance  DEVICE double [n_experts] (written)
+ *   mask        DEVICE uint8 [n_experts] (written): usable as create's expert_mask
+ *   counts      DEVICE int32 [n_experts] (written) or NULL
+ * Scratch memory (about 16 * n_tokens * top_k bytes) is allocated and released
+ * in stream order; nothing synchronizes the host.
+ * Errors: INVALID_ARG (arguments, configuration, routing infeasible with all
+ * experts kept), OUT_OF_MEMORY (scratch), DEVICE. */
+moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,
+                                   int32_t n_tokens, double alpha, double retain, double* importance,
+                                   uint8_t* mask, int32_t* counts, void* stream);
+
 /* Benchmark instrumentation: stage boundaries of moeq_forward.
  *   events  NULL (count 0) to stop, or MOEQ_STAGE_EVENTS hipEvent_t handles
  *           (as void*) owned by the caller.  Every following moeq_forward on

@@ -436,6 +436,80 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   return ok();
 }
 
+moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,
+                                   int32_t n_tokens, double alpha, double retain, double* importance,
+                                   uint8_t* mask, int32_t* counts, void* stream) {
+  moeq_status st = check_config(cfg);
+  if (st != MOEQ_OK) return st;
+  const int E = cfg->n_experts, k = cfg->top_k;
+  if (n_tokens < 1 || n_tokens > (1 << 24))
+    return fail(MOEQ_ERR_INVALID_ARG, "n_tokens %d outside 1..2^24", n_tokens);
+  if (!logits || !importance || !mask)
+    return fail(MOEQ_ERR_INVALID_ARG, "logits, importance and mask must not be NULL");
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(MOEQ_ERR_INVALID_ARG, "alpha must lie in [0, 1]");
+  if (!(retain > 0.0 && retain <= 1.0)) return fail(MOEQ_ERR_INVALID_ARG, "retain must lie in (0, 1]");
+  if (score_bias)
+    for (int e = 0; e < E; ++e)
+      if (!isfinite(score_bias[e]) || fabsf(score_bias[e]) > 1e30f)
+        return fail(MOEQ_ERR_INVALID_ARG, "score_bias[%d] is not a finite value of magnitude <= 1e30", e);
+  {
+    std::vector<uint8_t> all(E, 1);
+    int kept = 0;
+    if ((st = check_routing(cfg, all.data(), &kept)) != MOEQ_OK) return st;
+  }
+  int keep = (int)std::ceil(retain * (double)E - 1e-9);
+  keep = keep < 1 ? 1 : keep > E ? E : keep;
+
+  hipStream_t s = (hipStream_t)stream;
+  const size_t nk = (size_t)n_tokens * k, chunks = ((size_t)n_tokens + kChunk - 1) / kChunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  const size_t o_idx = take(nk * 4), o_w = take(nk * 4), o_cc = take(chunks * E * 4), o_rank = take(nk * 4),
+               o_off = take((size_t)(E + 1) * 4), o_perm = take(nk * 4), o_act = take((size_t)(E + 1) * 4),
+               o_mask = take(E), o_bias = take((size_t)E * 4);
+  uint8_t* buf = nullptr;
+  hipError_t e = hipMallocAsync((void**)&buf, off, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync (importance scratch)");
+  Workspace ws{};
+  ws.idx = (int32_t*)(buf + o_idx);
+  ws.w = (float*)(buf + o_w);
+  ws.chunk_cnt = (int32_t*)(buf + o_cc);
+  ws.rank = (int32_t*)(buf + o_rank);
+  ws.offsets = (int32_t*)(buf + o_off);
+  ws.perm = (int32_t*)(buf + o_perm);
+  ws.active = (int32_t*)(buf + o_act);
+  uint8_t* all_kept = buf + o_mask;
+  float* bias = (float*)(buf + o_bias);
+  e = launch_fill_u8(all_kept, E, 1, s);
+  if (e == hipSuccess)
+    e = score_bias ? hipMemcpyAsync(bias, score_bias, (size_t)E * 4, hipMemcpyHostToDevice, s)
+                   : hipMemsetAsync(bias, 0, (size_t)E * 4, s);
+  RouterParams rp{};
+  rp.logits = logits;
+  rp.mask = all_kept;
+  rp.bias = bias;
+  rp.E = E;
+  rp.G = cfg->n_group;
+  rp.TG = cfg->topk_group;
+  rp.k = k;
+  rp.topn = cfg->group_topn;
+  rp.norm = 0;       // weights = sigmoid scores
+  rp.scale = 1.0f;
+  rp.x = nullptr;
+  if (e == hipSuccess) e = launch_route_tokens(rp, n_tokens, ws.idx, ws.w, s);
+  if (e == hipSuccess) e = launch_bucket_chunked(ws.idx, n_tokens, k, E, ws, s);
+  if (e == hipSuccess)
+    e = launch_expert_importance(ws.offsets, ws.perm, ws.w, E, n_tokens, alpha, keep, importance, mask, counts, s);
+  const hipError_t ef = hipFreeAsync(buf, s);
+  if (e != hipSuccess) return hip_fail(e, "expert importance");
+  if (ef != hipSuccess) return hip_fail(ef, "hipFreeAsync (importance scratch)");
+  return ok();
+}
+
 moeq_status moeq_set_stage_events(moeq_layer* L, void* const* events, int32_t count) {
   if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
   if (count == 0) {

@@ -108,6 +108,11 @@ struct DecodeArgs {
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
+// prune.hip
+hipError_t launch_fill_u8(uint8_t* p, int n, uint8_t v, hipStream_t s);
+hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm, const float* w, int E, int n,
+                                    double alpha, int keep, double* importance, uint8_t* mask, int32_t* counts,
+                                    hipStream_t s);
 // prefill.hip
 constexpr int kGemmBM = 128;  // tokens per grouped-GEMM m-tile
 int prefill_max_mtiles(int n, int k, int S, int n_kept);

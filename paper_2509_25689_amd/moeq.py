@@ -76,6 +76,8 @@ def _load():
         "moeq_quantize": [P, I32, I32, I32, P, P, P],
         "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
         "moeq_set_stage_events": [P, ctypes.POINTER(P), I32],
+        "moeq_expert_importance": [ctypes.POINTER(moeq_config), P, P, I32, ctypes.c_double, ctypes.c_double,
+                                   P, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -153,6 +155,30 @@ def moeq_set_stage_events(layer, events):
         return
     arr = (ctypes.c_void_p * len(events))(*events)
     _check(lib.moeq_set_stage_events(layer, arr, len(events)))
+
+
+def moeq_expert_importance(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask, counts=0,
+                           stream=0):
+    """cfg: moeq_config; score_bias: host address or 0; the rest device addresses (counts may be 0)."""
+    _check(lib.moeq_expert_importance(ctypes.byref(cfg), score_bias or None, logits, n_tokens, alpha, retain,
+                                      importance, mask, counts or None, stream or None))
+
+
+def expert_importance(shape, logits, *, alpha, retain, bias=None, stream=None):
+    """Router-statistics importance and pruning mask (Section 3.1) for calibration
+    logits (float32 CUDA tensor [n, E]) -> (importance float64, mask uint8, counts int32)."""
+    import numpy as np
+    import torch
+    n, E = logits.shape
+    cfg = make_config(shape, max_tokens=1)
+    imp = torch.empty(E, dtype=torch.float64, device=logits.device)
+    mask = torch.empty(E, dtype=torch.uint8, device=logits.device)
+    counts = torch.empty(E, dtype=torch.int32, device=logits.device)
+    b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    moeq_expert_importance(cfg, 0 if b is None else b.ctypes.data, logits.data_ptr(), n, float(alpha), float(retain),
+                           imp.data_ptr(), mask.data_ptr(), counts.data_ptr(),
+                           stream if stream is not None else torch.cuda.current_stream().cuda_stream)
+    return imp, mask, counts
 
 
 def moeq_layer_bytes(layer):

@@ -170,3 +170,32 @@ def test_error_text_is_per_call():
     with pytest.raises(moeq.MoeqError) as ei:
         moeq.moeq_set_path(None, 0)
     assert ei.value.status == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_expert_importance_validation():
+    """Every argument check of moeq_expert_importance runs before any HIP call."""
+    lib = moeq.lib
+    cfg = _cfg()
+    E = cfg.n_experts
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+
+    def call(c=cfg, bias=None, logits=fake, n=8, alpha=0.5, retain=0.75, imp=fake, mask=fake):
+        return lib.moeq_expert_importance(ctypes.byref(c) if c is not None else None, bias, logits, n,
+                                          alpha, retain, imp, mask, None, None)
+
+    assert call(c=None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(n=0) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(logits=None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(imp=None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(mask=None) == moeq.MOEQ_ERR_INVALID_ARG
+    for a in (-0.1, 1.5, float("nan")):
+        assert call(alpha=a) == moeq.MOEQ_ERR_INVALID_ARG
+    for r in (0.0, -1.0, 1.01, float("nan")):
+        assert call(retain=r) == moeq.MOEQ_ERR_INVALID_ARG
+    bad = np.zeros(E, np.float32)
+    bad[3] = np.inf
+    assert call(bias=bad.ctypes.data) == moeq.MOEQ_ERR_INVALID_ARG
+    assert "score_bias" in moeq.moeq_last_error()
+    # top_k larger than what topk_group groups can hold even with every expert kept
+    c2 = _cfg(topk_group=1, top_k=12)
+    assert call(c=c2) == moeq.MOEQ_ERR_INVALID_ARG
