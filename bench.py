@@ -35,6 +35,32 @@ METRIC = "V3-shape MoE layer decode tokens/s + effective weight GB/s vs HBM peak
 HBM_PEAK_GBPS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 
+# HBM bytes per gate/up launch at batch 1 from rocprofv3 FETCH_SIZE + WRITE_SIZE,
+# each scaled by the same counter's reading for a plain 1 GiB copy (factors
+# 2.0 and 1.0; see profiles/gateup_kernel_decode_b1_traffic.md).  Valid only for
+# the kernel sources the counters were taken on, identified by their sha256:
+# any change to them reports traffic as null until the counters are retaken.
+GATEUP_TRAFFIC = {
+    "bytes": 119717754,
+    "sources": {
+        "paper_2509_25689_amd/csrc/decode.hip": "4b5bda7843426ad6eab188fd34198b80d212e794d69eb78b84e0ff805338904c",
+        "paper_2509_25689_amd/csrc/layout.h": "0ffefc9dd183ff9cda73bcc28611268423cc9fb3b52cad4fdd0ff92acd1f3919",
+    },
+}
+
+
+def gateup_traffic():
+    """The measured traffic if the gate/up kernel is still the one measured, else None."""
+    import hashlib
+    for rel, digest in GATEUP_TRAFFIC["sources"].items():
+        try:
+            with open(os.path.join(ROOT, rel), "rb") as f:
+                if hashlib.sha256(f.read()).hexdigest() != digest:
+                    return None
+        except OSError:
+            return None
+    return GATEUP_TRAFFIC["bytes"]
+
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
@@ -48,6 +74,8 @@ def parse():
     p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
     p.add_argument("--prefill-steps", type=int, default=10, help="2048-token prefill forwards timed (0 = skip)")
     p.add_argument("--b16-steps", type=int, default=2560, help="16-token decode steps timed (0 = skip)")
+    p.add_argument("--k6-steps", type=int, default=2560,
+                   help="batch-1 decode steps timed with 6 experts per token (0 = skip)")
     p.add_argument("--mode", choices=("all", "decode", "prefill", "copy", "stack", "sweep"), default="all",
                    help="all: batch-1 decode line with 16-token, prefill and CPU legs; decode / prefill: "
                         "one leg only (for profiling); copy: a plain 1 GiB device copy whose HBM counters "
@@ -488,7 +516,7 @@ def main():
         "down_GBps": round(r["dn_GBps"], 1),
         "roofline": {"bound": "hbm", "kernel": "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)",
                      "achieved": round(r["gu_GBps"], 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": gateup_traffic() if B == 1 else None,
                      "bytes_per_launch": int(r["gu_launch_bytes"])},
     }
     if args.mode == "all" and args.b16_steps > 0:
@@ -500,6 +528,19 @@ def main():
                              "hbm_frac": round(r16["GBps"] / HBM_PEAK_GBPS, 4)}
     for L, *_ in layers:
         L.close()
+    if args.mode == "all" and args.k6_steps > 0:
+        # Section 3.2: after keeping r = 0.75 of the experts, ceil(r * 8) = 6 per token
+        import dataclasses
+        shape6 = dataclasses.replace(shape, top_k=6)
+        layers6 = [random_layer(torch, moeq, synth, shape6, "gu3_d4_sh4", f"bench-k6-{li}", max_tokens=1)
+                   for li in range(NL)]
+        r6 = decode_leg(torch, np, moeq, synth, hip, shape6, layers6, 1, R, args.k6_steps, 64, 64, "bench-k6")
+        out["decode_b1_k6"] = {"tokens_per_s": round(r6["tokens_per_s"], 1),
+                               "us_per_step": round(r6["ms_per_step"] * 1e3, 2),
+                               "bytes_per_step": int(r6["bytes_per_step"]), "GBps": round(r6["GBps"], 1),
+                               "hbm_frac": round(r6["GBps"] / HBM_PEAK_GBPS, 4)}
+        for L, *_ in layers6:
+            L.close()
     if args.mode == "all" and args.prefill_steps > 0:
         out["prefill"] = prefill_bench(torch, np, moeq, synth, hip, args.prefill_steps)
     if args.mode == "all" and args.cpu_steps > 0:

@@ -260,3 +260,39 @@ def test_device_resident_weights(gpu_lib):
     L = gpu_lib.Layer(data.shape, data.mask, routed, shared, max_tokens=16, device_weights=True)
     _forward_check(gpu_lib, data, L, 16, "device-weights", gpu_lib.MOEQ_PATH_AUTO)
     L.close()
+
+
+# ---------------------------------------------------------------------------
+# Section 3.2's activation adjustment: after keeping r = 0.75 of the experts,
+# each token activates ceil(r * 8) = 6 of them instead of 8.
+@pytest.fixture(scope="module")
+def v3_k6(gpu_lib):
+    import dataclasses
+    shape = dataclasses.replace(synth.V3, top_k=6)
+    data = layers.random_packed_layer(shape, "gu3_d4_sh4", "v3_k6")
+    L = _make_layer(gpu_lib, data, max_tokens=300)
+    yield data, L
+    L.close()
+
+
+@pytest.mark.parametrize("n", [1, 16, 100])
+def test_route_v3_k6(v3_k6, n):
+    data, L = v3_k6
+    logits = synth.normal_logits(n, data.shape.n_experts, "route-k6", n)
+    idx, w = L.route(_dev(logits))
+    ref_idx, ref_w = _route_oracle(data.shape, data.mask, logits)
+    assert idx.shape[1] == 6
+    assert np.array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_allclose(w.cpu().numpy(), ref_w, atol=1e-6 * data.shape.routed_scale)
+
+
+def test_forward_v3_k6_decode(gpu_lib, v3_k6):
+    data, L = v3_k6
+    err = _forward_check(gpu_lib, data, L, 1, "fwd-k6-b1", gpu_lib.MOEQ_PATH_AUTO)
+    assert err.max() < 1e-4
+    _forward_check(gpu_lib, data, L, 16, "fwd-k6-b16", gpu_lib.MOEQ_PATH_AUTO, sample=[0, 9, 15])
+
+
+def test_forward_v3_k6_prefill(gpu_lib, v3_k6):
+    data, L = v3_k6
+    _forward_check(gpu_lib, data, L, 300, "fwd-k6-prefill", gpu_lib.MOEQ_PATH_PREFILL, sample=[0, 150, 299])
