@@ -462,6 +462,143 @@ __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
   reinterpret_cast<float4*>(a.y)[i] = acc;
 }
 
+// ---------------------------------------------------------------------------
+// One token: gate/up + SwiGLU with 16 lanes per row pair.  Lanes 0-7 of a
+// 16-lane group stream the gate row and lanes 8-15 the up row; lane j of a
+// half walks the units j, j + 8, j + 16, ... of its row, so all lanes are
+// busy for any number of units, and the per-row work (sums, activation,
+// store) is spread over several units per lane.  The codes of unit i + 1 are
+// in flight while unit i is reduced.  A half sums its lanes with DPP (quad
+// butterflies, then the half-row mirror); the up half's last lane receives
+// the gate total across the row (row_ror:8) and writes h.
+template <int B>
+struct UnitBuf {
+  uint32_t w[4 * B];
+  u32x2 s;
+};
+
+template <int B>
+__device__ __forceinline__ void load_unit_buf(UnitBuf<B>& b, const TensorDev& t, int row, int U, int u, int K) {
+  load_unit<B>(t.codes + (size_t)row * B * U * 4, U, u, b.w);
+  b.s = *gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (K / kBlock) + 4 * u));
+}
+
+// d * sum (c - z) x over one 128-weight unit, for the token staged at xu / su4
+template <int B>
+__device__ __forceinline__ float unit_dot(const UnitBuf<B>& b, const uint32_t* xu, const float* su4, float acc) {
+  const PairConsts pk = pair_consts();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t p[16];
+    block_pairs<B>(b.w + q * B, pk, p);
+    acc = block_dot<1>(p, xu + 16 * q, 0, block_scale<B>(b.s, q), su4[q], acc);
+  }
+  return acc;
+}
+
+__device__ __forceinline__ float half_sum8(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror: the other quad of the half row
+  return v;
+}
+
+// the half's partial dot over its units (units j, j + 8, ... of row `row`);
+// GU1_DEPTH units are in flight while one is reduced
+#ifndef MOEQ_GU1_DEPTH
+#define MOEQ_GU1_DEPTH 2
+#endif
+#ifndef MOEQ_GU1_MINBLOCKS
+#define MOEQ_GU1_MINBLOCKS 5
+#endif
+template <int B>
+__device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U, int j, int H, const uint32_t* xl,
+                                              const float* xs) {
+  constexpr int NB = MOEQ_GU1_DEPTH;
+  const int UPL = (U + 7) / 8;
+  UnitBuf<B> buf[NB];
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < NB - 1; ++i) load_unit_buf<B>(buf[i], t, row, U, min(j + 8 * min(i, UPL - 1), U - 1), H);
+#pragma unroll 1
+  for (int i0 = 0; i0 < UPL; i0 += NB) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int i = i0 + b;
+      if (i < UPL) {
+        // unit i + NB - 1 (clamped to the last valid one) goes out before unit i is reduced
+        load_unit_buf<B>(buf[(b + NB - 1) % NB], t, row, U, min(j + 8 * min(i + NB - 1, UPL - 1), U - 1), H);
+        const int u = j + 8 * i;
+        if (u < U) acc = unit_dot<B>(buf[b], xl + u * kXStride, xs + u * 4, acc);
+      }
+    }
+  }
+  return acc;
+}
+
+template <int BG, int BU>
+__device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
+                                             const TensorDev& tu, const uint32_t* xl, const float* xs) {
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 16 + wave * 4 + (lane >> 4);
+  const bool up = (lane & 8) != 0;
+  const int j = lane & 7;
+  const int rowc = min(row, I - 1);
+  float v;
+  if constexpr (BG == BU) {
+    v = row_half_dot<BG>(up ? tu : tg, rowc, U, j, H, xl, xs);
+  } else {
+    if (up)
+      v = row_half_dot<BU>(tu, rowc, U, j, H, xl, xs);
+    else
+      v = row_half_dot<BG>(tg, rowc, U, j, H, xl, xs);
+  }
+  v = half_sum8(v);
+  const float other = dpp_f<0x128>(v);  // row_ror:8: the other half's total
+  if ((lane & 15) == 15 && row < I) a.h[(size_t)sl.base * a.I + row] = silu(other) * v;
+}
+
+// grid = (I / 16, S + max_active), 256 threads; n = 1
+__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  const int H = a.H, U = H / kUnit;
+  uint32_t* xl = smem;
+  float* xs = reinterpret_cast<float*>(smem + U * kXStride);
+  // stage the token's x with per-block sums (16-byte pieces, 4 per block)
+  const int t = sl.shared >= 0 ? 0 : a.perm[sl.base] / a.k;
+  const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
+  for (int q = threadIdx.x; q < H / 8; q += 256) {
+    const u32x4 v = src[q];
+    float s = 0.0f;
+    s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
+    s += bf16_lo(v.z); s += bf16_hi(v.z); s += bf16_lo(v.w); s += bf16_hi(v.w);
+    s += __shfl_xor(s, 1, 64);
+    s += __shfl_xor(s, 2, 64);
+    const int uu = q >> 4, cq = q & 15;
+    *reinterpret_cast<u32x4*>(xl + uu * kXStride + cq * 4) = v;
+    if ((cq & 3) == 0) xs[uu * 4 + (cq >> 2)] = s;
+  }
+  __syncthreads();
+  switch (tg.bits * 8 + tu.bits) {
+    case 2 * 8 + 2: gateup1_body<2, 2>(a, sl, tg, tu, xl, xs); break;
+    case 2 * 8 + 3: gateup1_body<2, 3>(a, sl, tg, tu, xl, xs); break;
+    case 2 * 8 + 4: gateup1_body<2, 4>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 2: gateup1_body<3, 2>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 3: gateup1_body<3, 3>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 4: gateup1_body<3, 4>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 2: gateup1_body<4, 2>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 3: gateup1_body<4, 3>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 4: gateup1_body<4, 4>(a, sl, tg, tu, xl, xs); break;
+    default: break;
+  }
+}
+
 // Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
 // rows of one slot.
 
@@ -506,7 +643,14 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
-  return a.n == 1 ? launch_gateup_tm<1>(a, s) : launch_gateup_tm<4>(a, s);
+  if (a.n == 1) {
+    const int U = a.H / kUnit;
+    const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
+    dim3 grid((a.I + 15) / 16, a.S + a.max_active);
+    gateup1_kernel<<<grid, 256, lds, s>>>(a);
+    return hipGetLastError();
+  }
+  return launch_gateup_tm<4>(a, s);
 }
 
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {
