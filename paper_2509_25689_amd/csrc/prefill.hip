@@ -15,12 +15,12 @@
 //
 // Workgroup tile: 128 rows (tokens) x 128 output features (per projection;
 // gate/up computes both projections of the same features so SwiGLU is fused
-// into the epilogue), K step 64, four waves in a 2 x 2 arrangement, each
-// owning a 64 x 64 block of 4 x 4 MFMA tiles.  LDS holds two decoded K steps
-// and registers the raw data of the next two, so the decode of one step and
-// the loads of later ones overlap the current step's MFMAs.  Workgroup ids
-// are remapped so that consecutive tiles of one expert land on one XCD and
-// share its L2.
+// into the epilogue), K step 64, eight waves (two per SIMD) in a 2 x 4
+// arrangement, each owning 64 rows x 32 columns of 16 x 16 MFMA tiles.  LDS
+// holds two decoded K steps and registers the raw data of the next two, so
+// the decode of one step and the loads of later ones overlap the current
+// step's MFMAs.  Workgroup ids are remapped so that consecutive tiles of one
+// expert land on one XCD and share its L2.
 #include "internal.h"
 #include "layout.h"
 
@@ -106,32 +106,10 @@ __device__ __forceinline__ int xcd_logical(int hw, int total) {
   return xcd < extra ? xcd * (per + 1) + idx : extra * (per + 1) + (xcd - extra) * per + idx;
 }
 
-// ---- weight tile decode: one thread, one row, two blocks (64 weights) ----
-// The raw codes of half a unit (2*B dwords starting at dword 2*B*hs of the
-// unit) come from the two 16-byte chunks c0 = (2*B*hs)/4 and c1 = min(c0+1,
-// B-1) of the unit; they are kept as loaded (no selection at load time, so
-// the loads stay in flight) and picked apart when the tile is decoded.
-struct Raw {
-  u32x4 a, b;
-  uint32_t sc;  // the two binary16 scales of the half unit
-};
-
 // Row-base pointer of a tensor row in the device layout.
 __device__ __forceinline__ const MOEQ_GLOBAL u32x4* row_chunks(const TensorDev& t, int bits, int row) {
   const int U = t.K / kUnit;
   return gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)row * bits * U * 4));
-}
-
-// Half unit hs of unit u of a row (its blocks 4u + 2hs, 4u + 2hs + 1).
-__device__ __forceinline__ Raw load_raw(const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL uint32_t* rs, int U,
-                                        int bits, int u, int hs) {
-  const int c0 = (2 * bits * hs) >> 2;
-  const int c1 = min(c0 + 1, bits - 1);
-  Raw r;
-  r.a = rc[(size_t)c0 * U + u];
-  r.b = rc[(size_t)c1 * U + u];
-  r.sc = rs[2 * u + hs];
-  return r;
 }
 
 // (c_lo, c_hi) at bit offset s of each half -> binary16 pair d * (c - z), exact
@@ -143,79 +121,12 @@ __device__ __forceinline__ uint32_t dq_pair(uint32_t w, uint32_t mask, uint32_t 
   return __builtin_bit_cast(uint32_t, c * d2);          // rounded once
 }
 
-// Decodes the half unit in r (width B, half HS) to 64 binary16 values at dst.
-template <int B, int HS>
-__device__ __forceinline__ void decode_raw(const Raw& r, _Float16* dst) {
-  const uint32_t all[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
-  constexpr int o = (B == 3 && HS) ? 2 : 0;  // first dword of the half unit within chunk c0
-  uint32_t mask, base;
-  asm("v_mov_b32 %0, 0x64006400" : "=v"(base));
-  if constexpr (B == 4) asm("v_mov_b32 %0, 0x000F000F" : "=v"(mask));
-  if constexpr (B == 3) asm("v_mov_b32 %0, 0x00070007" : "=v"(mask));
-  if constexpr (B == 2) asm("v_mov_b32 %0, 0x00030003" : "=v"(mask));
-  const _Float16 zf = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
-  const half2_t zb = {zf, zf};
-#pragma unroll
-  for (int blk = 0; blk < 2; ++blk) {
-    const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)(r.sc >> (16 * blk)));
-    const half2_t d2 = {d, d};
-    const uint32_t* w = all + o + blk * B;
-    uint32_t p[16];
-    if constexpr (B == 4) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        p[4 * q + 0] = dq_pair<0>(w[q], mask, base, zb, d2);
-        p[4 * q + 1] = dq_pair<4>(w[q], mask, base, zb, d2);
-        p[4 * q + 2] = dq_pair<8>(w[q], mask, base, zb, d2);
-        p[4 * q + 3] = dq_pair<12>(w[q], mask, base, zb, d2);
-      }
-    } else if constexpr (B == 2) {
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-#pragma unroll
-        for (int f = 0; f < 8; ++f) p[8 * q + f] = dq_pair<0>(w[q] >> (2 * f), mask, base, zb, d2);
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 3; ++q) {
-#pragma unroll
-        for (int f = 0; f < 5; ++f) p[5 * q + f] = dq_pair<0>(w[q] >> (3 * f), mask, base, zb, d2);
-      }
-      // weights 30, 31: bit q of each in bit 15 / 31 of dword q
-      uint32_t m1, m2, m4;
-      asm("v_mov_b32 %0, 0x00010001" : "=v"(m1));
-      asm("v_mov_b32 %0, 0x00020002" : "=v"(m2));
-      asm("v_mov_b32 %0, 0x00040004" : "=v"(m4));
-      uint32_t t = and_or(w[0] >> 15, m1, base);
-      t = and_or(w[1] >> 14, m2, t);
-      t = and_or(w[2] >> 13, m4, t);
-      const half2_t c = __builtin_bit_cast(half2_t, t) + zb;
-      p[15] = __builtin_bit_cast(uint32_t, c * d2);
-    }
-    u32x4* out = reinterpret_cast<u32x4*>(dst + blk * 32);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = u32x4{p[4 * i], p[4 * i + 1], p[4 * i + 2], p[4 * i + 3]};
-  }
-}
-
-// ---- activation tile rows ----
-// 32 binary16 values (already prescaled) from registers into an LDS row
-__device__ __forceinline__ void store_row32(const u32x4 (&v)[4], _Float16* dst) {
-  u32x4* d = reinterpret_cast<u32x4*>(dst);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) d[i] = v[i];
-}
-
 __device__ __forceinline__ half8 lds_frag(const _Float16* p) {
   return *reinterpret_cast<const half8*>(p);
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
 
-// ---------------------------------------------------------------------------
-// gate/up grouped GEMM + SwiGLU.  Thread roles in the load phase: thread t
-// decodes half a unit of row (t & 127) of tensor (t >> 7) and converts 32
-// activations of tile row (t >> 1).
 // Field copies of the kernel arguments the GEMM bodies use (passing the
 // argument struct by reference would place it in scratch memory).
 struct GemmArgs {
@@ -249,43 +160,6 @@ __device__ __forceinline__ GemmArgs gemm_args(const DecodeArgs& a) {
   return g;
 }
 
-// A/B fragments of one K step (two MFMA K slices of 32) of a wave's 64 x 64
-// block, for NT weight tensors that share the activation fragments.
-template <int NT>
-struct Frags {
-  half8 a[2][4];
-  half8 b[2][NT][4];
-};
-
-template <int NT>
-__device__ __forceinline__ void read_frags(const _Float16* A, const _Float16* W, int lane, int wm, int wn,
-                                           Frags<NT>& f) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int kof = kk * 32 + (lane >> 4) * 8;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) f.a[kk][i] = lds_frag(A + (wm * 64 + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        f.b[kk][t][c] = lds_frag(W + (t * BN + wn * 64 + 16 * c + (lane & 15)) * LDS_STRIDE + kof);
-  }
-}
-
-template <int NT>
-__device__ __forceinline__ void mfmas(const Frags<NT>& f, f32x4v (&acc)[NT][4][4]) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          acc[t][i][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(f.a[kk][i], f.b[kk][t][c], acc[t][i][c], 0, 0, 0);
-}
-
 // Scheduling hint for one pipelined K step: the fragment reads first, then
 // the step's MFMAs each followed by a few VALU instructions of the next
 // step's decode (and its LDS writes), so that the matrix core and the vector
@@ -300,141 +174,6 @@ __device__ __forceinline__ void interleave_hint() {
     if (i % (NMFMA / NWRITE) == NMFMA / NWRITE - 1) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
     if (i == NMFMA / 2) __builtin_amdgcn_sched_group_barrier(0x020, 16, 0);  // VMEM read
   }
-}
-
-// The pipelined K loop of the gate/up GEMM for a wave whose weight rows have
-// width B.  LDS holds two decoded K steps (double buffer), registers hold the
-// raw data of the next two steps.  While step s is multiplied, step s+1 is
-// decoded into the other LDS buffer and the loads of step s+3 go into the
-// register slot just consumed.  Step s uses register slot and LDS buffer
-// s % 2, and half unit s % 2 of unit s / 2.  nk is even (H is a multiple of
-// 128); loads and decodes are unconditional (the last ones repeat the final
-// steps into buffers nobody reads again) so that every K step is one basic
-// block and the wait counts stay exact.
-template <int B>
-__device__ __forceinline__ void gateup_loop(const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL uint32_t* rs, int U,
-                                            const MOEQ_GLOBAL u32x4* xrow, _Float16* wdst, _Float16* adst,
-                                            const _Float16* As, const _Float16* Ws, int lane, int wm, int wn,
-                                            int nk, f32x4v (&acc)[2][4][4]) {
-  Raw hw[2];
-  u32x4 xv[2][4];
-#define GU_LOAD(slot, st)                                                                       \
-  do {                                                                                          \
-    hw[slot] = load_raw(rc, rs, U, B, (st) >> 1, slot);                                         \
-    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) xv[slot][i_] = xrow[(st) * (BK / 8) + i_]; \
-  } while (0)
-#define GU_DECODE(slot)                                                        \
-  do {                                                                         \
-    decode_raw<B, slot>(hw[slot], wdst + (slot) * (2 * BN * LDS_STRIDE));       \
-    store_row32(xv[slot], adst + (slot) * (BM * LDS_STRIDE));                  \
-  } while (0)
-#define GU_STEP(P, st_next)                                                                    \
-  do {                                                                                         \
-    Frags<2> f;                                                                                \
-    read_frags<2>(As + (P) * (BM * LDS_STRIDE), Ws + (P) * (2 * BN * LDS_STRIDE), lane, wm, wn, f); \
-    GU_DECODE(1 - (P));                                                                        \
-    GU_LOAD(1 - (P), st_next);                                                                 \
-    mfmas<2>(f, acc);                                                                          \
-    interleave_hint<64, 24, 4, 12>();                                                          \
-    __syncthreads();                                                                           \
-  } while (0)
-  GU_LOAD(0, 0);
-  GU_LOAD(1, 1);
-  GU_DECODE(0);
-  GU_LOAD(0, min(2, nk - 2));
-  __syncthreads();
-  for (int s0 = 0; s0 < nk; s0 += 2) {
-    GU_STEP(0, min(s0 + 3, nk - 1));  // step s0; decodes s0 + 1, loads s0 + 3
-    GU_STEP(1, min(s0 + 4, nk - 2));  // step s0 + 1; decodes s0 + 2, loads s0 + 4
-  }
-#undef GU_LOAD
-#undef GU_DECODE
-#undef GU_STEP
-}
-
-__device__ void gateup_gemm_body(const GemmArgs a, const SlotInfo sl, int m0, int n0,
-                                 const TensorDev tg, const TensorDev tu, _Float16* lds) {
-  _Float16* As = lds;                            // [2][BM][LDS_STRIDE]
-  _Float16* Ws = lds + 2 * BM * LDS_STRIDE;      // [2][2][BN][LDS_STRIDE]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int H = a.H, I = a.I, U = H / kUnit;
-  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
-  const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
-  // Load-phase roles.  Weights: waves 0-1 take gate rows, waves 2-3 up rows
-  // (so the tensor, hence the width, is wave-uniform); thread t decodes half a
-  // unit of row t & 127.  Activations (the prescaled binary16 copy of x): thread
-  // t moves 32 values of tile row t >> 1.  Rows past the bucket read token row
-  // 0: they only feed output rows that are never stored.
-  const int wt = __builtin_amdgcn_readfirstlane(tid >> 7);
-  const TensorDev t = wt ? tu : tg;
-  const int bits = __builtin_amdgcn_readfirstlane(t.bits);
-  const int wrow = n0 + (tid & 127);
-  const MOEQ_GLOBAL u32x4* rc = row_chunks(t, bits, wrow);
-  const MOEQ_GLOBAL uint32_t* rs = gptr(reinterpret_cast<const uint32_t*>(t.scales + (size_t)wrow * (H / kBlock)));
-  _Float16* wdst = Ws + (wt * BN + (tid & 127)) * LDS_STRIDE;
-  const int arow = tid >> 1, akh = tid & 1;
-  int tok = 0;
-  if (m0 + arow < sl.M) tok = sl.shared >= 0 ? m0 + arow : perm[sl.base + m0 + arow] / a.k;
-  const MOEQ_GLOBAL u32x4* xrow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + 4 * akh;
-  _Float16* adst = As + arow * LDS_STRIDE + 32 * akh;
-
-  f32x4v acc[2][4][4];
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) acc[q][i][c] = f32x4v{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = H / BK;
-  if (bits == 2)
-    gateup_loop<2>(rc, rs, U, xrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  else if (bits == 3)
-    gateup_loop<3>(rc, rs, U, xrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  else
-    gateup_loop<4>(rc, rs, U, xrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-
-  // epilogue: undo the activation prescale, SwiGLU, store h, track row maxima
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wm * 64 + 16 * i + (lane >> 4) * 4 + j;
-      const bool ok = m0 + r < sl.M;
-      float sc = 1.0f;
-      if (ok) {
-        const int tk = sl.shared >= 0 ? m0 + r : perm[sl.base + m0 + r] / a.k;
-        sc = __builtin_amdgcn_ldexpf(1.0f, xexp[tk]);
-      }
-      float rmax = 0.0f;
-      MOEQ_GLOBAL float* hout = (MOEQ_GLOBAL float*)(a.h + (size_t)(sl.base + m0 + r) * I);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int col = n0 + wn * 64 + 16 * c + (lane & 15);
-        const float hv = silu(acc[0][i][c][j] * sc) * (acc[1][i][c][j] * sc);
-        if (ok) hout[col] = hv;
-        rmax = fmaxf(rmax, fabsf(hv));
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
-      if (ok && (lane & 15) == 0) atomicMax(a.rowmax + sl.base + m0 + r, __float_as_uint(rmax));
-    }
-  }
-}
-
-__global__ __launch_bounds__(256, 1) void gateup_gemm_kernel(DecodeArgs a) {
-  extern __shared__ _Float16 lds_h[];
-  const int nN = a.I / BN;
-  const int L = xcd_logical(blockIdx.x, gridDim.x);
-  const int mt = L / nN, nt = L % nN;
-  if (mt >= a.tiles[0]) return;
-  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
-  const int m0 = a.tiles[2 + 2 * mt];
-  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
-  if (!tg.codes || !tu.codes) return;
-  if (tg.bits < 2 || tg.bits > 4 || tu.bits < 2 || tu.bits > 4) return;
-  gateup_gemm_body(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
 }
 
 // ---------------------------------------------------------------------------
@@ -457,13 +196,11 @@ __global__ __launch_bounds__(256) void h16_kernel(const float* h, const uint32_t
   }
 }
 
-// down grouped GEMM x routing weight -> partial rows.  Load-phase roles:
-// thread t decodes block t >> 7 of the K step of weight row n0 + (t & 127)
-// and moves the 32 binary16 activations of half t >> 7 of the K step of tile
-// row t & 127.
-
-// Block q = 2*hs + half of unit u (32 weights, B dwords at dword q*B of the
-// unit): chunks c0 = q*B/4 and min(c0+1, B-1), and the block's scale.
+// ---- weight tile decode: one thread, one row, one block (32 weights) ----
+// Block q of unit u (B dwords at dword q*B of the unit): the 16-byte chunks
+// c0 = q*B/4 and min(c0+1, B-1), kept as loaded (no selection at load time,
+// so the loads stay in flight), and the aligned pair of binary16 scales that
+// holds the block's.
 struct RawBlk {
   u32x4 a, b;
   uint32_t sc;
@@ -476,14 +213,16 @@ __device__ __forceinline__ RawBlk load_blk(const MOEQ_GLOBAL u32x4* rc, const MO
   RawBlk r;
   r.a = rc[(size_t)c0 * U + u];
   r.b = rc[(size_t)c1 * U + u];
-  r.sc = rs[4 * u + q];
+  // the aligned pair of binary16 scales holding block q's (q even: low half)
+  r.sc = *reinterpret_cast<const MOEQ_GLOBAL uint32_t*>(rs + 4 * u + (q & 2));
   return r;
 }
 
 // Decodes one block (width B) whose first dword is dword o (0..3, wave-
-// uniform) of the loaded pair of chunks.
+// uniform) of the loaded pair of chunks; its scale is the high half of the
+// loaded scale pair when o_half_shift (odd block index).
 template <int B>
-__device__ __forceinline__ void decode_blk(const RawBlk& r, int o, _Float16* dst) {
+__device__ __forceinline__ void decode_blk(const RawBlk& r, int o, bool o_half_shift, _Float16* dst) {
   const uint32_t all[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
   uint32_t w[4];
 #pragma unroll
@@ -496,7 +235,7 @@ __device__ __forceinline__ void decode_blk(const RawBlk& r, int o, _Float16* dst
   if constexpr (B == 2) asm("v_mov_b32 %0, 0x00030003" : "=v"(mask));
   const _Float16 zf = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
   const half2_t zb = {zf, zf};
-  const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)r.sc);
+  const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)(o_half_shift ? r.sc >> 16 : r.sc));
   const half2_t d2 = {d, d};
   uint32_t p[16];
   if constexpr (B == 4) {
@@ -529,85 +268,218 @@ __device__ __forceinline__ void decode_blk(const RawBlk& r, int o, _Float16* dst
   for (int i = 0; i < 4; ++i) out[i] = u32x4{p[4 * i], p[4 * i + 1], p[4 * i + 2], p[4 * i + 3]};
 }
 
-// The pipelined K loop of the down GEMM for width B (same scheme as the
-// gate/up loop).
-template <int B>
-__device__ __forceinline__ void down_loop(const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL uint16_t* rs, int U, int half,
-                                          const MOEQ_GLOBAL u32x4* hrow, _Float16* wdst, _Float16* adst,
-                                          const _Float16* As, const _Float16* Ws, int lane, int wm, int wn, int nk,
-                                          f32x4v (&acc)[1][4][4]) {
-  // first dword of block q = 2*hs + half inside its chunk pair
-  const int o0 = (half * B) & 3, o1 = ((2 + half) * B) & 3;
-  RawBlk hr[2];
-  u32x4 hv[2][4];
-#define DN_LOAD(slot, st)                                                                        \
-  do {                                                                                           \
-    hr[slot] = load_blk(rc, rs, U, B, (st) >> 1, 2 * (slot) + half);                             \
-    _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) hv[slot][i_] = hrow[(st) * (BK / 8) + i_];  \
-  } while (0)
-#define DN_DECODE(slot)                                                                 \
-  do {                                                                                  \
-    decode_blk<B>(hr[slot], (slot) ? o1 : o0, wdst + (slot) * (BN * LDS_STRIDE));       \
-    store_row32(hv[slot], adst + (slot) * (BM * LDS_STRIDE));                           \
-  } while (0)
-#define DN_STEP(P, st_next)                                                                   \
-  do {                                                                                        \
-    Frags<1> f;                                                                               \
-    read_frags<1>(As + (P) * (BM * LDS_STRIDE), Ws + (P) * (BN * LDS_STRIDE), lane, wm, wn, f); \
-    DN_DECODE(1 - (P));                                                                       \
-    DN_LOAD(1 - (P), st_next);                                                                \
-    mfmas<1>(f, acc);                                                                         \
-    interleave_hint<32, 16, 4, 8>();                                                          \
-    __syncthreads();                                                                          \
-  } while (0)
-  DN_LOAD(0, 0);
-  DN_LOAD(1, 1);
-  DN_DECODE(0);
-  DN_LOAD(0, min(2, nk - 2));
-  __syncthreads();
-  for (int s0 = 0; s0 < nk; s0 += 2) {
-    DN_STEP(0, min(s0 + 3, nk - 1));
-    DN_STEP(1, min(s0 + 4, nk - 2));
+// ---------------------------------------------------------------------------
+// Eight waves per workgroup (two per SIMD): the same 128 x 128 tile and K
+// step of 64, each wave owning 64 rows x 32 columns per tensor (2 x 4 wave
+// grid), so that while one wave of a SIMD waits on LDS or a barrier the other
+// issues MFMAs.  Weight roles: a thread decodes one 32-weight block per K
+// step (block 2*hs + BLK of its row's unit, BLK wave-uniform and a template
+// argument, hs = step parity), activation roles move 16 or 32 binary16
+// values.  Register slot and LDS buffer s % 2 hold step s; loads run two
+// steps ahead; the last loads repeat the final steps (their decodes land in a
+// buffer nobody reads again).
+template <int NT>
+__device__ __forceinline__ void read_frags8(const _Float16* A, const _Float16* W, int lane, int wm, int wn,
+                                            half8 (&fa)[2][4], half8 (&fb)[2][NT][2]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int kof = kk * 32 + (lane >> 4) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[kk][i] = lds_frag(A + (wm * 64 + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        fb[kk][t][c] = lds_frag(W + (t * BN + wn * 32 + 16 * c + (lane & 15)) * LDS_STRIDE + kof);
   }
-#undef DN_LOAD
-#undef DN_DECODE
-#undef DN_STEP
 }
 
-__device__ void down_gemm_body(const GemmArgs a, const SlotInfo sl, int m0, int n0,
-                               const TensorDev td, _Float16* lds) {
+template <int NT>
+__device__ __forceinline__ void mfmas8(const half8 (&fa)[2][4], const half8 (&fb)[2][NT][2], f32x4v (&acc)[NT][4][2]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[t][i][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[kk][i], fb[kk][t][c], acc[t][i][c], 0, 0, 0);
+}
+
+// One K loop.  DW: this wave decodes weight blocks (width B, block BLK of the
+// half unit); NA: u32x4 activation pieces this thread moves per step (0, 2
+// or 4).
+template <int NT, int B, int BLK, bool DW, int NA>
+__device__ __forceinline__ void gemm_loop8(const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL uint16_t* rs, int U,
+                                           const MOEQ_GLOBAL u32x4* arow, _Float16* wdst, _Float16* adst,
+                                           const _Float16* As, const _Float16* Ws, int lane, int wm, int wn, int nk,
+                                           f32x4v (&acc)[NT][4][2]) {
+  RawBlk hw[2];
+  u32x4 xv[2][NA > 0 ? NA : 1];
+#define L8(slot, st)                                                                        \
+  do {                                                                                      \
+    if constexpr (DW) hw[slot] = load_blk(rc, rs, U, B, (st) >> 1, 2 * (slot) + BLK);       \
+    _Pragma("unroll") for (int i_ = 0; i_ < NA; ++i_) xv[slot][i_] = arow[(st) * 8 + i_];   \
+  } while (0)
+#define D8(slot)                                                                                         \
+  do {                                                                                                   \
+    if constexpr (DW) decode_blk<B>(hw[slot], ((2 * (slot) + BLK) * B) & 3, BLK != 0, wdst + (slot) * (NT * BN * LDS_STRIDE)); \
+    u32x4* ad_ = reinterpret_cast<u32x4*>(adst + (slot) * (BM * LDS_STRIDE));                            \
+    _Pragma("unroll") for (int i_ = 0; i_ < NA; ++i_) ad_[i_] = xv[slot][i_];                            \
+  } while (0)
+#define STEP8(P, st_next)                                                                         \
+  do {                                                                                            \
+    half8 fa[2][4], fb[2][NT][2];                                                                 \
+    read_frags8<NT>(As + (P) * (BM * LDS_STRIDE), Ws + (P) * (NT * BN * LDS_STRIDE), lane, wm, wn, fa, fb); \
+    D8(1 - (P));                                                                                  \
+    L8(1 - (P), st_next);                                                                         \
+    mfmas8<NT>(fa, fb, acc);                                                                      \
+    interleave_hint<16 * NT, 8 + 4 * NT, 2, 4>();                                                 \
+    __syncthreads();                                                                              \
+  } while (0)
+  L8(0, 0);
+  L8(1, 1);
+  D8(0);
+  L8(0, min(2, nk - 2));
+  __syncthreads();
+  for (int s0 = 0; s0 < nk; s0 += 2) {
+    STEP8(0, min(s0 + 3, nk - 1));
+    STEP8(1, min(s0 + 4, nk - 2));
+  }
+#undef L8
+#undef D8
+#undef STEP8
+}
+
+__device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
+                                  const TensorDev tu, _Float16* lds) {
+  _Float16* As = lds;                            // [2][BM][LDS_STRIDE]
+  _Float16* Ws = lds + 2 * BM * LDS_STRIDE;      // [2][2][BN][LDS_STRIDE]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
+  const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
+  // weights: waves 0-3 gate rows, 4-7 up rows; waves 2w and 2w + 1 take
+  // block BLK = w % 2 of each half unit.  Activations: thread t moves 16
+  // values (quarter t % 4) of tile row t / 4.
+  const int wt = __builtin_amdgcn_readfirstlane(tid >> 8);
+  const int blk = __builtin_amdgcn_readfirstlane((tid >> 7) & 1);
+  const TensorDev t = wt ? tu : tg;
+  const int bits = __builtin_amdgcn_readfirstlane(t.bits);
+  const int wrow = n0 + (tid & 127);
+  const MOEQ_GLOBAL u32x4* rc = row_chunks(t, bits, wrow);
+  const MOEQ_GLOBAL uint16_t* rs = gptr(t.scales + (size_t)wrow * (H / kBlock));
+  _Float16* wdst = Ws + (wt * BN + (tid & 127)) * LDS_STRIDE + 32 * blk;
+  const int ar = tid >> 2, aq = tid & 3;
+  int tok = 0;
+  if (m0 + ar < sl.M) tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
+  const MOEQ_GLOBAL u32x4* arow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + 2 * aq;
+  _Float16* adst = As + ar * LDS_STRIDE + 16 * aq;
+
+  f32x4v acc[2][4][2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) acc[q][i][c] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  const int nk = H / BK;
+#define GU8(B, BL) gemm_loop8<2, B, BL, true, 2>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc)
+  if (bits == 2) {
+    if (blk) GU8(2, 1); else GU8(2, 0);
+  } else if (bits == 3) {
+    if (blk) GU8(3, 1); else GU8(3, 0);
+  } else {
+    if (blk) GU8(4, 1); else GU8(4, 0);
+  }
+#undef GU8
+
+  // epilogue: undo the activation prescale, SwiGLU, store h, track row maxima
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = wm * 64 + 16 * i + (lane >> 4) * 4 + j;
+      const bool ok = m0 + r < sl.M;
+      float sc = 1.0f;
+      if (ok) {
+        const int tk = sl.shared >= 0 ? m0 + r : perm[sl.base + m0 + r] / a.k;
+        sc = __builtin_amdgcn_ldexpf(1.0f, xexp[tk]);
+      }
+      float rmax = 0.0f;
+      MOEQ_GLOBAL float* hout = (MOEQ_GLOBAL float*)(a.h + (size_t)(sl.base + m0 + r) * I);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int col = n0 + wn * 32 + 16 * c + (lane & 15);
+        const float hv = silu(acc[0][i][c][j] * sc) * (acc[1][i][c][j] * sc);
+        if (ok) hout[col] = hv;
+        rmax = fmaxf(rmax, fabsf(hv));
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
+      if (ok && (lane & 15) == 0) atomicMax(a.rowmax + sl.base + m0 + r, __float_as_uint(rmax));
+    }
+  }
+}
+
+__global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
+  extern __shared__ _Float16 lds_h[];
+  const int nN = a.I / BN;
+  const int L = xcd_logical(blockIdx.x, gridDim.x);
+  const int mt = L / nN, nt = L % nN;
+  if (mt >= a.tiles[0]) return;
+  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
+  const int m0 = a.tiles[2 + 2 * mt];
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  if (tg.bits < 2 || tg.bits > 4 || tu.bits < 2 || tu.bits > 4) return;
+  gateup_gemm_body8(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
+}
+
+__device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev td,
+                                _Float16* lds) {
   _Float16* As = lds;                        // [2][BM][LDS_STRIDE]
   _Float16* Ws = lds + 2 * BM * LDS_STRIDE;  // [2][BN][LDS_STRIDE]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int H = a.H, I = a.I, U = I / kUnit;
-  const int r = tid & 127;
-  const int half = __builtin_amdgcn_readfirstlane(tid >> 7);  // wave-uniform
+  // waves 0-3 decode weight blocks (block BLK = (t >> 7) % 2 of row t % 128),
+  // waves 4-7 move the activations (32 values of tile row (t - 256) / 2)
+  const bool wrole = __builtin_amdgcn_readfirstlane(wave) < 4;
+  const int blk = __builtin_amdgcn_readfirstlane((tid >> 7) & 1);
   const int bits = __builtin_amdgcn_readfirstlane(td.bits);
-  const MOEQ_GLOBAL u32x4* rc = row_chunks(td, bits, n0 + r);
-  const MOEQ_GLOBAL uint16_t* rs = gptr(td.scales + (size_t)(n0 + r) * (I / kBlock));
-  _Float16* wdst = Ws + r * LDS_STRIDE + 32 * half;
-  const bool arow_ok = m0 + r < sl.M;
+  const int wrow = n0 + (tid & 127);
+  const MOEQ_GLOBAL u32x4* rc = row_chunks(td, bits, wrow);
+  const MOEQ_GLOBAL uint16_t* rs = gptr(td.scales + (size_t)wrow * (I / kBlock));
+  _Float16* wdst = Ws + (tid & 127) * LDS_STRIDE + 32 * blk;
+  const int at = tid & 255, ar = at >> 1, ah = at & 1;
+  const bool aok = m0 + ar < sl.M;
+  // rows past the bucket read activation row 0 of the slot (never stored)
+  const MOEQ_GLOBAL u32x4* arow =
+      gptr(reinterpret_cast<const u32x4*>(a.h16 + (size_t)(sl.base + m0 + (aok ? ar : 0)) * I)) + 4 * ah;
+  _Float16* adst = As + ar * LDS_STRIDE + 32 * ah;
   const MOEQ_GLOBAL uint32_t* rowmax = gptr((const uint32_t*)a.rowmax);
   const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
-  // rows past the bucket read activation row 0 of the slot (never stored)
-  const MOEQ_GLOBAL u32x4* hrow =
-      gptr(reinterpret_cast<const u32x4*>(a.h16 + (size_t)(sl.base + m0 + (arow_ok ? r : 0)) * I)) + 4 * half;
-  _Float16* adst = As + r * LDS_STRIDE + 32 * half;
 
-  f32x4v acc[1][4][4];
+  f32x4v acc[1][4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[0][i][c] = f32x4v{0.f, 0.f, 0.f, 0.f};
-
+    for (int c = 0; c < 2; ++c) acc[0][i][c] = f32x4v{0.f, 0.f, 0.f, 0.f};
   const int nk = I / BK;
-  if (bits == 2)
-    down_loop<2>(rc, rs, U, half, hrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  else if (bits == 3)
-    down_loop<3>(rc, rs, U, half, hrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  else
-    down_loop<4>(rc, rs, U, half, hrow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
+#define DN8(B, BL) gemm_loop8<1, B, BL, true, 0>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc)
+  if (!wrole) {
+    gemm_loop8<1, 4, 0, false, 4>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
+  } else if (bits == 2) {
+    if (blk) DN8(2, 1); else DN8(2, 0);
+  } else if (bits == 3) {
+    if (blk) DN8(3, 1); else DN8(3, 0);
+  } else {
+    if (blk) DN8(4, 1); else DN8(4, 0);
+  }
+#undef DN8
 
   // epilogue: undo the row prescale, scale by the routing weight, store partials
 #pragma unroll
@@ -629,15 +501,15 @@ __device__ void down_gemm_body(const GemmArgs a, const SlotInfo sl, int m0, int 
       const float sc = __builtin_amdgcn_ldexpf(wv, e);
       MOEQ_GLOBAL float* prow_out = (MOEQ_GLOBAL float*)(a.partial + (size_t)prow * H);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int col = n0 + wn * 64 + 16 * c + (lane & 15);
+      for (int c = 0; c < 2; ++c) {
+        const int col = n0 + wn * 32 + 16 * c + (lane & 15);
         prow_out[col] = acc[0][i][c][j] * sc;
       }
     }
   }
 }
 
-__global__ __launch_bounds__(256, 1) void down_gemm_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.H / BN;
   const int L = xcd_logical(blockIdx.x, gridDim.x);
@@ -648,7 +520,7 @@ __global__ __launch_bounds__(256, 1) void down_gemm_kernel(DecodeArgs a) {
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
   if (td.bits < 2 || td.bits > 4) return;
-  down_gemm_body(gemm_args(a), sl, m0, nt * BN, td, lds_h);
+  down_gemm_body8(gemm_args(a), sl, m0, nt * BN, td, lds_h);
 }
 
 }  // namespace
@@ -666,12 +538,12 @@ hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
   static bool attr = false;
   if (!attr) {
-    e = hipFuncSetAttribute((const void*)gateup_gemm_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    e = hipFuncSetAttribute((const void*)gateup_gemm8_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int grid = a.max_mtiles * (a.I / BN);
-  gateup_gemm_kernel<<<grid, 256, lds, s>>>(a);
+  gateup_gemm8_kernel<<<grid, 512, lds, s>>>(a);
   return hipGetLastError();
 }
 
@@ -683,13 +555,13 @@ hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
   static bool attr = false;
   if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)down_gemm_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+    hipError_t e = hipFuncSetAttribute((const void*)down_gemm8_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds);
     if (e != hipSuccess) return e;
     attr = true;
   }
   const int grid = a.max_mtiles * (a.H / BN);
-  down_gemm_kernel<<<grid, 256, lds, s>>>(a);
+  down_gemm8_kernel<<<grid, 512, lds, s>>>(a);
   return hipGetLastError();
 }
 
