@@ -24,7 +24,11 @@ Readings where the paper is silent (all listed with the design notes):
 * the sigmoid is evaluated in float64 and rounded once to float32;
 * the optional per-expert bias enters selection only; weights use the
   unbiased score;
-* if the chosen scores sum to zero, all weights are zero.
+* if the chosen scores sum to zero, all weights are zero;
+* with ``regroup`` (the literal reading of Section 3.2, "topk_group
+  partitions the pruned expert pool into groups"), the kept experts in
+  ascending id order are cut into ``n_group`` contiguous groups of equal size
+  and routing runs over them alone.
 """
 import numpy as np
 
@@ -78,12 +82,22 @@ def route_token(logits, mask, bias, n_group, topk_group, top_k, group_topn,
 
 
 def route(logits, mask, bias=None, *, n_group, topk_group, top_k, group_topn=2,
-          norm_topk=True, routed_scale=1.0):
+          norm_topk=True, routed_scale=1.0, regroup=False):
     """Route every token: logits float32 ``[n, E]`` -> (idx int32 ``[n, k]``, w float64 ``[n, k]``).
 
-    Slot order is selection order (score descending, lower id first on ties)."""
+    Slot order is selection order (score descending, lower id first on ties).
+    With ``regroup`` the groups are formed over the kept experts only."""
     logits = np.asarray(logits, dtype=np.float32)
     mask = np.asarray(mask).astype(bool)
+    if regroup:
+        kept = np.nonzero(mask)[0]
+        if len(kept) % n_group:
+            raise ValueError("regrouping needs a kept count divisible by n_group")
+        sub_bias = None if bias is None else np.asarray(bias, np.float32)[kept]
+        idx, w = route(logits[:, kept], np.ones(len(kept), np.uint8), sub_bias, n_group=n_group,
+                       topk_group=topk_group, top_k=top_k, group_topn=group_topn, norm_topk=norm_topk,
+                       routed_scale=routed_scale)
+        return kept[idx].astype(np.int32), w
     n = logits.shape[0]
     idx = np.zeros((n, top_k), np.int32)
     w = np.zeros((n, top_k), np.float64)

@@ -156,3 +156,35 @@ def test_feasibility_rule():
     assert not router.routing_is_feasible(m, 2, 1, 2)          # the 1-expert group may win
     assert router.routing_is_feasible(m, 2, 2, 3)
     assert not router.routing_is_feasible(np.array([1, 1, 0, 0], np.uint8), 2, 2, 1)
+
+
+def test_regroup_equals_masking_when_groups_are_untouched():
+    """No pruning, or pruning that leaves every original group the same number
+    of survivors at the same positions, gives the same groups either way."""
+    r = np.random.default_rng(11)
+    E, G = 16, 4
+    lg = _grid_logits(r, 30, E)
+    full = np.ones(E, np.uint8)
+    kw = dict(n_group=G, topk_group=2, top_k=3, routed_scale=2.5)
+    a = router.route(lg, full, **kw)
+    b = router.route(lg, full, regroup=True, **kw)
+    assert np.array_equal(a[0], b[0]) and np.allclose(a[1], b[1])
+    even = np.array([1, 1, 1, 0] * 4, np.uint8)      # three survivors in every group
+    a = router.route(lg, even, **kw)
+    b = router.route(lg, even, regroup=True, **kw)
+    assert np.array_equal(a[0], b[0])
+
+
+def test_regroup_hand_example():
+    """E = 8, two groups, kept {0, 1, 2, 4}, one group per token, k = 2.
+    Masking keeps the original groups {0, 1, 2} and {4}: group 0 scores
+    s(1.0) + s(0.95), group 1 only s(0.99), so experts 0 and 2 are chosen.
+    Regrouping makes {0, 1} and {2, 4}: s(0.99) + s(0.95) beats s(1.0) + s(0.9),
+    so experts 4 and 2 are chosen (the sigmoid keeps the logits' order)."""
+    mask = np.array([1, 1, 1, 0, 1, 0, 0, 0], np.uint8)
+    lg = np.array([[1.0, 0.9, 0.95, 5.0, 0.99, 5.0, 5.0, 5.0]], np.float32)
+    kw = dict(n_group=2, topk_group=1, top_k=2, group_topn=2, routed_scale=1.0)
+    idx_m, _ = router.route(lg, mask, **kw)
+    idx_r, _ = router.route(lg, mask, regroup=True, **kw)
+    assert idx_m[0].tolist() == [0, 2]
+    assert idx_r[0].tolist() == [4, 2]
