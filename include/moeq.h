@@ -85,6 +85,11 @@ typedef struct moeq_layer moeq_layer; /* opaque; owns every device buffer it all
  *   decode_max_tokens  forward takes the decode path (dequant-GEMV) for
  *                   n_tokens <= this and the prefill path (grouped GEMM on
  *                   MFMA) above it; 0 selects the library default (32)
+ *   regroup         0: routing groups are the original id ranges with pruned
+ *                   experts masked; 1: the kept experts, in ascending id order,
+ *                   are cut into n_group equal contiguous groups (Section 3.2's
+ *                   partition of the pruned expert pool; the kept count must be
+ *                   a multiple of n_group)
  */
 typedef struct {
   int32_t hidden;
@@ -99,6 +104,7 @@ typedef struct {
   float routed_scale;
   int32_t max_tokens;
   int32_t decode_max_tokens;
+  int32_t regroup;
 } moeq_config;
 
 /* One quantized tensor in the canonical packing described above.
@@ -125,7 +131,8 @@ typedef struct {
  *   out          receives the handle
  * The routing must be feasible: topk_group must not exceed the number of
  * groups with a kept expert, and the topk_group smallest non-empty groups
- * must hold at least top_k kept experts (else INVALID_ARG).
+ * must hold at least top_k kept experts (with regroup: topk_group groups of
+ * kept / n_group experts must hold top_k) (else INVALID_ARG).
  * All weight data is copied and re-laid-out on the device; the caller may
  * free its buffers when this returns.  Synchronizes the device.
  * Errors: INVALID_ARG, UNSUPPORTED (widths or shapes), OUT_OF_MEMORY, DEVICE;

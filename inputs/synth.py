@@ -46,6 +46,7 @@ class LayerShape:
     group_topn: int = 2
     norm_topk: int = 1
     routed_scale: float = 2.5
+    regroup: int = 0      # 1: routing groups formed over the kept experts only
 
     def rows_cols(self, proj):
         """(rows, K) of a projection: gate/up are [inter, hidden], down [hidden, inter]."""

@@ -62,6 +62,7 @@ struct moeq_layer {
   TensorDev* desc = nullptr;
   uint8_t* mask = nullptr;
   float* bias = nullptr;
+  int32_t* kept_ids = nullptr;  // kept experts ascending, when the router regroups them
   void* ws_mem = nullptr;
   Workspace ws{};
   hipEvent_t stage_events[MOEQ_STAGE_EVENTS] = {};
@@ -76,6 +77,7 @@ void release(moeq_layer* L) {
   hipFree(L->desc);
   hipFree(L->mask);
   hipFree(L->bias);
+  hipFree(L->kept_ids);
   hipFree(L->ws_mem);
   delete L;
 }
@@ -110,6 +112,7 @@ moeq_status check_config(const moeq_config* c) {
     return fail(MOEQ_ERR_INVALID_ARG, "n_shared %d outside 0..%d", c->n_shared, kMaxShared);
   if (c->max_tokens < 1 || c->max_tokens > (1 << 20))
     return fail(MOEQ_ERR_INVALID_ARG, "max_tokens %d outside 1..2^20", c->max_tokens);
+  if (c->regroup != 0 && c->regroup != 1) return fail(MOEQ_ERR_INVALID_ARG, "regroup must be 0 or 1");
   if (c->decode_max_tokens < 0 || c->decode_max_tokens > kDecodeMaxTokens)
     return fail(MOEQ_ERR_INVALID_ARG, "decode_max_tokens %d outside 0..%d", c->decode_max_tokens,
                 kDecodeMaxTokens);
@@ -137,6 +140,19 @@ moeq_status check_routing(const moeq_config* c, const uint8_t* mask, int* n_kept
     if (n > 0) counts.push_back(n);
   }
   *n_kept = kept;
+  if (c->regroup) {
+    // the kept experts form n_group equal groups of their own
+    if (kept % c->n_group)
+      return fail(MOEQ_ERR_INVALID_ARG, "regroup needs the kept count (%d) to be a multiple of n_group %d", kept,
+                  c->n_group);
+    if (c->group_topn > kept / c->n_group)
+      return fail(MOEQ_ERR_INVALID_ARG, "group_topn %d exceeds the %d experts of a regrouped group", c->group_topn,
+                  kept / c->n_group);
+    if (c->topk_group * (kept / c->n_group) < c->top_k)
+      return fail(MOEQ_ERR_INVALID_ARG, "topk_group regrouped groups of %d experts hold fewer than top_k %d",
+                  kept / c->n_group, c->top_k);
+    return ok();
+  }
   if ((int)counts.size() < c->topk_group)
     return fail(MOEQ_ERR_INVALID_ARG, "only %d groups have kept experts; topk_group is %d",
                 (int)counts.size(), c->topk_group);
@@ -158,8 +174,10 @@ RouterParams router_params(const moeq_layer* L, const float* logits, const void*
   rp.x16 = L->ws.x16;
   rp.logits = logits;
   rp.mask = L->mask;
+  rp.kept_ids = L->kept_ids;
+  rp.E_row = L->cfg.n_experts;
   rp.bias = L->bias;
-  rp.E = L->cfg.n_experts;
+  rp.E = L->kept_ids ? L->n_kept : L->cfg.n_experts;
   rp.G = L->cfg.n_group;
   rp.TG = L->cfg.topk_group;
   rp.k = L->cfg.top_k;
@@ -290,6 +308,14 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   if ((he = hipMalloc((void**)&L->desc, sizeof(TensorDev) * plan.size())) != hipSuccess)
     return bail(he, "hipMalloc(descriptors)");
   if ((he = hipMalloc((void**)&L->mask, E)) != hipSuccess) return bail(he, "hipMalloc(mask)");
+  if (cfg->regroup) {
+    std::vector<int32_t> ids;
+    for (int e = 0; e < E; ++e)
+      if (expert_mask[e]) ids.push_back(e);
+    if ((he = hipMalloc((void**)&L->kept_ids, ids.size() * 4)) != hipSuccess) return bail(he, "hipMalloc(kept ids)");
+    if ((he = hipMemcpy(L->kept_ids, ids.data(), ids.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+      return bail(he, "hipMemcpy(kept ids)");
+  }
   if ((he = hipMalloc((void**)&L->bias, sizeof(float) * E)) != hipSuccess) return bail(he, "hipMalloc(bias)");
   if (weights_location == MOEQ_WEIGHTS_HOST && max_codes &&
       (he = hipMalloc((void**)&staging, max_codes)) != hipSuccess)
@@ -492,6 +518,8 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
   rp.logits = logits;
   rp.mask = all_kept;
   rp.bias = bias;
+  rp.kept_ids = nullptr;
+  rp.E_row = E;
   rp.E = E;
   rp.G = cfg->n_group;
   rp.TG = cfg->topk_group;

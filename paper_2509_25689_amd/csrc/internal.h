@@ -38,9 +38,13 @@ struct TensorDev {
 };
 
 struct RouterParams {
-  const float* logits;    // [n x E]
-  const uint8_t* mask;    // [E] device copy
-  const float* bias;      // [E] device copy (zeros when none was given)
+  const float* logits;    // [n x E_row]
+  const uint8_t* mask;    // [E_row] device copy
+  const float* bias;      // [E_row] device copy (zeros when none was given)
+  // router experts: E_row (original ids) or, when kept_ids is set, the E
+  // kept experts in ascending id order (groups formed over them alone)
+  const int32_t* kept_ids;
+  int32_t E_row;
   int32_t E, G, TG, k, topn, norm;
   float scale;
   // optional (many-token path): activations whose per-token binary exponent

@@ -132,7 +132,7 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
     }
   }
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
-  const float* lg = rp.logits + (size_t)t * E;
+  const float* lg = rp.logits + (size_t)t * rp.E_row;
   float s[EPL], b[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
@@ -140,11 +140,12 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
     s[i] = 0.0f;
     b[i] = -INFINITY;
     if (e < E) {
+      const int eo = rp.kept_ids ? rp.kept_ids[e] : e;  // original expert id
       // sigmoid evaluated in double precision, rounded once to float
-      float v = (float)(1.0 / (1.0 + exp(-(double)lg[e])));
+      float v = (float)(1.0 / (1.0 + exp(-(double)lg[eo])));
       if (!(v == v)) v = 0.0f;  // a NaN logit must not leave the index range undefined
       s[i] = v;
-      if (rp.mask[e]) b[i] = v + rp.bias[e];
+      if (rp.kept_ids || rp.mask[eo]) b[i] = v + rp.bias[eo];
     }
   }
 
@@ -275,9 +276,10 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
       wv = sum == 0.0f ? 0.0f : my_s / sum * rp.scale;
     else
       wv = my_s * rp.scale;
-    idx_g[(size_t)t * rp.k + lane] = my_i;
+    const int id = rp.kept_ids ? rp.kept_ids[my_i] : my_i;  // back to original ids
+    idx_g[(size_t)t * rp.k + lane] = id;
     w_g[(size_t)t * rp.k + lane] = wv;
-    if (idx_s) idx_s[t * rp.k + lane] = my_i;
+    if (idx_s) idx_s[t * rp.k + lane] = id;
   }
   wave_sync();  // gs_l is reused by this wave's next token
 }
@@ -337,7 +339,8 @@ __global__ __launch_bounds__(small_threads<EPL>()) void route_bucket_small_kerne
   __shared__ int32_t off[kMaxExperts + 1];
 
   const int tid = threadIdx.x, wave = tid >> 6;
-  const int E = rp.E, k = rp.k, nk = n * k;
+  // buckets are over the original expert ids
+  const int E = rp.E_row, k = rp.k, nk = n * k;
   for (int e = tid; e < E; e += NT) emask[e] = 0ull;
   if (idx_in) {
     for (int a = tid; a < nk; a += NT) idx_l[a] = idx_in[a];
@@ -428,7 +431,8 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const int32_t* idx,
 
 hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_in, int n,
                                      const Workspace& ws, hipStream_t s) {
-  switch (experts_per_lane(rp.E)) {
+  // lanes own enough experts for both the router's and the buckets' id range
+  switch (experts_per_lane(rp.E_row)) {
     case 1: route_bucket_small_kernel<1><<<1, small_threads<1>(), 0, s>>>(rp, idx_in, n, ws); break;
     case 2: route_bucket_small_kernel<2><<<1, small_threads<2>(), 0, s>>>(rp, idx_in, n, ws); break;
     case 4: route_bucket_small_kernel<4><<<1, small_threads<4>(), 0, s>>>(rp, idx_in, n, ws); break;
@@ -441,7 +445,7 @@ hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_
 hipError_t launch_route_tokens(const RouterParams& rp, int n, int32_t* idx, float* w,
                                hipStream_t s) {
   const int grid = (n + kWaves - 1) / kWaves;
-  switch (experts_per_lane(rp.E)) {
+  switch (experts_per_lane(rp.E_row)) {
     case 1: route_tokens_kernel<1><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
     case 2: route_tokens_kernel<2><<<grid, 256, 0, s>>>(rp, n, idx, w); break;
     case 4: route_tokens_kernel<4><<<grid, 256, 0, s>>>(rp, n, idx, w); break;

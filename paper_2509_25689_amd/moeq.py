@@ -44,7 +44,8 @@ class moeq_config(ctypes.Structure):
                 ("n_group", ctypes.c_int32), ("topk_group", ctypes.c_int32),
                 ("top_k", ctypes.c_int32), ("group_topn", ctypes.c_int32),
                 ("norm_topk", ctypes.c_int32), ("routed_scale", ctypes.c_float),
-                ("max_tokens", ctypes.c_int32), ("decode_max_tokens", ctypes.c_int32)]
+                ("max_tokens", ctypes.c_int32), ("decode_max_tokens", ctypes.c_int32),
+                ("regroup", ctypes.c_int32)]
 
 
 class moeq_qtensor(ctypes.Structure):
@@ -192,7 +193,7 @@ def make_config(shape, max_tokens, decode_max_tokens=0):
     """A moeq_config from any object with the layer-shape attribute names."""
     return moeq_config(shape.hidden, shape.inter, shape.n_experts, shape.n_shared, shape.n_group,
                        shape.topk_group, shape.top_k, shape.group_topn, shape.norm_topk,
-                       shape.routed_scale, max_tokens, decode_max_tokens)
+                       shape.routed_scale, max_tokens, decode_max_tokens, int(getattr(shape, "regroup", 0)))
 
 
 def _addr(a):

@@ -199,3 +199,13 @@ def test_expert_importance_validation():
     # top_k larger than what topk_group groups can hold even with every expert kept
     c2 = _cfg(topk_group=1, top_k=12)
     assert call(c=c2) == moeq.MOEQ_ERR_INVALID_ARG
+
+
+def test_regroup_validation():
+    """regroup must be 0 or 1 and needs a kept count divisible by n_group."""
+    assert _create(_cfg(regroup=2))[0] == moeq.MOEQ_ERR_INVALID_ARG
+    E = synth.TINY.n_experts
+    mask = np.ones(E, np.uint8)
+    mask[:3] = 0                      # 13 kept, not a multiple of 2 groups
+    assert _create(_cfg(regroup=1), mask=mask)[0] == moeq.MOEQ_ERR_INVALID_ARG
+    assert "multiple of n_group" in moeq.moeq_last_error()

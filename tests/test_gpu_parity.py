@@ -35,7 +35,8 @@ def _x(n, H, *key):
 def _route_oracle(shape, mask, logits):
     return router.route(logits, mask, n_group=shape.n_group, topk_group=shape.topk_group,
                         top_k=shape.top_k, group_topn=shape.group_topn,
-                        norm_topk=shape.norm_topk, routed_scale=shape.routed_scale)
+                        norm_topk=shape.norm_topk, routed_scale=shape.routed_scale,
+                        regroup=bool(shape.regroup))
 
 
 def _make_layer(moeq, data, max_tokens, **kw):
@@ -296,3 +297,39 @@ def test_forward_v3_k6_decode(gpu_lib, v3_k6):
 def test_forward_v3_k6_prefill(gpu_lib, v3_k6):
     data, L = v3_k6
     _forward_check(gpu_lib, data, L, 300, "fwd-k6-prefill", gpu_lib.MOEQ_PATH_PREFILL, sample=[0, 150, 299])
+
+
+# ---------------------------------------------------------------------------
+# Section 3.2 read literally: the kept experts are partitioned into groups of
+# their own (regroup = 1) instead of masking the original groups.
+@pytest.fixture(scope="module", params=["tiny", "v3"])
+def regrouped(gpu_lib, request):
+    import dataclasses
+    base = synth.TINY if request.param == "tiny" else synth.V3
+    shape = dataclasses.replace(base, regroup=1)
+    data = layers.random_packed_layer(shape, "all4" if request.param == "tiny" else "gu3_d4_sh4",
+                                      f"regroup-{request.param}")
+    L = _make_layer(gpu_lib, data, max_tokens=128)
+    yield data, L
+    L.close()
+
+
+@pytest.mark.parametrize("n", [1, 16, 100])
+def test_route_regrouped(regrouped, n):
+    data, L = regrouped
+    logits = synth.normal_logits(n, data.shape.n_experts, "route-regroup", n)
+    idx, w = L.route(_dev(logits))
+    ref_idx, ref_w = _route_oracle(data.shape, data.mask, logits)
+    assert np.array_equal(idx.cpu().numpy(), ref_idx)
+    np.testing.assert_allclose(w.cpu().numpy(), ref_w, atol=1e-6 * data.shape.routed_scale)
+    # the seeded masks leave the original groups uneven, so the two readings differ
+    masked, _ = router.route(logits, data.mask, n_group=data.shape.n_group, topk_group=data.shape.topk_group,
+                             top_k=data.shape.top_k, group_topn=data.shape.group_topn)
+    if n >= 16:
+        assert not np.array_equal(masked, ref_idx)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+def test_forward_regrouped(gpu_lib, regrouped, path):
+    data, L = regrouped
+    _forward_check(gpu_lib, data, L, 24, "fwd-regroup", path, sample=[0, 11, 23])
