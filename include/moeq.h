@@ -145,7 +145,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
 /* The layer forward (the whole hot path: route, bucket, expert products,
  * SwiGLU, weighted combine, shared expert).
  *   x        DEVICE bfloat16 [n_tokens x hidden], row-major
- *   logits   DEVICE float32 [n_tokens x n_experts] router logits (finite)
+ *   logits   DEVICE float32 [n_tokens x n_experts] router logits (finite), or
+ *            NULL when a router weight is set: the forward then first
+ *            computes them as moeq_router_logits does, into layer memory
  *   n_tokens 0..max_tokens; 0 enqueues nothing and returns OK
  *   y        DEVICE float32 [n_tokens x hidden]; fully overwritten
  * Borrowed pointers must stay valid until the stream work completes.  No
@@ -154,6 +156,32 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
  * Errors: INVALID_ARG, CAPACITY (n_tokens > max_tokens), DEVICE. */
 moeq_status moeq_forward(moeq_layer* layer, const void* x, const float* logits,
                          int32_t n_tokens, float* y, void* stream);
+
+/* The router's gate weight W_r, so that a forward needs only x: the logits
+ * l = x W_r^T are the token-to-expert affinities whose sigmoid the router of
+ * Section 3.2 (and the statistics of Section 3.1) score.
+ *   w         float32 [n_experts x hidden], row-major, finite; HOST or
+ *             DEVICE (current device) per location (MOEQ_WEIGHTS_*); NULL
+ *             removes the weight and frees its memory
+ * Copied; the caller may free w on return.  Allocates, on the first set,
+ * n_experts * hidden * 4 bytes for the weight and max_tokens * n_experts * 4
+ * for the logits a forward computes.  Synchronizes the device (do not call
+ * while a forward of this layer is being captured).
+ * Errors: INVALID_ARG (location, a non-finite HOST element), OUT_OF_MEMORY,
+ * DEVICE. */
+moeq_status moeq_set_router_weight(moeq_layer* layer, const float* w, int32_t location);
+
+/* The gate alone: logits = x W_r^T with the set weight, float32 products and
+ * sums.  Each logit is accumulated in a fixed order that depends only on
+ * whether n_tokens <= 8 (one streaming pass per expert, per-thread partial
+ * sums over strided columns combined by a fixed tree) or not (one fused
+ * multiply-add chain over the hidden index), so results are deterministic.
+ *   x        DEVICE bfloat16 [n_tokens x hidden], 16-byte aligned
+ *   n_tokens 0..max_tokens
+ *   logits   DEVICE float32 [n_tokens x n_experts] (written)
+ * Errors: INVALID_ARG (no weight set, arguments), CAPACITY, DEVICE. */
+moeq_status moeq_router_logits(moeq_layer* layer, const void* x, int32_t n_tokens, float* logits,
+                               void* stream);
 
 /* Frees everything the layer owns after synchronizing the device.  NULL-safe. */
 void moeq_destroy(moeq_layer* layer);
@@ -239,7 +267,8 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
  *   events  NULL (count 0) to stop, or MOEQ_STAGE_EVENTS hipEvent_t handles
  *           (as void*) owned by the caller.  Every following moeq_forward on
  *           this layer records, on its stream, events[0] before its first
- *           kernel, events[1] after routing and bucketing, events[2] after the
+ *           kernel, events[1] after routing and bucketing (and the gate,
+ *           when the forward computes the logits), events[2] after the
  *           gate/up kernel, events[3] after the down kernel and events[4]
  *           after the combine, so hipEventElapsedTime between neighbours is
  *           the duration of one stage.

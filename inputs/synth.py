@@ -150,6 +150,27 @@ def activations(n, H, *key):
     return bf16_from_f32(rng("x", *key).standard_normal((n, H), dtype=np.float32))
 
 
+def router_weight(E, H, *key):
+    """float32 gate ``[E, H]`` of N(0, 1/H) draws: with N(0, 1) activations the
+    logits are about N(0, 1)."""
+    return (rng("router_w", *key).standard_normal((E, H), dtype=np.float32)
+            / np.float32(np.sqrt(H))).astype(np.float32)
+
+
+def grid_activations(n, H, *key):
+    """bfloat16 bit patterns ``[n, H]`` of integers drawn uniformly from -4..4."""
+    return bf16_from_f32(rng("xgrid", *key).integers(-4, 5, size=(n, H)).astype(np.float32))
+
+
+def grid_router_weight(E, H, *key):
+    """float32 gate ``[E, H]``: integers from -64..64 times 2^-12.  Against
+    ``grid_activations`` every product and every partial sum of a row of up to
+    8192 terms is a multiple of 2^-12 below 2^12 in magnitude, so float32
+    arithmetic computes the logits exactly in any order."""
+    ints = rng("wgrid", *key).integers(-64, 65, size=(E, H)).astype(np.float32)
+    return (ints * np.float32(2.0 ** -12)).astype(np.float32)
+
+
 def normal_logits(n, E, *key):
     """float32 ``[n, E]`` router logits drawn from N(0, 1)."""
     return rng("logits", *key).standard_normal((n, E), dtype=np.float32)

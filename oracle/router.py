@@ -33,6 +33,14 @@ Readings where the paper is silent (all listed with the design notes):
 import numpy as np
 
 
+def gate_logits(x_bits, w_r):
+    """Router affinities ``l = x W_r^T``: bfloat16 bit patterns ``[n, H]`` and a
+    float32 gate ``[E, H]`` -> float64 ``[n, E]`` (Section 3.2 routes on these;
+    the paper's model computes them in float32 from the hidden state)."""
+    x = (np.asarray(x_bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return x @ np.asarray(w_r, dtype=np.float32).astype(np.float64).T
+
+
 def sigmoid_f32(logits):
     """float32(1 / (1 + exp(-l))) with the expression evaluated in float64."""
     l64 = np.asarray(logits, dtype=np.float32).astype(np.float64)

@@ -63,6 +63,8 @@ struct moeq_layer {
   uint8_t* mask = nullptr;
   float* bias = nullptr;
   int32_t* kept_ids = nullptr;  // kept experts ascending, when the router regroups them
+  float* router_w = nullptr;    // float32 [n_experts x hidden] gate weight, when set
+  float* gate_logits = nullptr; // float32 [max_tokens x n_experts], logits the forward computes
   void* ws_mem = nullptr;
   Workspace ws{};
   hipEvent_t stage_events[MOEQ_STAGE_EVENTS] = {};
@@ -78,6 +80,8 @@ void release(moeq_layer* L) {
   hipFree(L->mask);
   hipFree(L->bias);
   hipFree(L->kept_ids);
+  hipFree(L->router_w);
+  hipFree(L->gate_logits);
   hipFree(L->ws_mem);
   delete L;
 }
@@ -413,8 +417,10 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   if (n > L->cfg.max_tokens)
     return fail(MOEQ_ERR_CAPACITY, "n_tokens %d exceeds max_tokens %d", n, L->cfg.max_tokens);
   if (n == 0) return ok();
-  if (!x || !logits || !y) return fail(MOEQ_ERR_INVALID_ARG, "x, logits and y must not be NULL");
-  if (!aligned16(x) || !aligned16(y) || !aligned16(logits))
+  if (!x || !y) return fail(MOEQ_ERR_INVALID_ARG, "x and y must not be NULL");
+  if (!logits && !L->router_w)
+    return fail(MOEQ_ERR_INVALID_ARG, "logits is NULL and no router weight is set");
+  if (!aligned16(x) || !aligned16(y) || (logits && !aligned16(logits)))
     return fail(MOEQ_ERR_INVALID_ARG, "x, logits and y must be 16-byte aligned");
   moeq_status st = check_device(L);
   if (st != MOEQ_OK) return st;
@@ -450,6 +456,11 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
     if (L->timing && e == hipSuccess) e = hipEventRecord(L->stage_events[i], s);
   };
   mark(0);
+  if (!logits) {
+    if (e == hipSuccess)
+      e = launch_router_gate(a.x, L->router_w, n, a.H, a.E, L->gate_logits, s);
+    logits = L->gate_logits;
+  }
   if (e == hipSuccess) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
   mark(1);
   if (e == hipSuccess) e = prefill ? launch_gateup_prefill(a, s) : launch_gateup_decode(a, s);
@@ -460,6 +471,56 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   mark(4);
   if (e != hipSuccess) return hip_fail(e, prefill ? "forward (prefill path)" : "forward (decode path)");
   return ok();
+}
+
+moeq_status moeq_set_router_weight(moeq_layer* L, const float* w, int32_t location) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (location != MOEQ_WEIGHTS_HOST && location != MOEQ_WEIGHTS_DEVICE)
+    return fail(MOEQ_ERR_INVALID_ARG, "location %d is neither HOST nor DEVICE", location);
+  const int E = L->cfg.n_experts, H = L->cfg.hidden;
+  const size_t wb = (size_t)E * H * 4;
+  if (w && location == MOEQ_WEIGHTS_HOST)
+    for (size_t i = 0; i < (size_t)E * H; ++i)
+      if (!isfinite(w[i])) return fail(MOEQ_ERR_INVALID_ARG, "router weight element %zu is not finite", i);
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "set_router_weight");
+  if (!w) {
+    hipFree(L->router_w);
+    hipFree(L->gate_logits);
+    L->router_w = nullptr;
+    L->gate_logits = nullptr;
+    return ok();
+  }
+  if (!L->router_w) {
+    float *rw = nullptr, *lg = nullptr;
+    if ((e = hipMalloc((void**)&rw, wb)) != hipSuccess) return hip_fail(e, "hipMalloc(router weight)");
+    if ((e = hipMalloc((void**)&lg, (size_t)L->cfg.max_tokens * E * 4)) != hipSuccess) {
+      hipFree(rw);
+      return hip_fail(e, "hipMalloc(router logits)");
+    }
+    L->router_w = rw;
+    L->gate_logits = lg;
+  }
+  e = hipMemcpy(L->router_w, w, wb, location == MOEQ_WEIGHTS_HOST ? hipMemcpyHostToDevice : hipMemcpyDeviceToDevice);
+  if (e != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "hipMemcpy(router weight)");
+  return ok();
+}
+
+moeq_status moeq_router_logits(moeq_layer* L, const void* x, int32_t n, float* logits, void* stream) {
+  if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (n < 0 || n > L->cfg.max_tokens)
+    return fail(n < 0 ? MOEQ_ERR_INVALID_ARG : MOEQ_ERR_CAPACITY, "n_tokens %d outside 0..max_tokens", n);
+  if (n == 0) return ok();
+  if (!x || !logits) return fail(MOEQ_ERR_INVALID_ARG, "x and logits must not be NULL");
+  if (!aligned16(x)) return fail(MOEQ_ERR_INVALID_ARG, "x must be 16-byte aligned");
+  if (!L->router_w) return fail(MOEQ_ERR_INVALID_ARG, "no router weight is set");
+  moeq_status st = check_device(L);
+  if (st != MOEQ_OK) return st;
+  const hipError_t e = launch_router_gate((const uint16_t*)x, L->router_w, n, L->cfg.hidden, L->cfg.n_experts,
+                                          logits, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "router gate launch");
 }
 
 moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,

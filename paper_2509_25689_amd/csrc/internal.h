@@ -112,6 +112,11 @@ struct DecodeArgs {
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
+// gate.hip: logits = x W_r^T (bf16 x [n x H], float32 W_r [E x H]); up to
+// kGateFewTokens tokens take the streaming kernel, more the tiled one
+constexpr int kGateFewTokens = 8;
+hipError_t launch_router_gate(const uint16_t* x, const float* w, int n, int H, int E, float* logits,
+                              hipStream_t s);
 // prune.hip
 hipError_t launch_fill_u8(uint8_t* p, int n, uint8_t v, hipStream_t s);
 hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm, const float* w, int E, int n,

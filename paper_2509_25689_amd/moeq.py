@@ -77,6 +77,8 @@ def _load():
         "moeq_quantize": [P, I32, I32, I32, P, P, P],
         "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
         "moeq_set_stage_events": [P, ctypes.POINTER(P), I32],
+        "moeq_set_router_weight": [P, P, I32],
+        "moeq_router_logits": [P, P, I32, P, P],
         "moeq_expert_importance": [ctypes.POINTER(moeq_config), P, P, I32, ctypes.c_double, ctypes.c_double,
                                    P, P, P, P],
     }
@@ -120,6 +122,14 @@ def moeq_layer_create(cfg, expert_mask, score_bias, routed, shared, weights_loca
 
 def moeq_forward(layer, x, logits, n_tokens, y, stream=0):
     _check(lib.moeq_forward(layer, x, logits, n_tokens, y, stream or None))
+
+
+def moeq_set_router_weight(layer, w, location):
+    _check(lib.moeq_set_router_weight(layer, w or None, location))
+
+
+def moeq_router_logits(layer, x, n_tokens, logits, stream=0):
+    _check(lib.moeq_router_logits(layer, x, n_tokens, logits, stream or None))
 
 
 def moeq_destroy(layer):
@@ -251,15 +261,38 @@ class Layer:
         import torch
         return torch.cuda.current_stream().cuda_stream
 
-    def forward(self, x, logits, y=None, stream=None):
-        """x: bf16 CUDA tensor [n, H]; logits: float32 CUDA tensor [n, E] -> y float32 [n, H]."""
+    def forward(self, x, logits=None, y=None, stream=None):
+        """x: bf16 CUDA tensor [n, H]; logits: float32 CUDA tensor [n, E], or None
+        to let the layer compute them with its router weight -> y float32 [n, H]."""
         import torch
         n = x.shape[0]
         if y is None:
             y = torch.empty((n, self.shape.hidden), dtype=torch.float32, device=x.device)
-        moeq_forward(self.handle, x.data_ptr(), logits.data_ptr(), n, y.data_ptr(),
-                     self._stream(stream))
+        moeq_forward(self.handle, x.data_ptr(), 0 if logits is None else logits.data_ptr(), n,
+                     y.data_ptr(), self._stream(stream))
         return y
+
+    def set_router_weight(self, w):
+        """w: float32 [E, H], a numpy array (host) or CUDA tensor (device); None removes it."""
+        if w is None:
+            moeq_set_router_weight(self.handle, 0, MOEQ_WEIGHTS_HOST)
+            return
+        if hasattr(w, "data_ptr"):
+            self._router_w = w.contiguous()
+            moeq_set_router_weight(self.handle, self._router_w.data_ptr(), MOEQ_WEIGHTS_DEVICE)
+        else:
+            import numpy as np
+            self._router_w = np.ascontiguousarray(w, dtype=np.float32)
+            moeq_set_router_weight(self.handle, self._router_w.ctypes.data, MOEQ_WEIGHTS_HOST)
+        self._router_w = None
+
+    def router_logits(self, x, stream=None):
+        """x: bf16 CUDA tensor [n, H] -> float32 logits [n, E] from the set router weight."""
+        import torch
+        n = x.shape[0]
+        out = torch.empty((n, self.shape.n_experts), dtype=torch.float32, device=x.device)
+        moeq_router_logits(self.handle, x.data_ptr(), n, out.data_ptr(), self._stream(stream))
+        return out
 
     def route(self, logits, stream=None):
         import torch

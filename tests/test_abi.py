@@ -151,6 +151,8 @@ def test_entry_points_reject_null_layer():
     assert L.moeq_dequant(None, 0, 0, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_set_path(None, 0) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_layer_bytes(None, None, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_set_router_weight(None, 1, moeq.MOEQ_WEIGHTS_HOST) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_router_logits(None, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     L.moeq_destroy(None)                             # NULL-safe
 
 

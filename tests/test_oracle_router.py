@@ -188,3 +188,52 @@ def test_regroup_hand_example():
     idx_r, _ = router.route(lg, mask, regroup=True, **kw)
     assert idx_m[0].tolist() == [0, 2]
     assert idx_r[0].tolist() == [4, 2]
+
+
+# ---------------------------------------------------------------------------
+# The router gate l = x W_r^T.
+def _bf16_value(bits):
+    """bfloat16 bits -> float, by sign, exponent and mantissa fields (normals and zero)."""
+    b = int(bits)
+    sign = -1.0 if b >> 15 else 1.0
+    exp, man = (b >> 7) & 0xFF, b & 0x7F
+    if exp == 0:
+        return sign * man * 2.0 ** -133
+    return sign * (1.0 + man / 128.0) * 2.0 ** (exp - 127)
+
+
+def test_gate_logits_brute_force():
+    """Triple loop over tokens, experts and the hidden index, with x decoded field by field."""
+    x_bits = synth.activations(3, 32, "gate-brute")
+    w = synth.router_weight(5, 32, "gate-brute")
+    got = router.gate_logits(x_bits, w)
+    assert got.shape == (3, 5)
+    for t in range(3):
+        for e in range(5):
+            ref = sum(_bf16_value(x_bits[t, h]) * float(w[e, h]) for h in range(32))
+            assert abs(got[t, e] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+def test_gate_logits_one_hot_picks_a_column():
+    """x = unit vector e_h gives logits W_r[:, h]: catches a transposed gate."""
+    E, H = 6, 40
+    w = synth.router_weight(E, H, "gate-onehot")
+    for h in (0, 17, 39):
+        x = np.zeros(H, np.float32)
+        x[h] = 1.0
+        l = router.gate_logits(synth.bf16_from_f32(x)[None, :], w)
+        assert np.array_equal(l[0], w[:, h].astype(np.float64))
+
+
+def test_gate_grid_inputs_are_exact_in_float32():
+    """The grid generators' logits are integers times 2^-12 within float32's exact range."""
+    x_bits = synth.grid_activations(4, 7168, "gate-grid")
+    w = synth.grid_router_weight(8, 7168, "gate-grid")
+    l = router.gate_logits(x_bits, w)
+    units = l * 4096.0
+    assert np.array_equal(units, np.round(units))
+    assert np.abs(units).max() < 2 ** 24
+    # every partial sum is bounded by the sum of magnitudes
+    xa = np.abs((x_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64))
+    assert (xa @ np.abs(w.astype(np.float64)).T * 4096.0).max() < 2 ** 24
+    assert np.array_equal(l.astype(np.float32).astype(np.float64), l)
