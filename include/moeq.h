@@ -39,7 +39,8 @@
  *     are ordinary host memory;
  *   - stream arguments are hipStream_t values passed as void*; NULL means the
  *     default stream.  Work is enqueued asynchronously; no entry point except
- *     moeq_layer_create and moeq_destroy synchronizes the host;
+ *     moeq_layer_create, moeq_set_router_weight and moeq_destroy synchronizes
+ *     the host;
  *   - a layer handle owns one workspace, so calls on one handle must not run
  *     concurrently on different streams.
  */
@@ -262,6 +263,99 @@ moeq_status moeq_layer_bytes(const moeq_layer* layer, uint64_t* weight_bytes,
 moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,
                                    int32_t n_tokens, double alpha, double retain, double* importance,
                                    uint8_t* mask, int32_t* counts, void* stream);
+
+/* ---- Mixed-precision bit allocation (Section 3.3), host only ----------------
+ * These entry points run on the host, make no HIP call and need no device.
+ *
+ * Sensitivity of each tensor (Section 3.3's tensor-level analysis):
+ *   sens[t] = (ppl_low - ppl_high[t]) / rho_t,  rho_t = params[t] / layer_params[t]
+ * in float64 (rho_t first, then one subtraction and one division).
+ *   ppl_low       perplexity with every tensor at the base width
+ *   ppl_high      HOST double [n]: perplexity with tensor t alone raised
+ *   params, layer_params  HOST int64 [n], positive, params[t] <= layer_params[t]
+ *   sens          HOST double [n] (written)
+ * Errors: INVALID_ARG (NULL, n < 0, non-finite perplexity, bad counts). */
+moeq_status moeq_sensitivity(int32_t n, double ppl_low, const double* ppl_high, const int64_t* params,
+                             const int64_t* layer_params, double* sens);
+
+/* The order in which rule 3 of the back-off visits MoE layers: a breadth-first
+ * binary partition of the layer positions 0..n_layers-1 over half-open
+ * intervals [lo, hi), each contributing position ceil((lo + hi) / 2) (lo for an
+ * interval of one) and splitting into [lo, mid) and [mid + 1, hi).  For 58
+ * layers it begins 29, 15, 44, 8, 23, 37, 52.
+ *   order  HOST int32 [n_layers] (written), n_layers 1..4096 */
+moeq_status moeq_layer_order(int32_t n_layers, int32_t* order);
+
+/* Tensor kinds for moeq_plan_bits. */
+enum {
+  MOEQ_TENSOR_OTHER = 0,        /* may be upgraded by its size tier */
+  MOEQ_TENSOR_ROUTED_GATE = 1,  /* routed-expert tensors: never upgraded, */
+  MOEQ_TENSOR_ROUTED_UP = 2,    /* lowered to Q_low' by rule 3 */
+  MOEQ_TENSOR_ROUTED_DOWN = 3
+};
+
+#define MOEQ_PLAN_MAX_LEVELS 8
+
+/* The width ladder and budget of a plan.  Widths are bits per weight,
+ * scales included, in units of 1/64 bit (so 1.75 -> 112, 4.5 -> 288), strictly
+ * increasing.  Level indices satisfy low_prime < low < floor <= medium_level
+ * <= small_level < n_levels. */
+typedef struct {
+  int32_t n_levels;                       /* 3..MOEQ_PLAN_MAX_LEVELS */
+  int32_t width64[MOEQ_PLAN_MAX_LEVELS];  /* 1..4096 each */
+  int32_t low_prime;                      /* Q_low': rule 3's target for routed experts */
+  int32_t low;                            /* Q_low: every tensor's starting width */
+  int32_t floor;                          /* Q4: no upgraded tensor ends below it */
+  int32_t small_level;                    /* target below small_params parameters (Q8) */
+  int32_t medium_level;                   /* target up to medium_params parameters (Q6) */
+  int64_t small_params;                   /* 10,000,000 in the paper */
+  int64_t medium_params;                  /* 50,000,000 in the paper */
+  uint64_t m_limit_bytes;                 /* M_limit, at most 2^50 */
+  int32_t n_moe_layers;                   /* positions of routed tensors: 0..n_moe_layers-1 */
+} moeq_plan_params;
+
+/* Budget figures of a plan; GB are 10^9 bytes. */
+typedef struct {
+  double s_low_gb;     /* S_low: every tensor at Q_low */
+  double b_base_gb;    /* B_base = M_limit - S_low */
+  double b_delta_gb;   /* released by rule 3 (sum of B_delta) */
+  double b_total_gb;   /* B_base + b_delta */
+  double upgrade_gb;   /* the upgrades' extra bytes, <= b_total when feasible */
+  double total_gb;     /* size of the planned model */
+  int32_t n_upgraded;  /* tensors left above Q_low */
+  int32_t n_rule2;     /* one-level downgrades of earlier upgrades */
+  int32_t n_rule3;     /* routed tensors lowered to Q_low' */
+  int32_t feasible;    /* 1 if total <= M_limit */
+} moeq_plan_report;
+
+/* Dynamic allocation with back-off (Section 3.3): every tensor starts at
+ * Q_low; tensors that are not routed experts are taken in descending
+ * sensitivity (ties: lower index first) and raised to small_level (fewer than
+ * small_params parameters) or medium_level (up to medium_params; larger ones
+ * are not raised) while the upgrades' extra bits fit B_total.  When one does
+ * not fit: (1) it is tried one, then two levels lower (not below floor);
+ * (2) failing that, the upgraded tensor with the most parameters (ties: the
+ * later in sensitivity order) is lowered one level, never below floor, and
+ * (3) when none is left, the next routed tensor in rule 3's order (the gate
+ * and up tensors of the layers in moeq_layer_order, then their down tensors;
+ * ties by index) is lowered from Q_low to Q_low', raising B_total, until the
+ * tensor fits at the lowest level rule 1 tried.  Rules 2 and 3 run only if
+ * together they can make it fit; otherwise it stays at Q_low.  If Q_low alone
+ * exceeds M_limit, rule 3 runs first.  All fit decisions are exact integer
+ * comparisons in 1/64-bit units, so the plan is deterministic.
+ *   p         HOST; the ladder and budget
+ *   n         number of tensors, 1..2^20; sum of params <= 2^45
+ *   params    HOST int64 [n], positive
+ *   sens      HOST double [n], finite
+ *   kind      HOST int32 [n], MOEQ_TENSOR_*
+ *   layer     HOST int32 [n]: MoE layer position of routed tensors (ignored
+ *             for others); NULL only if no tensor is routed
+ *   level     HOST int32 [n] (written): each tensor's ladder level
+ *   report    HOST (written) or NULL
+ * Errors: INVALID_ARG (arguments, ladder, sizes).  An infeasible budget is
+ * not an error: the plan is returned with report->feasible = 0. */
+moeq_status moeq_plan_bits(const moeq_plan_params* p, int32_t n, const int64_t* params, const double* sens,
+                           const int32_t* kind, const int32_t* layer, int32_t* level, moeq_plan_report* report);
 
 /* Benchmark instrumentation: stage boundaries of moeq_forward.
  *   events  NULL (count 0) to stop, or MOEQ_STAGE_EVENTS hipEvent_t handles

@@ -194,3 +194,59 @@ def zipf_logits(n, mask, *key, s=1.1):
     logp -= np.log(np.sum(np.arange(1, len(kept) + 1, dtype=np.float64) ** -s))
     gumbel = r.gumbel(0.0, 1.0, size=(n, E))
     return (logp[None, :] + gumbel).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Model-level inventory for the bit-allocation planner.
+def v3_tensor_inventory(n_kept=192):
+    """The quantizable matrices of a DeepSeek-V3-architecture model (61 layers,
+    the first 3 dense, 58 MoE; multi-head latent attention with q rank 1536,
+    kv rank 512, 128 heads of 128 + 64 rope dims; dense intermediate 18432;
+    one shared and ``n_kept`` routed experts of intermediate 2048; vocabulary
+    129280), one entry per matrix, routed experts as one tensor per layer and
+    projection.  Norm vectors are left out.
+
+    Returns (names, params, kind, layer, layer_params): kind 0 = other,
+    1/2/3 = routed gate/up/down; layer = MoE layer position (0..57) of routed
+    tensors, else -1; layer_params = parameters of the tensor's layer (the
+    tensor itself for the embedding and output matrices)."""
+    H, vocab, heads = 7168, 129280, 128
+    attn = {"attn_q_a": H * 1536, "attn_q_b": 1536 * heads * 192, "attn_kv_a_mqa": H * 576,
+            "attn_kv_b": 512 * heads * 256, "attn_output": heads * 128 * H}
+    names, params, kind, layer, owner = [], [], [], [], []
+
+    def add(name, p, k=0, pos=-1, lid=None):
+        names.append(name)
+        params.append(int(p))
+        kind.append(k)
+        layer.append(pos)
+        owner.append(lid)
+    add("token_embd", vocab * H, lid="token_embd")
+    for L in range(61):
+        for a, p in attn.items():
+            add(f"blk.{L}.{a}", p, lid=L)
+        if L < 3:
+            for f in ("ffn_gate", "ffn_up", "ffn_down"):
+                add(f"blk.{L}.{f}", H * 18432, lid=L)
+            continue
+        pos = L - 3
+        add(f"blk.{L}.ffn_gate_inp", 256 * H, lid=L)
+        for f in ("ffn_gate_shexp", "ffn_up_shexp", "ffn_down_shexp"):
+            add(f"blk.{L}.{f}", H * 2048, lid=L)
+        for k, f in ((1, "ffn_gate_exps"), (2, "ffn_up_exps"), (3, "ffn_down_exps")):
+            add(f"blk.{L}.{f}", n_kept * H * 2048, k, pos, lid=L)
+    add("output", vocab * H, lid="output")
+    totals = {}
+    for p, o in zip(params, owner):
+        totals[o] = totals.get(o, 0) + p
+    layer_params = [totals[o] for o in owner]
+    return names, params, kind, layer, layer_params
+
+
+def synthetic_perplexities(params, layer_params, *key, ppl_low=12.0):
+    """Seeded stand-ins for PPL(Q_low) and PPL(Q_high, t): raising tensor t
+    lowers the perplexity by rho_t * 0.05 * LogNormal(0, 1)."""
+    r = rng("ppl", *key)
+    rho = np.asarray(params, np.float64) / np.asarray(layer_params, np.float64)
+    drop = rho * 0.05 * np.exp(r.standard_normal(len(params)))
+    return float(ppl_low), (ppl_low - drop).astype(np.float64)

@@ -18,16 +18,23 @@
 using namespace moeq;
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+moeq_status moeq::vset_error(moeq_status st, const char* fmt, va_list ap) {
+  char buf[512];
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  g_last_error = buf;
+  return st;
+}
+
+namespace {
 
 moeq_status fail(moeq_status st, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vset_error(st, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return st;
 }
 

@@ -3,11 +3,15 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stdarg.h>
 #include <stdint.h>
 
 #include "moeq.h"
 
 namespace moeq {
+
+// Records the calling thread's error text (moeq_last_error) and returns st.
+moeq_status vset_error(moeq_status st, const char* fmt, va_list ap);
 
 // Weights per device unit: four blocks of 32.  A lane of a GEMV wave owns one
 // unit of a row at a time; hidden and inter must be multiples of this.

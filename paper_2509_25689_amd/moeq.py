@@ -53,6 +53,26 @@ class moeq_qtensor(ctypes.Structure):
                 ("scales", ctypes.c_void_p)]
 
 
+MOEQ_TENSOR_OTHER, MOEQ_TENSOR_ROUTED_GATE, MOEQ_TENSOR_ROUTED_UP, MOEQ_TENSOR_ROUTED_DOWN = 0, 1, 2, 3
+MOEQ_PLAN_MAX_LEVELS = 8
+
+
+class moeq_plan_params(ctypes.Structure):
+    _fields_ = [("n_levels", ctypes.c_int32), ("width64", ctypes.c_int32 * MOEQ_PLAN_MAX_LEVELS),
+                ("low_prime", ctypes.c_int32), ("low", ctypes.c_int32), ("floor", ctypes.c_int32),
+                ("small_level", ctypes.c_int32), ("medium_level", ctypes.c_int32),
+                ("small_params", ctypes.c_int64), ("medium_params", ctypes.c_int64),
+                ("m_limit_bytes", ctypes.c_uint64), ("n_moe_layers", ctypes.c_int32)]
+
+
+class moeq_plan_report(ctypes.Structure):
+    _fields_ = [("s_low_gb", ctypes.c_double), ("b_base_gb", ctypes.c_double),
+                ("b_delta_gb", ctypes.c_double), ("b_total_gb", ctypes.c_double),
+                ("upgrade_gb", ctypes.c_double), ("total_gb", ctypes.c_double),
+                ("n_upgraded", ctypes.c_int32), ("n_rule2", ctypes.c_int32),
+                ("n_rule3", ctypes.c_int32), ("feasible", ctypes.c_int32)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
@@ -78,6 +98,10 @@ def _load():
         "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
         "moeq_set_stage_events": [P, ctypes.POINTER(P), I32],
         "moeq_set_router_weight": [P, P, I32],
+        "moeq_sensitivity": [I32, ctypes.c_double, P, P, P, P],
+        "moeq_layer_order": [I32, P],
+        "moeq_plan_bits": [ctypes.POINTER(moeq_plan_params), I32, P, P, P, P, P,
+                           ctypes.POINTER(moeq_plan_report)],
         "moeq_router_logits": [P, P, I32, P, P],
         "moeq_expert_importance": [ctypes.POINTER(moeq_config), P, P, I32, ctypes.c_double, ctypes.c_double,
                                    P, P, P, P],
@@ -130,6 +154,52 @@ def moeq_set_router_weight(layer, w, location):
 
 def moeq_router_logits(layer, x, n_tokens, logits, stream=0):
     _check(lib.moeq_router_logits(layer, x, n_tokens, logits, stream or None))
+
+
+def moeq_sensitivity(ppl_low, ppl_high, params, layer_params):
+    """-> numpy float64 [n]: Sens(t) for every tensor."""
+    import numpy as np
+    ph = np.ascontiguousarray(ppl_high, dtype=np.float64)
+    pa = np.ascontiguousarray(params, dtype=np.int64)
+    lp = np.ascontiguousarray(layer_params, dtype=np.int64)
+    out = np.empty(len(ph), np.float64)
+    _check(lib.moeq_sensitivity(len(ph), float(ppl_low), ph.ctypes.data, pa.ctypes.data, lp.ctypes.data,
+                                out.ctypes.data))
+    return out
+
+
+def moeq_layer_order(n_layers):
+    import numpy as np
+    out = np.empty(max(n_layers, 0), np.int32)
+    _check(lib.moeq_layer_order(n_layers, out.ctypes.data if n_layers > 0 else None))
+    return out
+
+
+def plan_params(*, ladder, low_prime, low, floor, small_level, medium_level, m_limit_bytes, n_moe_layers,
+                small_params=10_000_000, medium_params=50_000_000):
+    p = moeq_plan_params()
+    p.n_levels = len(ladder)
+    for i, v in enumerate(ladder[:MOEQ_PLAN_MAX_LEVELS]):
+        p.width64[i] = int(v)
+    p.low_prime, p.low, p.floor = low_prime, low, floor
+    p.small_level, p.medium_level = small_level, medium_level
+    p.small_params, p.medium_params = small_params, medium_params
+    p.m_limit_bytes, p.n_moe_layers = m_limit_bytes, n_moe_layers
+    return p
+
+
+def moeq_plan_bits(p, params, sens, kind, layer):
+    """-> (levels numpy int32 [n], moeq_plan_report)."""
+    import numpy as np
+    pa = np.ascontiguousarray(params, dtype=np.int64)
+    se = np.ascontiguousarray(sens, dtype=np.float64)
+    ki = np.ascontiguousarray(kind, dtype=np.int32)
+    la = None if layer is None else np.ascontiguousarray(layer, dtype=np.int32)
+    levels = np.empty(len(pa), np.int32)
+    rep = moeq_plan_report()
+    _check(lib.moeq_plan_bits(ctypes.byref(p), len(pa), pa.ctypes.data, se.ctypes.data, ki.ctypes.data,
+                              None if la is None else la.ctypes.data, levels.ctypes.data, ctypes.byref(rep)))
+    return levels, rep
 
 
 def moeq_destroy(layer):
