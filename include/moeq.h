@@ -11,7 +11,8 @@
  *     activates (top_k) and how grouped routing restricts them (topk_group);
  *   - mixed-precision quantization (Section 3.3) gives every weight tensor
  *     its own low bit width.  This library stores tensors in a symmetric
- *     block format (32 weights per binary16 scale, 2/3/4-bit codes) instead
+ *     block format (32 weights per binary16 scale, 2/3/4-bit codes, and
+ *     5/6/8-bit codes for the tensors the allocation upgrades) instead
  *     of the paper's llama.cpp formats;
  *   - each expert is a SwiGLU feed-forward network and the layer output is
  *     the routing-weighted sum of the chosen experts plus the shared
@@ -109,7 +110,7 @@ typedef struct {
 } moeq_config;
 
 /* One quantized tensor in the canonical packing described above.
- *   bits    2, 3 or 4
+ *   bits    2, 3, 4, 5, 6 or 8 (any tensor may take any of them)
  *   codes   rows * K * bits / 8 bytes
  *   scales  rows * K / 32 binary16 bit patterns */
 typedef struct {
@@ -136,7 +137,8 @@ typedef struct {
  * kept / n_group experts must hold top_k) (else INVALID_ARG).
  * All weight data is copied and re-laid-out on the device; the caller may
  * free its buffers when this returns.  Synchronizes the device.
- * Errors: INVALID_ARG, UNSUPPORTED (widths or shapes), OUT_OF_MEMORY, DEVICE;
+ * Errors: INVALID_ARG (including widths outside {2,3,4,5,6,8}), UNSUPPORTED
+ * (shapes), OUT_OF_MEMORY, DEVICE;
  * on error *out is set to NULL and nothing is leaked. */
 moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask,
                               const float* score_bias, const moeq_qtensor* routed,
@@ -225,7 +227,7 @@ moeq_status moeq_dequant(moeq_layer* layer, int32_t expert, int32_t proj, float*
  * the exact quotient, codes clamp(rint(w/d)) + 2^(b-1) (ties to even; all
  * codes 2^(b-1) when d = 0).
  *   w       DEVICE float32 [rows x K], K a multiple of 32, finite
- *   bits    2, 3 or 4
+ *   bits    2, 3, 4, 5, 6 or 8
  *   codes   DEVICE [rows * K * bits / 8] bytes
  *   scales  DEVICE uint16 [rows * K / 32] */
 moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits,

@@ -97,16 +97,23 @@ def expert_mask(shape, *key):
 def bit_plan(shape, plan, *key):
     """Per-tensor widths: (routed int32 ``[E, 3]``, shared int32 ``[n_shared, 3]``).
 
-    Plans: ``all2``/``all4``/``all3``; ``gu3_d4_sh4`` (routed gate/up 3, routed
-    down 4, shared 4); ``p234_<pppppp>`` (each tensor drawn from {2,3,4} with
-    the given percentages); ``mixed`` (shared 4-bit, routed 2-bit)."""
+    Plans: ``all2``/``all4``/``all3``/``all5``/``all6``/``all8``;
+    ``gu3_d4_sh<b>`` (routed gate/up 3, routed down 4, shared experts b bits,
+    e.g. 6 or 8 for the upgraded shared expert); ``p234_<pppppp>`` (each
+    tensor drawn from {2,3,4} with the given percentages); ``wide_all`` (each
+    tensor drawn uniformly from {2,3,4,5,6,8}); ``mixed`` (shared 4-bit,
+    routed 2-bit)."""
     E, S = shape.n_experts, shape.n_shared
     if plan.startswith("all"):
         b = int(plan[3:])
         return np.full((E, 3), b, np.int32), np.full((S, 3), b, np.int32)
-    if plan == "gu3_d4_sh4":
+    if plan.startswith("gu3_d4_sh"):
         routed = np.tile(np.array([3, 3, 4], np.int32), (E, 1))
-        return routed, np.full((S, 3), 4, np.int32)
+        return routed, np.full((S, 3), int(plan[len("gu3_d4_sh"):]), np.int32)
+    if plan == "wide_all":
+        r = rng("bits", plan, *key)
+        widths = np.array([2, 3, 4, 5, 6, 8], np.int32)
+        return r.choice(widths, size=(E, 3)).astype(np.int32), r.choice(widths, size=(S, 3)).astype(np.int32)
     if plan == "mixed":
         return np.full((E, 3), 2, np.int32), np.full((S, 3), 4, np.int32)
     if plan.startswith("p234_"):

@@ -69,6 +69,7 @@ struct moeq_layer {
   TensorDev* desc = nullptr;
   uint8_t* mask = nullptr;
   float* bias = nullptr;
+  int wide_gateup = 0, wide_down = 0;  // 0: no 5/6/8-bit tensor, 1: shared experts only, 2: routed too
   int32_t* kept_ids = nullptr;  // kept experts ascending, when the router regroups them
   float* router_w = nullptr;    // float32 [n_experts x hidden] gate weight, when set
   float* gate_logits = nullptr; // float32 [max_tokens x n_experts], logits the forward computes
@@ -130,10 +131,11 @@ moeq_status check_config(const moeq_config* c) {
   return ok();
 }
 
+bool valid_bits(int b) { return (b >= 2 && b <= 6) || b == 8; }
+
 moeq_status check_tensor(const moeq_qtensor& t, const char* who, int e, int p) {
-  if (t.bits < 2 || t.bits > 4)
-    return fail(t.bits == 5 || t.bits == 6 || t.bits == 8 ? MOEQ_ERR_UNSUPPORTED : MOEQ_ERR_INVALID_ARG,
-                "%s %d proj %d: bits %d not in {2,3,4}", who, e, p, t.bits);
+  if (!valid_bits(t.bits))
+    return fail(MOEQ_ERR_INVALID_ARG, "%s %d proj %d: bits %d not in {2,3,4,5,6,8}", who, e, p, t.bits);
   if (!t.codes || !t.scales) return fail(MOEQ_ERR_INVALID_ARG, "%s %d proj %d: NULL codes or scales", who, e, p);
   return ok();
 }
@@ -302,6 +304,16 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->decode_max = cfg->decode_max_tokens ? cfg->decode_max_tokens : kDefaultDecodeMax;
   L->weight_bytes = wbytes;
   L->ws_bytes = wo;
+  auto wide = [](const moeq_qtensor& t) { return t.bits > 4; };
+  for (int s = 0; s < S; ++s) {
+    if (wide(shared[s * 3 + 0]) || wide(shared[s * 3 + 1])) L->wide_gateup = 1;
+    if (wide(shared[s * 3 + 2])) L->wide_down = 1;
+  }
+  for (int e = 0; e < E; ++e)
+    if (expert_mask[e]) {
+      if (wide(routed[e * 3 + 0]) || wide(routed[e * 3 + 1])) L->wide_gateup = 2;
+      if (wide(routed[e * 3 + 2])) L->wide_down = 2;
+    }
   hipError_t he = hipGetDevice(&L->device);
   if (he != hipSuccess) {
     release(L);
@@ -456,6 +468,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.max_mtiles = prefill_max_mtiles(n, a.k, a.S, L->n_kept);
   a.x16 = L->ws.x16;
   a.h16 = L->ws.h16;
+  a.wide_gateup = L->wide_gateup;
+  a.wide_down = L->wide_down;
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
   hipError_t e = hipSuccess;
@@ -691,9 +705,7 @@ moeq_status moeq_quantize(const float* w, int32_t rows, int32_t K, int32_t bits,
                           uint16_t* scales, void* stream) {
   if (!w || !codes || !scales) return fail(MOEQ_ERR_INVALID_ARG, "w, codes and scales must not be NULL");
   if (rows < 0 || K < 0 || K % kBlock) return fail(MOEQ_ERR_INVALID_ARG, "rows %d / K %d invalid", rows, K);
-  if (bits < 2 || bits > 4)
-    return fail(bits == 5 || bits == 6 || bits == 8 ? MOEQ_ERR_UNSUPPORTED : MOEQ_ERR_INVALID_ARG,
-                "bits %d not in {2,3,4}", bits);
+  if (!valid_bits(bits)) return fail(MOEQ_ERR_INVALID_ARG, "bits %d not in {2,3,4,5,6,8}", bits);
   if (rows == 0 || K == 0) return ok();
   hipError_t e = launch_quantize(w, rows, K, bits, (uint8_t*)codes, scales, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "quantize launch");

@@ -599,6 +599,265 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wide tensors (5, 6 and 8 bits).  The kernels above skip a slot whose gate or
+// up (down) tensor is wide; these take exactly those slots.  Eight lanes per
+// row: lane j walks the units j, j + 8, ... of its row with the next unit in
+// flight, for up to TM tokens per pass.  Gate, up and down are reduced
+// one tensor at a time, so a wave decodes one width at a time.  TM: tokens per
+// pass (1 for a single token, else 4).
+
+__device__ __forceinline__ bool wide_bits(int b) { return b > 4; }
+
+template <int B>
+struct WideUnit {
+  uint32_t w[4 * B];
+  u32x2 s;
+};
+
+template <int B>
+__device__ __forceinline__ void wide_load(WideUnit<B>& b, const TensorDev& t, int row, int U, int u, int K) {
+  load_unit<B>(t.codes + (size_t)row * B * U * 4, U, u, b.w);
+  b.s = *gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (K / kBlock) + 4 * u));
+}
+
+// acc[m] += d * sum (c - z) x_m over one unit, for the mc staged tokens
+template <int B, int NX, int TM>
+__device__ __forceinline__ void wide_unit_dot(const WideUnit<B>& b, const uint32_t* xu, int xts, int lo,
+                                              const float* su4, int sts, int mc, float (&acc)[TM]) {
+  const PairConsts pk = pair_consts();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float d = half_to_float(((q < 2 ? b.s.x : b.s.y) >> (16 * (q & 1))) & 0xFFFFu);
+    if constexpr (B == 8) {
+      // two 4-bit planes: d (c - 128) = 16 d (hi - 8) + d (lo - 8) + 8 d
+      uint32_t p[16];
+      block_pairs<4>(b.w + 8 * q + 4, pk, p);
+#pragma unroll
+      for (int m = 0; m < TM; ++m)
+        if (m < mc) acc[m] = block_dot<NX>(p, xu + m * xts + 16 * q, lo, 2.0f * d, su4[m * sts + q], acc[m]);
+      block_pairs<4>(b.w + 8 * q, pk, p);
+#pragma unroll
+      for (int m = 0; m < TM; ++m) {
+        if (m < mc) {
+          const float X = su4[m * sts + q];
+          acc[m] = fmaf(8.0f * d, X, block_dot<NX>(p, xu + m * xts + 16 * q, lo, 0.125f * d, X, acc[m]));
+        }
+      }
+    } else {
+      uint32_t p[16];
+      block_pairs<B>(b.w + q * B, pk, p);
+      const float ds = d * (1.0f / (float)(1 << (7 - B)));
+#pragma unroll
+      for (int m = 0; m < TM; ++m)
+        if (m < mc) acc[m] = block_dot<NX>(p, xu + m * xts + 16 * q, lo, ds, su4[m * sts + q], acc[m]);
+    }
+  }
+}
+
+template <int TM>
+struct WideAcc {
+  float v[TM];
+};
+
+// The staged tokens live in the kernel's dynamic LDS; naming it here (not
+// through a pointer argument) keeps the accesses LDS instructions.
+extern __shared__ uint32_t wide_lds[];
+
+// This lane's share (units j, j + 8, ...) of row `row` against the staged
+// tokens.  Not inlined: one function per width keeps each width's registers
+// to itself (inlined together, the allocator merges all six).
+template <int B, int NX, int TM>
+__device__ __noinline__ WideAcc<TM> wide_row_dot(const TensorDev t, int row, int U, int K, int j, int xts, int lo,
+                                                 int sts, int mc) {
+  const uint32_t* xl = wide_lds;
+  const float* xs = reinterpret_cast<const float*>(wide_lds + TM * xts);
+  WideAcc<TM> r;
+#pragma unroll
+  for (int m = 0; m < TM; ++m) r.v[m] = 0.0f;
+  const int UPL = (U + 7) / 8;
+  WideUnit<B> buf[2];
+  wide_load<B>(buf[0], t, row, U, min(j, U - 1), K);
+#pragma unroll 1
+  for (int i0 = 0; i0 < UPL; i0 += 2) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int i = i0 + b;
+      if (i < UPL) {
+        // the next unit (clamped to the last valid one) goes out before this one is reduced
+        wide_load<B>(buf[1 - b], t, row, U, min(j + 8 * min(i + 1, UPL - 1), U - 1), K);
+        const int u = j + 8 * i;
+        if (u < U) wide_unit_dot<B, NX, TM>(buf[b], xl + u * kXStride, xts, lo, xs + u * 4, sts, mc, r.v);
+      }
+    }
+  }
+  return r;
+}
+
+template <int NX, int TM>
+__device__ __forceinline__ WideAcc<TM> wide_row_dot_any(const TensorDev& t, int row, int U, int K, int j, int xts,
+                                                        int lo, int sts, int mc) {
+  switch (t.bits) {
+    case 2: return wide_row_dot<2, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    case 3: return wide_row_dot<3, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    case 4: return wide_row_dot<4, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    case 5: return wide_row_dot<5, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    case 6: return wide_row_dot<6, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    default: return wide_row_dot<8, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+  }
+}
+
+// grid = (ceil(I / 32), slots), 256 threads: 32 rows of one slot
+template <int TM>
+__global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  if (!wide_bits(tg.bits) && !wide_bits(tu.bits)) return;
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const int xts = U * kXStride, sts = U * 4;
+  uint32_t* xl = wide_lds;
+  float* xs = reinterpret_cast<float*>(wide_lds + TM * xts);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 32 + wave * 8 + (lane >> 3), j = lane & 7;
+  const int rowc = min(row, I - 1);
+  for (int m0 = 0; m0 < sl.M; m0 += TM) {
+    const int mc = min(TM, sl.M - m0);
+    __syncthreads();
+    for (int m = 0; m < mc; ++m) {
+      const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
+      const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
+      for (int q = threadIdx.x; q < H / 8; q += 256) {
+        const u32x4 v = src[q];
+        float s = 0.0f;
+        s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
+        s += bf16_lo(v.z); s += bf16_hi(v.z); s += bf16_lo(v.w); s += bf16_hi(v.w);
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        const int uu = q >> 4, cq = q & 15;
+        *reinterpret_cast<u32x4*>(xl + m * xts + uu * kXStride + cq * 4) = v;
+        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
+      }
+    }
+    __syncthreads();
+    const WideAcc<TM> g = wide_row_dot_any<1, TM>(tg, rowc, U, H, j, xts, 0, sts, mc);
+    const WideAcc<TM> u = wide_row_dot_any<1, TM>(tu, rowc, U, H, j, xts, 0, sts, mc);
+#pragma unroll
+    for (int m = 0; m < TM; ++m) {
+      if (m < mc) {
+        const float gs = half_sum8(g.v[m]), us = half_sum8(u.v[m]);
+        if (j == 7 && row < I) a.h[(size_t)(sl.base + m0 + m) * I + row] = silu(gs) * us;
+      }
+    }
+  }
+}
+
+// grid = (ceil(H / 32), slots), 256 threads: 32 rows of one slot's down tensor
+template <int TM>
+__global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
+  const TensorDev td = a.desc[sl.desc * 3 + 2];
+  if (!td.codes || !wide_bits(td.bits)) return;
+  const int H = a.H, I = a.I, U = I / kUnit;
+  const int xts = 2 * U * kXStride, sts = U * 4, lo = U * kXStride;
+  uint32_t* xl = wide_lds;
+  float* xs = reinterpret_cast<float*>(wide_lds + TM * xts);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 32 + wave * 8 + (lane >> 3), j = lane & 7;
+  const int rowc = min(row, H - 1);
+  for (int m0 = 0; m0 < sl.M; m0 += TM) {
+    const int mc = min(TM, sl.M - m0);
+    __syncthreads();
+    // h rows as bfloat16 hi + lo pairs; block sums of hi + lo
+    for (int m = 0; m < mc; ++m) {
+      const MOEQ_GLOBAL f32x4* src = gptr(reinterpret_cast<const f32x4*>(a.h + (size_t)(sl.base + m0 + m) * I));
+      for (int q = threadIdx.x; q < I / 8; q += 256) {
+        const f32x4 v0 = src[2 * q], v1 = src[2 * q + 1];
+        const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        uint32_t hi[4], lw[4];
+        float s = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t h0 = bf16_rne(f[2 * i]), h1 = bf16_rne(f[2 * i + 1]);
+          const uint32_t l0 = bf16_rne(f[2 * i] - __uint_as_float(h0 << 16));
+          const uint32_t l1 = bf16_rne(f[2 * i + 1] - __uint_as_float(h1 << 16));
+          hi[i] = h0 | h1 << 16;
+          lw[i] = l0 | l1 << 16;
+          s += __uint_as_float(h0 << 16) + __uint_as_float(l0 << 16);
+          s += __uint_as_float(h1 << 16) + __uint_as_float(l1 << 16);
+        }
+        s += __shfl_xor(s, 1, 64);
+        s += __shfl_xor(s, 2, 64);
+        const int uu = q >> 4, cq = q & 15;
+        uint32_t* dst = xl + m * xts + uu * kXStride + cq * 4;
+        *reinterpret_cast<u32x4*>(dst) = u32x4{hi[0], hi[1], hi[2], hi[3]};
+        *reinterpret_cast<u32x4*>(dst + lo) = u32x4{lw[0], lw[1], lw[2], lw[3]};
+        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
+      }
+    }
+    __syncthreads();
+    const WideAcc<TM> o = wide_row_dot_any<2, TM>(td, rowc, U, I, j, xts, lo, sts, mc);
+#pragma unroll
+    for (int m = 0; m < TM; ++m) {
+      if (m < mc) {
+        const float os = half_sum8(o.v[m]);
+        if (j == 7 && row < H) {
+          int prow;
+          float wv;
+          if (sl.shared >= 0) {
+            prow = a.n * a.k + sl.shared * a.n + m0 + m;
+            wv = 1.0f;
+          } else {
+            prow = a.perm[sl.base + m0 + m];
+            wv = a.w[prow];
+          }
+          a.partial[(size_t)prow * H + row] = wv * os;
+        }
+      }
+    }
+  }
+}
+
+// launches a kernel whose dynamic LDS may exceed the 64 KiB default
+template <typename K>
+hipError_t launch_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const DecodeArgs& a) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  kernel<<<grid, 256, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int TM>
+hipError_t launch_wide_gateup_tm(const DecodeArgs& a, hipStream_t s) {
+  const int U = a.H / kUnit;
+  const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
+  dim3 grid((a.I + 31) / 32, a.wide_gateup == 1 ? a.S : a.S + a.max_active);
+  return launch_lds(wide_gateup_kernel<TM>, grid, lds, s, a);
+}
+
+template <int TM>
+hipError_t launch_wide_down_tm(const DecodeArgs& a, hipStream_t s) {
+  const int U = a.I / kUnit;
+  const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
+  dim3 grid((a.H + 31) / 32, a.wide_down == 1 ? a.S : a.S + a.max_active);
+  return launch_lds(wide_down_kernel<TM>, grid, lds, s, a);
+}
+
+hipError_t launch_wide_gateup(const DecodeArgs& a, hipStream_t s) {
+  if (!a.wide_gateup) return hipSuccess;
+  return a.n == 1 ? launch_wide_gateup_tm<1>(a, s) : launch_wide_gateup_tm<4>(a, s);
+}
+
+hipError_t launch_wide_down(const DecodeArgs& a, hipStream_t s) {
+  if (!a.wide_down) return hipSuccess;
+  return a.n == 1 ? launch_wide_down_tm<1>(a, s) : launch_wide_down_tm<4>(a, s);
+}
+
 // Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
 // rows of one slot.
 
@@ -609,8 +868,7 @@ hipError_t launch_gateup_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
   const int rows_wg = 4 * (64 / LPR) * kGateUpSteps;
   dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
-  gateup_kernel<LPR, TM, kGateUpSteps, kGateUpBuf><<<grid, 256, lds, s>>>(a);
-  return hipGetLastError();
+  return launch_lds(gateup_kernel<LPR, TM, kGateUpSteps, kGateUpBuf>, grid, lds, s, a);
 }
 
 template <int LPR, int TM>
@@ -620,8 +878,7 @@ hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
   const int rows_wg = 4 * (64 / LPR) * kDownSteps;
   dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);
-  down_kernel<LPR, TM, kDownSteps, kDownBuf><<<grid, 256, lds, s>>>(a);
-  return hipGetLastError();
+  return launch_lds(down_kernel<LPR, TM, kDownSteps, kDownBuf>, grid, lds, s, a);
 }
 
 template <int TM>
@@ -643,18 +900,22 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
+  hipError_t e;
   if (a.n == 1) {
     const int U = a.H / kUnit;
     const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
     dim3 grid((a.I + 15) / 16, a.S + a.max_active);
     gateup1_kernel<<<grid, 256, lds, s>>>(a);
-    return hipGetLastError();
+    e = hipGetLastError();
+  } else {
+    e = launch_gateup_tm<4>(a, s);
   }
-  return launch_gateup_tm<4>(a, s);
+  return e == hipSuccess ? launch_wide_gateup(a, s) : e;
 }
 
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {
-  return a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
+  const hipError_t e = a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
+  return e == hipSuccess ? launch_wide_down(a, s) : e;
 }
 
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s) {

@@ -112,6 +112,9 @@ struct DecodeArgs {
   int32_t max_mtiles;
   const uint16_t* x16;
   uint16_t* h16;
+  // slots with a 5/6/8-bit gate or up (down) tensor: 0 none, 1 shared
+  // experts only, 2 routed experts too
+  int32_t wide_gateup, wide_down;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);

@@ -131,6 +131,55 @@ __device__ __forceinline__ void block_pairs<3>(const uint32_t* w, const PairCons
   p[15] = and_or(shl<-9>(w[2]), k.b32, t);
 }
 
+// 5-bit blocks: dword d (0..4) holds pairs 3d + f (f = 0..2), the even code
+// of a pair at bits [5f, 5f+5) of the low half, the odd one in the high half;
+// pair 15 (codes 30, 31) is spread over bit 15 (code 30) and bit 31 (code 31)
+// of the five dwords, bit q of each code in dword q.
+template <>
+__device__ __forceinline__ void block_pairs<5>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  uint32_t m5, b0, b1;
+  asm("v_mov_b32 %0, 0x007C007C" : "=v"(m5));  // bits [2,7) of each half
+  asm("v_mov_b32 %0, 0x00040004" : "=v"(b0));
+  asm("v_mov_b32 %0, 0x00080008" : "=v"(b1));
+#pragma unroll
+  for (int d = 0; d < 5; ++d) {
+    p[3 * d + 0] = and_or(shl<2>(w[d]), m5, k.base);
+    p[3 * d + 1] = and_or(shl<-3>(w[d]), m5, k.base);
+    p[3 * d + 2] = and_or(shl<-8>(w[d]), m5, k.base);
+  }
+  // bit q of the spare bits goes to mantissa bit 2 + q of each half
+  uint32_t t = and_or(shl<-13>(w[0]), b0, k.base);
+  t = and_or(shl<-12>(w[1]), b1, t);
+  t = and_or(shl<-11>(w[2]), k.b30, t);
+  t = and_or(shl<-10>(w[3]), k.b31, t);
+  p[15] = and_or(shl<-9>(w[4]), k.b32, t);
+}
+
+// 6-bit blocks: dword d (0..5) holds pairs 2d + f (f = 0, 1) at bits
+// [6f, 6f+6) of each half; pairs 12 + m (m = 0..3) keep their codes' low
+// four bits in bits [12,16) of each half of dword m and their top two bits in
+// bits [12 + 2(m&1), 14 + 2(m&1)) of each half of dword 4 + m/2.
+template <>
+__device__ __forceinline__ void block_pairs<6>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  uint32_t m6, lo4;
+  asm("v_mov_b32 %0, 0x007E007E" : "=v"(m6));   // bits [1,7) of each half
+  asm("v_mov_b32 %0, 0x001E001E" : "=v"(lo4));  // bits [1,5)
+#pragma unroll
+  for (int d = 0; d < 6; ++d) {
+    p[2 * d + 0] = and_or(shl<1>(w[d]), m6, k.base);
+    p[2 * d + 1] = and_or(shl<-5>(w[d]), m6, k.base);
+  }
+  // top two bits to mantissa bits [5,7) (mask m2)
+  p[12] = and_or(shl<-7>(w[4]), k.m2, and_or(shl<-11>(w[0]), lo4, k.base));
+  p[13] = and_or(shl<-9>(w[4]), k.m2, and_or(shl<-11>(w[1]), lo4, k.base));
+  p[14] = and_or(shl<-7>(w[5]), k.m2, and_or(shl<-11>(w[2]), lo4, k.base));
+  p[15] = and_or(shl<-9>(w[5]), k.m2, and_or(shl<-11>(w[3]), lo4, k.base));
+}
+
+// 8-bit blocks are two 4-bit planes: dwords 0..3 encode the codes' low
+// nibbles and dwords 4..7 their high nibbles, each plane exactly as a 4-bit
+// block.  The 8-bit value d (c - 128) = 16 d (hi - 8) + d (lo - 8) + 8 d.
+
 // Load unit u of a row (4*B dwords) with B coalesced 16-byte loads.
 //   row: the row's first dword; U: units per row.
 template <int B>

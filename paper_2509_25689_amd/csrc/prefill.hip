@@ -224,21 +224,79 @@ __device__ __forceinline__ RawBlk load_blk(const MOEQ_GLOBAL u32x4* rc, const MO
 template <int B>
 __device__ __forceinline__ void decode_blk(const RawBlk& r, int o, bool o_half_shift, _Float16* dst) {
   const uint32_t all[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
-  uint32_t w[4];
+  // a block starts at dword o = (q * B) % 4 of its first chunk: o + B <= 8
+  // for every width here (B = 6 has o in {0, 2}, B = 8 has o = 0)
+  uint32_t w[B];
 #pragma unroll
-  for (int i = 0; i < B; ++i)
-    w[i] = o == 0 ? all[i] : o == 1 ? all[i + 1] : o == 2 ? all[i + 2] : all[i + 3];
+  for (int i = 0; i < B; ++i) {
+    if constexpr (B == 8)
+      w[i] = all[i];
+    else if constexpr (B == 6)
+      w[i] = o == 0 ? all[i] : all[i + 2];
+    else
+      w[i] = o == 0 ? all[i] : o == 1 ? all[i + 1] : o == 2 ? all[i + 2] : all[i + 3];
+  }
   uint32_t mask, base;
   asm("v_mov_b32 %0, 0x64006400" : "=v"(base));
-  if constexpr (B == 4) asm("v_mov_b32 %0, 0x000F000F" : "=v"(mask));
+  if constexpr (B == 4 || B == 8) asm("v_mov_b32 %0, 0x000F000F" : "=v"(mask));
   if constexpr (B == 3) asm("v_mov_b32 %0, 0x00070007" : "=v"(mask));
   if constexpr (B == 2) asm("v_mov_b32 %0, 0x00030003" : "=v"(mask));
+  if constexpr (B == 5) asm("v_mov_b32 %0, 0x001F001F" : "=v"(mask));
+  if constexpr (B == 6) asm("v_mov_b32 %0, 0x003F003F" : "=v"(mask));
   const _Float16 zf = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
   const half2_t zb = {zf, zf};
   const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)(o_half_shift ? r.sc >> 16 : r.sc));
   const half2_t d2 = {d, d};
   uint32_t p[16];
-  if constexpr (B == 4) {
+  if constexpr (B == 8) {
+    // low nibbles in dwords 0..3 and high nibbles in 4..7, each a 4-bit
+    // block: 1024 + c is the low nibble under the base with the high
+    // nibble placed at bits [4, 8)
+    uint32_t hm;
+    asm("v_mov_b32 %0, 0x00F000F0" : "=v"(hm));
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int f = 0; f < 4; ++f) {
+        const uint32_t hs = f == 0 ? w[4 + q] << 4 : w[4 + q] >> (4 * f - 4);
+        const uint32_t t = and_or(hs, hm, and_or(w[q] >> (4 * f), mask, base));
+        const half2_t c = __builtin_bit_cast(half2_t, t) + zb;
+        p[4 * q + f] = __builtin_bit_cast(uint32_t, c * d2);
+      }
+  } else if constexpr (B == 6) {
+#pragma unroll
+    for (int q = 0; q < 6; ++q)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) p[2 * q + f] = dq_pair<0>(w[q] >> (6 * f), mask, base, zb, d2);
+    uint32_t lo4, hi2;
+    asm("v_mov_b32 %0, 0x000F000F" : "=v"(lo4));
+    asm("v_mov_b32 %0, 0x00300030" : "=v"(hi2));
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const uint32_t t = and_or(w[4 + m / 2] >> (8 + 2 * (m & 1)), hi2, and_or(w[m] >> 12, lo4, base));
+      const half2_t c = __builtin_bit_cast(half2_t, t) + zb;
+      p[12 + m] = __builtin_bit_cast(uint32_t, c * d2);
+    }
+  } else if constexpr (B == 5) {
+#pragma unroll
+    for (int q = 0; q < 5; ++q)
+#pragma unroll
+      for (int f = 0; f < 3; ++f) p[3 * q + f] = dq_pair<0>(w[q] >> (5 * f), mask, base, zb, d2);
+    // bit q of codes 30 and 31 sits at bit 15 (31) of dword q
+    uint32_t m0, m1, m2, m3, m4;
+    asm("v_mov_b32 %0, 0x00010001" : "=v"(m0));
+    asm("v_mov_b32 %0, 0x00020002" : "=v"(m1));
+    asm("v_mov_b32 %0, 0x00040004" : "=v"(m2));
+    asm("v_mov_b32 %0, 0x00080008" : "=v"(m3));
+    asm("v_mov_b32 %0, 0x00100010" : "=v"(m4));
+    uint32_t t = and_or(w[0] >> 15, m0, base);
+    t = and_or(w[1] >> 14, m1, t);
+    t = and_or(w[2] >> 13, m2, t);
+    t = and_or(w[3] >> 12, m3, t);
+    t = and_or(w[4] >> 11, m4, t);
+    const half2_t c = __builtin_bit_cast(half2_t, t) + zb;
+    p[15] = __builtin_bit_cast(uint32_t, c * d2);
+  } else if constexpr (B == 4) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -352,6 +410,7 @@ __device__ __forceinline__ void gemm_loop8(const MOEQ_GLOBAL u32x4* rc, const MO
 #undef STEP8
 }
 
+template <bool WIDE>
 __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
                                   const TensorDev tu, _Float16* lds) {
   _Float16* As = lds;                            // [2][BM][LDS_STRIDE]
@@ -391,8 +450,16 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
     if (blk) GU8(2, 1); else GU8(2, 0);
   } else if (bits == 3) {
     if (blk) GU8(3, 1); else GU8(3, 0);
-  } else {
+  } else if (!WIDE || bits == 4) {
     if (blk) GU8(4, 1); else GU8(4, 0);
+  } else if constexpr (WIDE) {
+    if (bits == 5) {
+      if (blk) GU8(5, 1); else GU8(5, 0);
+    } else if (bits == 6) {
+      if (blk) GU8(6, 1); else GU8(6, 0);
+    } else {
+      if (blk) GU8(8, 1); else GU8(8, 0);
+    }
   }
 #undef GU8
 
@@ -424,6 +491,9 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
   }
 }
 
+// WIDE = false takes the tiles whose gate and up tensors are 2-4 bits wide,
+// WIDE = true those with a 5, 6 or 8-bit gate or up tensor
+template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.I / BN;
@@ -434,10 +504,11 @@ __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   const int m0 = a.tiles[2 + 2 * mt];
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
-  if (tg.bits < 2 || tg.bits > 4 || tu.bits < 2 || tu.bits > 4) return;
-  gateup_gemm_body8(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
+  if ((tg.bits > 4 || tu.bits > 4) != WIDE) return;
+  gateup_gemm_body8<WIDE>(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
 }
 
+template <bool WIDE>
 __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev td,
                                 _Float16* lds) {
   _Float16* As = lds;                        // [2][BM][LDS_STRIDE]
@@ -472,12 +543,22 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
 #define DN8(B, BL) gemm_loop8<1, B, BL, true, 0>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc)
   if (!wrole) {
     gemm_loop8<1, 4, 0, false, 4>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  } else if (bits == 2) {
-    if (blk) DN8(2, 1); else DN8(2, 0);
-  } else if (bits == 3) {
-    if (blk) DN8(3, 1); else DN8(3, 0);
+  } else if constexpr (!WIDE) {
+    if (bits == 2) {
+      if (blk) DN8(2, 1); else DN8(2, 0);
+    } else if (bits == 3) {
+      if (blk) DN8(3, 1); else DN8(3, 0);
+    } else {
+      if (blk) DN8(4, 1); else DN8(4, 0);
+    }
   } else {
-    if (blk) DN8(4, 1); else DN8(4, 0);
+    if (bits == 5) {
+      if (blk) DN8(5, 1); else DN8(5, 0);
+    } else if (bits == 6) {
+      if (blk) DN8(6, 1); else DN8(6, 0);
+    } else {
+      if (blk) DN8(8, 1); else DN8(8, 0);
+    }
   }
 #undef DN8
 
@@ -509,6 +590,9 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
   }
 }
 
+// WIDE = false takes the tiles whose down tensor is 2-4 bits wide, WIDE = true
+// the 5, 6 and 8-bit ones
+template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.H / BN;
@@ -519,8 +603,8 @@ __global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
   const int m0 = a.tiles[2 + 2 * mt];
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
-  if (td.bits < 2 || td.bits > 4) return;
-  down_gemm_body8(gemm_args(a), sl, m0, nt * BN, td, lds_h);
+  if ((td.bits > 4) != WIDE) return;
+  down_gemm_body8<WIDE>(gemm_args(a), sl, m0, nt * BN, td, lds_h);
 }
 
 }  // namespace
@@ -531,38 +615,45 @@ int prefill_max_mtiles(int n, int k, int S, int n_kept) {
   return (int)(routed + (long long)S * ((n + BM - 1) / BM));
 }
 
+namespace {
+
+// sets the LDS limit of a GEMM kernel once per process, then launches it
+template <typename K>
+hipError_t launch_gemm(K kernel, bool& attr, int grid, size_t lds, hipStream_t s, const DecodeArgs& a) {
+  if (!attr) {
+    const hipError_t e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  kernel<<<grid, 512, lds, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
   prefill_tiles_kernel<<<1, 1024, 0, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
-  static bool attr = false;
-  if (!attr) {
-    e = hipFuncSetAttribute((const void*)gateup_gemm8_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
   const int grid = a.max_mtiles * (a.I / BN);
-  gateup_gemm8_kernel<<<grid, 512, lds, s>>>(a);
-  return hipGetLastError();
+  static bool attr_n = false, attr_w = false;
+  e = launch_gemm(gateup_gemm8_kernel<false>, attr_n, grid, lds, s, a);
+  if (e == hipSuccess && a.wide_gateup) e = launch_gemm(gateup_gemm8_kernel<true>, attr_w, grid, lds, s, a);
+  return e;
 }
 
 hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) {
   const int rows = a.n * (a.k + a.S);
   h16_kernel<<<(rows + 3) / 4, 256, 0, s>>>(a.h, a.rowmax, rows, a.I, a.h16);
-  hipError_t e0 = hipGetLastError();
-  if (e0 != hipSuccess) return e0;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)down_gemm8_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)lds);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
   const int grid = a.max_mtiles * (a.H / BN);
-  down_gemm8_kernel<<<grid, 512, lds, s>>>(a);
-  return hipGetLastError();
+  static bool attr_n = false, attr_w = false;
+  e = launch_gemm(down_gemm8_kernel<false>, attr_n, grid, lds, s, a);
+  if (e == hipSuccess && a.wide_down) e = launch_gemm(down_gemm8_kernel<true>, attr_w, grid, lds, s, a);
+  return e;
 }
 
 }  // namespace moeq

@@ -17,7 +17,31 @@ namespace {
 template <int B>
 __device__ void encode_block(const uint8_t* c, uint32_t* w) {
   for (int d = 0; d < B; ++d) w[d] = 0u;
-  if constexpr (B == 4) {
+  if constexpr (B == 8) {
+    uint8_t lo[32], hi[32];
+    for (int i = 0; i < 32; ++i) {
+      lo[i] = c[i] & 15;
+      hi[i] = c[i] >> 4;
+    }
+    encode_block<4>(lo, w);
+    encode_block<4>(hi, w + 4);
+  } else if constexpr (B == 6) {
+    for (int d = 0; d < 6; ++d)
+      for (int f = 0; f < 2; ++f)
+        w[d] |= (uint32_t)c[4 * d + 2 * f] << (6 * f) | (uint32_t)c[4 * d + 2 * f + 1] << (16 + 6 * f);
+    for (int m = 0; m < 4; ++m) {
+      const uint32_t c0 = c[24 + 2 * m], c1 = c[25 + 2 * m];
+      w[m] |= (c0 & 15u) << 12 | (c1 & 15u) << 28;
+      const int sh = 12 + 2 * (m & 1);
+      w[4 + m / 2] |= (c0 >> 4) << sh | (c1 >> 4) << (16 + sh);
+    }
+  } else if constexpr (B == 5) {
+    for (int d = 0; d < 5; ++d)
+      for (int f = 0; f < 3; ++f)
+        w[d] |= (uint32_t)c[6 * d + 2 * f] << (5 * f) | (uint32_t)c[6 * d + 2 * f + 1] << (16 + 5 * f);
+    for (int q = 0; q < 5; ++q)
+      w[q] |= ((uint32_t)(c[30] >> q) & 1u) << 15 | ((uint32_t)(c[31] >> q) & 1u) << 31;
+  } else if constexpr (B == 4) {
     for (int d = 0; d < 4; ++d)
       for (int s = 0; s < 4; ++s)
         w[d] |= (uint32_t)c[8 * d + 2 * s] << (4 * s) | (uint32_t)c[8 * d + 2 * s + 1] << (16 + 4 * s);
@@ -69,17 +93,29 @@ __global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {
   uint32_t w[4 * B];
   load_unit<B>(t.codes + (size_t)r * B * U * 4, U, u, w);
   const uint16_t* sc = t.scales + (size_t)r * (t.K / kBlock) + 4 * u;
-  const float z = (float)(1 << (B - 1)), unit = (float)(1 << (7 - B));
+  const float z = (float)(1 << (B - 1)), unit = (float)(1 << (B <= 7 ? 7 - B : 0));
   float* o = out + (size_t)r * t.K + kUnit * u;
   const PairConsts pk = pair_consts();
   for (int q = 0; q < 4; ++q) {
-    uint32_t p[16];
-    block_pairs<B>(w + q * B, pk, p);
     const float d = half_to_float(sc[q]);
-    for (int P = 0; P < 16; ++P) {
-      const float c0 = (bf16_lo(p[P]) - 128.0f) / unit, c1 = (bf16_hi(p[P]) - 128.0f) / unit;
-      o[32 * q + 2 * P] = d * (c0 - z);
-      o[32 * q + 2 * P + 1] = d * (c1 - z);
+    if constexpr (B == 8) {
+      uint32_t pl[16], ph[16];
+      block_pairs<4>(w + 8 * q, pk, pl);
+      block_pairs<4>(w + 8 * q + 4, pk, ph);
+      for (int P = 0; P < 16; ++P) {
+        const float c0 = (bf16_lo(ph[P]) - 128.0f) * 2.0f + (bf16_lo(pl[P]) - 128.0f) / 8.0f;
+        const float c1 = (bf16_hi(ph[P]) - 128.0f) * 2.0f + (bf16_hi(pl[P]) - 128.0f) / 8.0f;
+        o[32 * q + 2 * P] = d * (c0 - z);
+        o[32 * q + 2 * P + 1] = d * (c1 - z);
+      }
+    } else {
+      uint32_t p[16];
+      block_pairs<B>(w + q * B, pk, p);
+      for (int P = 0; P < 16; ++P) {
+        const float c0 = (bf16_lo(p[P]) - 128.0f) / unit, c1 = (bf16_hi(p[P]) - 128.0f) / unit;
+        o[32 * q + 2 * P] = d * (c0 - z);
+        o[32 * q + 2 * P + 1] = d * (c1 - z);
+      }
     }
   }
 }
@@ -139,6 +175,9 @@ hipError_t launch_repack(const uint8_t* canon, int rows, int K, int bits, uint32
     case 2: repack_kernel<2><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
     case 3: repack_kernel<3><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
     case 4: repack_kernel<4><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    case 5: repack_kernel<5><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    case 6: repack_kernel<6><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    case 8: repack_kernel<8><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -151,6 +190,9 @@ hipError_t launch_dequant(const TensorDev& t, float* out, hipStream_t s) {
     case 2: dequant_kernel<2><<<grid, 256, 0, s>>>(t, out); break;
     case 3: dequant_kernel<3><<<grid, 256, 0, s>>>(t, out); break;
     case 4: dequant_kernel<4><<<grid, 256, 0, s>>>(t, out); break;
+    case 5: dequant_kernel<5><<<grid, 256, 0, s>>>(t, out); break;
+    case 6: dequant_kernel<6><<<grid, 256, 0, s>>>(t, out); break;
+    case 8: dequant_kernel<8><<<grid, 256, 0, s>>>(t, out); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -75,12 +75,18 @@ def test_config_validation(field, value, status):
     assert moeq.moeq_last_error()
 
 
-@pytest.mark.parametrize("bits,status", [(1, moeq.MOEQ_ERR_INVALID_ARG), (5, moeq.MOEQ_ERR_UNSUPPORTED),
-                                         (6, moeq.MOEQ_ERR_UNSUPPORTED), (8, moeq.MOEQ_ERR_UNSUPPORTED),
-                                         (9, moeq.MOEQ_ERR_INVALID_ARG)])
-def test_bit_width_validation(bits, status):
+@pytest.mark.parametrize("bits", [0, 1, 7, 9, 16])
+def test_bit_width_validation(bits):
     st, _ = _create(_cfg(), bits=bits)
-    assert st == status
+    assert st == moeq.MOEQ_ERR_INVALID_ARG
+    assert moeq.lib.moeq_quantize(1, 1, 32, bits, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 5, 6, 8])
+def test_every_supported_width_passes_validation(bits):
+    """Validation accepts the width; without a device the call then stops at the device step."""
+    st, _ = _create(_cfg(), bits=bits)
+    assert st not in (moeq.MOEQ_ERR_INVALID_ARG, moeq.MOEQ_ERR_UNSUPPORTED), moeq.moeq_last_error()
 
 
 def test_null_pointers():
@@ -161,7 +167,7 @@ def test_quantize_validation():
     assert L.moeq_quantize(None, 1, 32, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_quantize(1, 1, 33, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_quantize(1, -1, 32, 4, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
-    assert L.moeq_quantize(1, 1, 32, 8, 1, 1, None) == moeq.MOEQ_ERR_UNSUPPORTED
+    assert L.moeq_quantize(1, 1, 32, 7, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_quantize(1, 1, 32, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_quantize(1, 0, 32, 4, 1, 1, None) == moeq.MOEQ_OK   # empty: nothing to do
 
