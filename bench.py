@@ -41,10 +41,10 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 # the kernel sources the counters were taken on, identified by their sha256:
 # any change to them reports traffic as null until the counters are retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 119717754,
+    "bytes": 127364395,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "4b5bda7843426ad6eab188fd34198b80d212e794d69eb78b84e0ff805338904c",
-        "paper_2509_25689_amd/csrc/layout.h": "0ffefc9dd183ff9cda73bcc28611268423cc9fb3b52cad4fdd0ff92acd1f3919",
+        "paper_2509_25689_amd/csrc/decode.hip": "0d4b7c3716d265cc63ac8d06ec4af0de20f8700b31ce82de2addd1c2960e7d47",
+        "paper_2509_25689_amd/csrc/layout.h": "60e009a556d1f9a60b3c0e727bd3d2b64bc5a2426b4bfaa43f5eb982ccdfcea7",
     },
 }
 
@@ -76,6 +76,10 @@ def parse():
     p.add_argument("--b16-steps", type=int, default=2560, help="16-token decode steps timed (0 = skip)")
     p.add_argument("--k6-steps", type=int, default=2560,
                    help="batch-1 decode steps timed with 6 experts per token (0 = skip)")
+    p.add_argument("--gate-steps", type=int, default=2560,
+                   help="batch-1 decode steps timed with logits from the router gate (0 = skip)")
+    p.add_argument("--wide-steps", type=int, default=2560,
+                   help="batch-1 decode steps timed with a 6-bit shared expert (0 = skip)")
     p.add_argument("--mode", choices=("all", "decode", "prefill", "copy", "stack", "sweep"), default="all",
                    help="all: batch-1 decode line with 16-token, prefill and CPU legs; decode / prefill: "
                         "one leg only (for profiling); copy: a plain 1 GiB device copy whose HBM counters "
@@ -311,10 +315,12 @@ def step_bytes_of(np, shape, layer, bits_r, bits_s, logits):
 
 
 def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, kernel_steps, key,
-               zipf=False, path=None):
+               zipf=False, path=None, gate=False):
     """Batch-B decode over the given layers (step s uses layer s % NL and
     input set s), replayed from one HIP graph with inputs resident in HBM.
-    Returns timing, bytes and per-stage kernel durations."""
+    With gate, each layer holds a float32 router weight and computes its own
+    logits (moeq_forward with NULL logits).  Returns timing, bytes and
+    per-stage kernel durations."""
     NL = len(layers)
     n_sets = R * NL
     if path is not None:
@@ -327,6 +333,10 @@ def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, 
         mask = layers[i % NL][1]
         lg = synth.zipf_logits(B, mask, key, "l", i) if zipf else synth.normal_logits(B, shape.n_experts, key, "l", i)
         lgs.append(torch.from_numpy(lg).cuda())
+    if gate:
+        for li, (L, *_) in enumerate(layers):
+            L.set_router_weight(synth.router_weight(shape.n_experts, shape.hidden, key, "wr", li))
+        lgs = [layers[i % NL][0].router_logits(xs[i]) for i in range(n_sets)]
     ys = [torch.empty((B, shape.hidden), device="cuda") for _ in range(NL)]
     gu_bytes, down_bytes, n_exp = [], [], []
     for i in range(n_sets):
@@ -336,10 +346,13 @@ def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, 
         down_bytes.append(d)
         n_exp.append(ne)
     io_bytes = B * (shape.hidden * 2 + shape.n_experts * 4 + shape.hidden * 4)
+    if gate:
+        io_bytes += shape.n_experts * shape.hidden * 4
 
     def run_step(i, stream):
         layer = layers[i % NL][0]
-        moeq.moeq_forward(layer.handle, xs[i].data_ptr(), lgs[i].data_ptr(), B, ys[i % NL].data_ptr(), stream)
+        moeq.moeq_forward(layer.handle, xs[i].data_ptr(), 0 if gate else lgs[i].data_ptr(), B,
+                          ys[i % NL].data_ptr(), stream)
 
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -390,6 +403,9 @@ def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, 
     if path is not None:
         for L, *_ in layers:
             L.set_path(moeq.MOEQ_PATH_AUTO)
+    if gate:
+        for L, *_ in layers:
+            L.set_router_weight(None)
     stage_mean = stage_ms.mean(axis=0)
     mean_step_bytes = float(np.mean(gu_bytes) + np.mean(down_bytes) + io_bytes)
     gu_launch = float(np.mean(gu_bytes[:KT]))
@@ -514,11 +530,20 @@ def main():
         "stage_us": {"route_bucket": round(st[0] * 1e3, 2), "gate_up": round(st[1] * 1e3, 2),
                      "down": round(st[2] * 1e3, 2), "combine": round(st[3] * 1e3, 2)},
         "down_GBps": round(r["dn_GBps"], 1),
-        "roofline": {"bound": "hbm", "kernel": "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)",
+        "roofline": {"bound": "hbm",
+                     "kernel": ("gateup1_kernel" if B == 1 else "gateup_kernel") + " (fused dequant-GEMV gate/up + SwiGLU)",
                      "achieved": round(r["gu_GBps"], 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": gateup_traffic() if B == 1 else None,
                      "bytes_per_launch": int(r["gu_launch_bytes"])},
     }
+    if args.mode == "all" and args.gate_steps > 0:
+        # the same layers, logits computed in the forward by the router gate x W_r^T
+        rg = decode_leg(torch, np, moeq, synth, hip, shape, layers, 1, R, args.gate_steps, 64, 64, "bench-gate",
+                        gate=True)
+        out["decode_b1_with_gate"] = {"tokens_per_s": round(rg["tokens_per_s"], 1),
+                                      "us_per_step": round(rg["ms_per_step"] * 1e3, 2),
+                                      "route_stage_us": round(rg["stage_ms"][0] * 1e3, 2),
+                                      "bytes_per_step": int(rg["bytes_per_step"]), "GBps": round(rg["GBps"], 1)}
     if args.mode == "all" and args.b16_steps > 0:
         r16 = decode_leg(torch, np, moeq, synth, hip, shape, layers, 16, 16, args.b16_steps, 64, 64, "bench-b16")
         out["decode_b16"] = {"tokens_per_s": round(r16["tokens_per_s"], 1),
@@ -540,6 +565,21 @@ def main():
                                "bytes_per_step": int(r6["bytes_per_step"]), "GBps": round(r6["GBps"], 1),
                                "hbm_frac": round(r6["GBps"] / HBM_PEAK_GBPS, 4)}
         for L, *_ in layers6:
+            L.close()
+    if args.mode == "all" and args.wide_steps > 0:
+        # Section 3.3's Q6 upgrade of a medium tensor: the shared expert at 6 bits
+        layers_w = [random_layer(torch, moeq, synth, shape, "gu3_d4_sh6", f"bench-sh6-{li}", max_tokens=1)
+                    for li in range(NL)]
+        rw = decode_leg(torch, np, moeq, synth, hip, shape, layers_w, 1, R, args.wide_steps, 64, 64, "bench-sh6")
+        st = rw["stage_ms"]
+        out["decode_b1_shared_6bit"] = {"tokens_per_s": round(rw["tokens_per_s"], 1),
+                                        "us_per_step": round(rw["ms_per_step"] * 1e3, 2),
+                                        "stage_us": {"route_bucket": round(st[0] * 1e3, 2),
+                                                     "gate_up": round(st[1] * 1e3, 2),
+                                                     "down": round(st[2] * 1e3, 2), "combine": round(st[3] * 1e3, 2)},
+                                        "bytes_per_step": int(rw["bytes_per_step"]), "GBps": round(rw["GBps"], 1),
+                                        "hbm_frac": round(rw["GBps"] / HBM_PEAK_GBPS, 4)}
+        for L, *_ in layers_w:
             L.close()
     if args.mode == "all" and args.prefill_steps > 0:
         out["prefill"] = prefill_bench(torch, np, moeq, synth, hip, args.prefill_steps)
