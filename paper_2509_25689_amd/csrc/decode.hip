@@ -513,13 +513,14 @@ __device__ __forceinline__ float half_sum8(float v) {
 #endif
 template <int B>
 __device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U, int j, int H, const uint32_t* xl,
-                                              const float* xs) {
+                                              const float* xs, const UnitBuf<B>& first) {
   constexpr int NB = MOEQ_GU1_DEPTH;
   const int UPL = (U + 7) / 8;
   UnitBuf<B> buf[NB];
-  float acc = 0.0f;
+  buf[0] = first;
 #pragma unroll
-  for (int i = 0; i < NB - 1; ++i) load_unit_buf<B>(buf[i], t, row, U, min(j + 8 * min(i, UPL - 1), U - 1), H);
+  for (int i = 1; i < NB - 1; ++i) load_unit_buf<B>(buf[i], t, row, U, min(j + 8 * min(i, UPL - 1), U - 1), H);
+  float acc = 0.0f;
 #pragma unroll 1
   for (int i0 = 0; i0 < UPL; i0 += NB) {
     asm volatile("" ::: "memory");
@@ -537,40 +538,9 @@ __device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U
   return acc;
 }
 
-template <int BG, int BU>
-__device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
-                                             const TensorDev& tu, const uint32_t* xl, const float* xs) {
-  const int H = a.H, I = a.I, U = H / kUnit;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 16 + wave * 4 + (lane >> 4);
-  const bool up = (lane & 8) != 0;
-  const int j = lane & 7;
-  const int rowc = min(row, I - 1);
-  float v;
-  if constexpr (BG == BU) {
-    v = row_half_dot<BG>(up ? tu : tg, rowc, U, j, H, xl, xs);
-  } else {
-    if (up)
-      v = row_half_dot<BU>(tu, rowc, U, j, H, xl, xs);
-    else
-      v = row_half_dot<BG>(tg, rowc, U, j, H, xl, xs);
-  }
-  v = half_sum8(v);
-  const float other = dpp_f<0x128>(v);  // row_ror:8: the other half's total
-  if ((lane & 15) == 15 && row < I) a.h[(size_t)sl.base * a.I + row] = silu(other) * v;
-}
-
-// grid = (I / 16, S + max_active), 256 threads; n = 1
-__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
-  extern __shared__ uint32_t smem[];
-  const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
-  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
-  if (!tg.codes || !tu.codes) return;
-  const int H = a.H, U = H / kUnit;
-  uint32_t* xl = smem;
-  float* xs = reinterpret_cast<float*>(smem + U * kXStride);
-  // stage the token's x with per-block sums (16-byte pieces, 4 per block)
+// the token's x with per-block sums (16-byte pieces, 4 per block) into LDS
+__device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uint32_t* xl, float* xs) {
+  const int H = a.H;
   const int t = sl.shared >= 0 ? 0 : a.perm[sl.base] / a.k;
   const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
   for (int q = threadIdx.x; q < H / 8; q += 256) {
@@ -584,7 +554,56 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
     *reinterpret_cast<u32x4*>(xl + uu * kXStride + cq * 4) = v;
     if ((cq & 3) == 0) xs[uu * 4 + (cq >> 2)] = s;
   }
-  __syncthreads();
+}
+
+// Each lane requests its first unit before x is staged, so the staging
+// latency overlaps the weight traffic.
+template <int BG, int BU>
+__device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
+                                             const TensorDev& tu, uint32_t* xl, float* xs) {
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 16 + wave * 4 + (lane >> 4);
+  const bool up = (lane & 8) != 0;
+  const int j = lane & 7;
+  const int rowc = min(row, I - 1);
+  float v;
+  if constexpr (BG == BU) {
+    const TensorDev& t = up ? tu : tg;
+    UnitBuf<BG> first;
+    load_unit_buf<BG>(first, t, rowc, U, min(j, U - 1), H);
+    stage_x1(a, sl, xl, xs);
+    __syncthreads();
+    v = row_half_dot<BG>(t, rowc, U, j, H, xl, xs, first);
+  } else {
+    UnitBuf<BG> fg;
+    UnitBuf<BU> fu;
+    if (up)
+      load_unit_buf<BU>(fu, tu, rowc, U, min(j, U - 1), H);
+    else
+      load_unit_buf<BG>(fg, tg, rowc, U, min(j, U - 1), H);
+    stage_x1(a, sl, xl, xs);
+    __syncthreads();
+    if (up)
+      v = row_half_dot<BU>(tu, rowc, U, j, H, xl, xs, fu);
+    else
+      v = row_half_dot<BG>(tg, rowc, U, j, H, xl, xs, fg);
+  }
+  v = half_sum8(v);
+  const float other = dpp_f<0x128>(v);  // row_ror:8: the other half's total
+  if ((lane & 15) == 15 && row < I) a.h[(size_t)sl.base * a.I + row] = silu(other) * v;
+}
+
+// grid = (I / 16, S + max_active), 256 threads; n = 1
+__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 0) return;
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  const int U = a.H / kUnit;
+  uint32_t* xl = smem;
+  float* xs = reinterpret_cast<float*>(smem + U * kXStride);
   switch (tg.bits * 8 + tu.bits) {
     case 2 * 8 + 2: gateup1_body<2, 2>(a, sl, tg, tu, xl, xs); break;
     case 2 * 8 + 3: gateup1_body<2, 3>(a, sl, tg, tu, xl, xs); break;
@@ -601,12 +620,12 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
 
 // ---------------------------------------------------------------------------
 // Wide tensors (5, 6 and 8 bits).  The kernels above skip a slot whose gate or
-// up (down) tensor is wide; these take exactly those slots.  Eight lanes per
-// row: lane j walks the units j, j + 8, ... of its row with the next unit in
-// flight, for up to TM tokens per pass.  Gate, up and down are reduced
-// one tensor at a time, so a wave decodes one width at a time.  TM: tokens per
-// pass (1 for a single token, else 4).
-
+// up (down) tensor is wide; these take exactly those slots.  LPR lanes per
+// row (8, 16 or 32): lane j walks the units j, j + LPR, ... of its row with the
+// next unit in flight, for up to TM tokens per pass (1 for a single token,
+// else 4).  Gate, up and down are reduced one tensor at a time, so a wave
+// decodes one width at a time.  Few slots (shared experts only) take more
+// lanes per row, so that the grid still covers the chip.
 __device__ __forceinline__ bool wide_bits(int b) { return b > 4; }
 
 template <int B>
@@ -667,7 +686,7 @@ extern __shared__ uint32_t wide_lds[];
 // This lane's share (units j, j + 8, ...) of row `row` against the staged
 // tokens.  Not inlined: one function per width keeps each width's registers
 // to itself (inlined together, the allocator merges all six).
-template <int B, int NX, int TM>
+template <int B, int NX, int TM, int LPR>
 __device__ __noinline__ WideAcc<TM> wide_row_dot(const TensorDev t, int row, int U, int K, int j, int xts, int lo,
                                                  int sts, int mc) {
   const uint32_t* xl = wide_lds;
@@ -675,7 +694,7 @@ __device__ __noinline__ WideAcc<TM> wide_row_dot(const TensorDev t, int row, int
   WideAcc<TM> r;
 #pragma unroll
   for (int m = 0; m < TM; ++m) r.v[m] = 0.0f;
-  const int UPL = (U + 7) / 8;
+  const int UPL = (U + LPR - 1) / LPR;
   WideUnit<B> buf[2];
   wide_load<B>(buf[0], t, row, U, min(j, U - 1), K);
 #pragma unroll 1
@@ -686,8 +705,8 @@ __device__ __noinline__ WideAcc<TM> wide_row_dot(const TensorDev t, int row, int
       const int i = i0 + b;
       if (i < UPL) {
         // the next unit (clamped to the last valid one) goes out before this one is reduced
-        wide_load<B>(buf[1 - b], t, row, U, min(j + 8 * min(i + 1, UPL - 1), U - 1), K);
-        const int u = j + 8 * i;
+        wide_load<B>(buf[1 - b], t, row, U, min(j + LPR * min(i + 1, UPL - 1), U - 1), K);
+        const int u = j + LPR * i;
         if (u < U) wide_unit_dot<B, NX, TM>(buf[b], xl + u * kXStride, xts, lo, xs + u * 4, sts, mc, r.v);
       }
     }
@@ -695,21 +714,30 @@ __device__ __noinline__ WideAcc<TM> wide_row_dot(const TensorDev t, int row, int
   return r;
 }
 
-template <int NX, int TM>
+template <int NX, int TM, int LPR>
 __device__ __forceinline__ WideAcc<TM> wide_row_dot_any(const TensorDev& t, int row, int U, int K, int j, int xts,
                                                         int lo, int sts, int mc) {
   switch (t.bits) {
-    case 2: return wide_row_dot<2, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
-    case 3: return wide_row_dot<3, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
-    case 4: return wide_row_dot<4, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
-    case 5: return wide_row_dot<5, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
-    case 6: return wide_row_dot<6, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
-    default: return wide_row_dot<8, NX, TM>(t, row, U, K, j, xts, lo, sts, mc);
+    case 2: return wide_row_dot<2, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
+    case 3: return wide_row_dot<3, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
+    case 4: return wide_row_dot<4, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
+    case 5: return wide_row_dot<5, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
+    case 6: return wide_row_dot<6, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
+    default: return wide_row_dot<8, NX, TM, LPR>(t, row, U, K, j, xts, lo, sts, mc);
   }
 }
 
-// grid = (ceil(I / 32), slots), 256 threads: 32 rows of one slot
-template <int TM>
+// sum over the LPR lanes of a row group; the group's last lane holds it
+template <int LPR>
+__device__ __forceinline__ float wide_sum(float v) {
+  if constexpr (LPR == 8)
+    return half_sum8(v);
+  else
+    return group_sum<LPR>(v);
+}
+
+// grid = (ceil(I / (4 * 64 / LPR)), slots), 256 threads
+template <int TM, int LPR>
 __global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
   const Slot sl = slot_info(a, blockIdx.y);
   if (sl.M < 0) return;
@@ -721,7 +749,8 @@ __global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
   uint32_t* xl = wide_lds;
   float* xs = reinterpret_cast<float*>(wide_lds + TM * xts);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 32 + wave * 8 + (lane >> 3), j = lane & 7;
+  constexpr int RPW = 64 / LPR;  // rows per wave
+  const int row = blockIdx.x * 4 * RPW + wave * RPW + lane / LPR, j = lane % LPR;
   const int rowc = min(row, I - 1);
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
     const int mc = min(TM, sl.M - m0);
@@ -742,20 +771,20 @@ __global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
       }
     }
     __syncthreads();
-    const WideAcc<TM> g = wide_row_dot_any<1, TM>(tg, rowc, U, H, j, xts, 0, sts, mc);
-    const WideAcc<TM> u = wide_row_dot_any<1, TM>(tu, rowc, U, H, j, xts, 0, sts, mc);
+    const WideAcc<TM> g = wide_row_dot_any<1, TM, LPR>(tg, rowc, U, H, j, xts, 0, sts, mc);
+    const WideAcc<TM> u = wide_row_dot_any<1, TM, LPR>(tu, rowc, U, H, j, xts, 0, sts, mc);
 #pragma unroll
     for (int m = 0; m < TM; ++m) {
       if (m < mc) {
-        const float gs = half_sum8(g.v[m]), us = half_sum8(u.v[m]);
-        if (j == 7 && row < I) a.h[(size_t)(sl.base + m0 + m) * I + row] = silu(gs) * us;
+        const float gs = wide_sum<LPR>(g.v[m]), us = wide_sum<LPR>(u.v[m]);
+        if (j == LPR - 1 && row < I) a.h[(size_t)(sl.base + m0 + m) * I + row] = silu(gs) * us;
       }
     }
   }
 }
 
-// grid = (ceil(H / 32), slots), 256 threads: 32 rows of one slot's down tensor
-template <int TM>
+// grid = (ceil(H / (4 * 64 / LPR)), slots), 256 threads
+template <int TM, int LPR>
 __global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
   const Slot sl = slot_info(a, blockIdx.y);
   if (sl.M < 0) return;
@@ -766,7 +795,8 @@ __global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
   uint32_t* xl = wide_lds;
   float* xs = reinterpret_cast<float*>(wide_lds + TM * xts);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 32 + wave * 8 + (lane >> 3), j = lane & 7;
+  constexpr int RPW = 64 / LPR;  // rows per wave
+  const int row = blockIdx.x * 4 * RPW + wave * RPW + lane / LPR, j = lane % LPR;
   const int rowc = min(row, H - 1);
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
     const int mc = min(TM, sl.M - m0);
@@ -799,12 +829,12 @@ __global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
       }
     }
     __syncthreads();
-    const WideAcc<TM> o = wide_row_dot_any<2, TM>(td, rowc, U, I, j, xts, lo, sts, mc);
+    const WideAcc<TM> o = wide_row_dot_any<2, TM, LPR>(td, rowc, U, I, j, xts, lo, sts, mc);
 #pragma unroll
     for (int m = 0; m < TM; ++m) {
       if (m < mc) {
-        const float os = half_sum8(o.v[m]);
-        if (j == 7 && row < H) {
+        const float os = wide_sum<LPR>(o.v[m]);
+        if (j == LPR - 1 && row < H) {
           int prow;
           float wv;
           if (sl.shared >= 0) {
@@ -832,30 +862,38 @@ hipError_t launch_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const Deco
   return hipGetLastError();
 }
 
-template <int TM>
+template <int TM, int LPR>
 hipError_t launch_wide_gateup_tm(const DecodeArgs& a, hipStream_t s) {
   const int U = a.H / kUnit;
   const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
-  dim3 grid((a.I + 31) / 32, a.wide_gateup == 1 ? a.S : a.S + a.max_active);
-  return launch_lds(wide_gateup_kernel<TM>, grid, lds, s, a);
+  const int rows_wg = 4 * (64 / LPR);
+  dim3 grid((a.I + rows_wg - 1) / rows_wg, a.wide_gateup == 1 ? a.S : a.S + a.max_active);
+  return launch_lds(wide_gateup_kernel<TM, LPR>, grid, lds, s, a);
 }
 
-template <int TM>
+template <int TM, int LPR>
 hipError_t launch_wide_down_tm(const DecodeArgs& a, hipStream_t s) {
   const int U = a.I / kUnit;
   const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
-  dim3 grid((a.H + 31) / 32, a.wide_down == 1 ? a.S : a.S + a.max_active);
-  return launch_lds(wide_down_kernel<TM>, grid, lds, s, a);
+  const int rows_wg = 4 * (64 / LPR);
+  dim3 grid((a.H + rows_wg - 1) / rows_wg, a.wide_down == 1 ? a.S : a.S + a.max_active);
+  return launch_lds(wide_down_kernel<TM, LPR>, grid, lds, s, a);
 }
 
+// shared experts only: more lanes per row (as many as the units allow, up
+// to 32 for gate/up and 16 for down) keep enough workgroups for a few slots
 hipError_t launch_wide_gateup(const DecodeArgs& a, hipStream_t s) {
   if (!a.wide_gateup) return hipSuccess;
-  return a.n == 1 ? launch_wide_gateup_tm<1>(a, s) : launch_wide_gateup_tm<4>(a, s);
+  const bool few = a.wide_gateup == 1 && a.H / kUnit >= 32;
+  if (a.n == 1) return few ? launch_wide_gateup_tm<1, 32>(a, s) : launch_wide_gateup_tm<1, 8>(a, s);
+  return few ? launch_wide_gateup_tm<4, 32>(a, s) : launch_wide_gateup_tm<4, 8>(a, s);
 }
 
 hipError_t launch_wide_down(const DecodeArgs& a, hipStream_t s) {
   if (!a.wide_down) return hipSuccess;
-  return a.n == 1 ? launch_wide_down_tm<1>(a, s) : launch_wide_down_tm<4>(a, s);
+  const bool few = a.wide_down == 1 && a.I / kUnit >= 16;
+  if (a.n == 1) return few ? launch_wide_down_tm<1, 16>(a, s) : launch_wide_down_tm<1, 8>(a, s);
+  return few ? launch_wide_down_tm<4, 16>(a, s) : launch_wide_down_tm<4, 8>(a, s);
 }
 
 // Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
