@@ -207,15 +207,22 @@ struct RawBlk {
   uint32_t sc;
 };
 
+// Block Q of unit u: its first chunk, and the next one only when the block
+// runs past the end of the first (Q and B are compile-time, so a block that
+// sits in one chunk issues one load).
+template <int B, int Q>
 __device__ __forceinline__ RawBlk load_blk(const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL uint16_t* rs, int U,
-                                           int bits, int u, int q) {
-  const int c0 = (q * bits) >> 2;
-  const int c1 = min(c0 + 1, bits - 1);
+                                           int u) {
+  constexpr int c0 = (Q * B) >> 2;
+  constexpr bool two = ((Q * B) & 3) + B > 4;
   RawBlk r;
   r.a = rc[(size_t)c0 * U + u];
-  r.b = rc[(size_t)c1 * U + u];
-  // the aligned pair of binary16 scales holding block q's (q even: low half)
-  r.sc = *reinterpret_cast<const MOEQ_GLOBAL uint32_t*>(rs + 4 * u + (q & 2));
+  if constexpr (two)
+    r.b = rc[(size_t)(c0 + 1) * U + u];
+  else
+    r.b = u32x4{0u, 0u, 0u, 0u};
+  // the aligned pair of binary16 scales holding block Q's (Q even: low half)
+  r.sc = *reinterpret_cast<const MOEQ_GLOBAL uint32_t*>(rs + 4 * u + (Q & 2));
   return r;
 }
 
@@ -378,7 +385,7 @@ __device__ __forceinline__ void gemm_loop8(const MOEQ_GLOBAL u32x4* rc, const MO
   u32x4 xv[2][NA > 0 ? NA : 1];
 #define L8(slot, st)                                                                        \
   do {                                                                                      \
-    if constexpr (DW) hw[slot] = load_blk(rc, rs, U, B, (st) >> 1, 2 * (slot) + BLK);       \
+    if constexpr (DW) hw[slot] = load_blk<B, 2 * (slot) + BLK>(rc, rs, U, (st) >> 1);        \
     _Pragma("unroll") for (int i_ = 0; i_ < NA; ++i_) xv[slot][i_] = arow[(st) * 8 + i_];   \
   } while (0)
 #define D8(slot)                                                                                         \
