@@ -619,6 +619,304 @@ __global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
   down_gemm_body8<WIDE>(gemm_args(a), sl, m0, nt * BN, td, lds_h);
 }
 
+// ---------------------------------------------------------------------------
+// Raw-staged grouped GEMM for 2-4 bit weights.
+//
+// In the kernels above every lane loads one 16-byte chunk of a different
+// weight row per K step: each load brings a whole cache line from L2 and
+// uses a quarter of it or less, and the line is gone before the same thread
+// needs its neighbour, so the L1 miss traffic, not the matrix cores, sets
+// the pace.  Here the decode waves load the packed codes (and scales) of 4
+// units (512 k, 8 K steps) of all 128 weight rows of the tile at once, 4
+// lanes per row and chunk plane (64 contiguous bytes), store them in LDS,
+// and each K step decodes its block from LDS into the binary16 tile.
+//
+// Used for gate/up (the down GEMM, with a quarter of the K steps per tile,
+// measured faster with the per-thread loads above).  The loop is written for
+// NT tensors of 128 / NT rows each.  Tile: 128 tokens x 128 weight rows (64
+// features of each projection, rows 0-63 gate and 64-127 up).  Waves
+// 0-3 load and decode (wave w: rows 64 (w % 2) .. +63, block half w / 2 of
+// each half unit, so every wave works on one tensor and one width), waves
+// 4-7 move activations (32 values of tile row (t - 256) / 2 per step).
+// The eight waves share the MFMAs: 2 x 4 waves of 64 tokens x 16 features
+// per projection.
+constexpr int RS_ROWS = 128;
+constexpr int RS_RAW = 4 * 16 + 4;   // dwords per staged row: 4 chunk planes x 4 units (+ padding)
+constexpr int RS_SCL = 10;           // dwords per staged row of scales: 16 binary16 (+ padding; even, so
+                                     // the 8-byte stores stay aligned)
+constexpr size_t RS_LDS = (size_t)2 * (BM + RS_ROWS) * LDS_STRIDE * 2 + (size_t)2 * RS_ROWS * RS_RAW * 4 +
+                          (size_t)2 * RS_ROWS * RS_SCL * 4;
+static_assert(RS_LDS <= 160 * 1024, "the raw-staged tile must fit the LDS of a compute unit");
+
+// one raw stage (4 units) of this lane: 2B chunk pieces and 2 scale pieces
+template <int B>
+struct RsStage {
+  u32x4 c[2 * B];
+  u32x2 s[2];
+};
+
+// Piece m of a wave's tensor (RPT rows, WPT waves per tensor, h = this wave's
+// index among them): row ((lane / 4) + 16 m) mod RPT, unit lane % 4, chunk
+// plane m / (RPT / 16); the wave takes m = WPT i + h.
+template <int B, int NT>
+__device__ __forceinline__ void rs_load(RsStage<B>& st, const TensorDev& t, int n0, int U, int K, int u0, int lane,
+                                        int h) {
+  constexpr int RPT = RS_ROWS / NT, WPT = 4 / NT;
+  const int uu = min(u0 + (lane & 3), U - 1);
+#pragma unroll
+  for (int i = 0; i < 2 * B; ++i) {
+    const int m = WPT * i + h;
+    const int r = ((lane >> 2) + 16 * m) % RPT, j = m / (RPT / 16);
+    const MOEQ_GLOBAL u32x4* rc = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)(n0 + r) * B * U * 4));
+    st.c[i] = rc[(size_t)j * U + uu];
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = WPT * i + h;
+    const int r = ((lane >> 2) + 16 * m) % RPT;
+    st.s[i] = *gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)(n0 + r) * (K / kBlock)) + uu);
+  }
+}
+
+template <int B, int NT>
+__device__ __forceinline__ void rs_store(const RsStage<B>& st, uint32_t* raw, uint32_t* scl, int tt, int lane, int h) {
+  constexpr int RPT = RS_ROWS / NT, WPT = 4 / NT;
+#pragma unroll
+  for (int i = 0; i < 2 * B; ++i) {
+    const int m = WPT * i + h;
+    const int r = ((lane >> 2) + 16 * m) % RPT, j = m / (RPT / 16);
+    *reinterpret_cast<u32x4*>(raw + (tt * RPT + r) * RS_RAW + j * 16 + (lane & 3) * 4) = st.c[i];
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = WPT * i + h;
+    const int r = ((lane >> 2) + 16 * m) % RPT;
+    *reinterpret_cast<u32x2*>(scl + (tt * RPT + r) * RS_SCL + (lane & 3) * 2) = st.s[i];
+  }
+}
+
+// Block Q of staged unit ul of LDS row `row` (the chunks it occupies and the
+// aligned pair of scales holding its own).
+template <int B, int Q>
+__device__ __forceinline__ RawBlk rs_block(const uint32_t* raw, const uint32_t* scl, int row, int ul) {
+  constexpr int c0 = (Q * B) >> 2;
+  constexpr bool two = ((Q * B) & 3) + B > 4;
+  RawBlk r;
+  const uint32_t* base = raw + row * RS_RAW + ul * 4;
+  r.a = *reinterpret_cast<const u32x4*>(base + c0 * 16);
+  if constexpr (two)
+    r.b = *reinterpret_cast<const u32x4*>(base + (c0 + 1) * 16);
+  else
+    r.b = u32x4{0u, 0u, 0u, 0u};
+  r.sc = scl[row * RS_SCL + ul * 2 + (Q >> 1)];
+  return r;
+}
+
+template <int NT, int C>
+__device__ __forceinline__ void read_frags_rs(const _Float16* A, const _Float16* W, int lane, int wm, int wn,
+                                              half8 (&fa)[2][4], half8 (&fb)[2][NT][C]) {
+  constexpr int RPT = RS_ROWS / NT;
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int kof = kk * 32 + (lane >> 4) * 8;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) fa[kk][i] = lds_frag(A + (wm * 64 + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        fb[kk][t][c] = lds_frag(W + (t * RPT + wn * 16 * C + 16 * c + (lane & 15)) * LDS_STRIDE + kof);
+  }
+}
+
+template <int NT, int C>
+__device__ __forceinline__ void mfmas_rs(const half8 (&fa)[2][4], const half8 (&fb)[2][NT][C],
+                                         f32x4v (&acc)[NT][4][C]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          acc[t][i][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[kk][i], fb[kk][t][c], acc[t][i][c], 0, 0, 0);
+}
+
+// One K loop.  DW: this wave stages and decodes weights of width B (block
+// half BLK of its rows; its tensor t, index h among the tensor's waves),
+// else it moves 4 pieces of activations per step.  LDS: A [2][BM], W
+// [2][128] (binary16 rows of LDS_STRIDE), raw [2][128][RS_RAW], scales
+// [2][128][RS_SCL].  Raw stage t (K steps 8t .. 8t + 7) is stored to LDS at
+// step 8t - 2 and requested one stage earlier, at step 8t - 10 (the prologue
+// loads stage 0 and requests stage 1), so its loads have a whole stage to
+// arrive; step s + 1 is decoded during step s.
+template <int NT, int C, int B, int BLK, bool DW>
+__device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, int n0, int U, int K,
+                                             const MOEQ_GLOBAL u32x4* arow, _Float16* adst, _Float16* As, _Float16* Ws,
+                                             uint32_t* raw, uint32_t* scl, int lane, int wm, int wn, int nk,
+                                             f32x4v (&acc)[NT][4][C]) {
+  const int wrow = tt * 64 + lane;     // decode row: rows 64 (w % 2) + lane
+  const int ts = NT == 2 ? tt : 0;     // the staged tensor of this wave
+  RsStage<B> st;
+  u32x4 xv[2][4];
+  // decode step s into W buffer s % 2 (S2: s % 2, compile-time)
+#define RS_DECODE(S2, s)                                                                                   \
+  do {                                                                                                     \
+    if constexpr (DW) {                                                                                    \
+      const int sb_ = ((s) >> 3) & 1, ul_ = ((s) >> 1) & 3;                                               \
+      const RawBlk rb_ = rs_block<B, 2 * (S2) + BLK>(raw + sb_ * RS_ROWS * RS_RAW, scl + sb_ * RS_ROWS * RS_SCL, \
+                                                     wrow, ul_);                                           \
+      decode_blk<B>(rb_, ((2 * (S2) + BLK) * B) & 3, BLK != 0,                                            \
+                    Ws + (S2) * (RS_ROWS * LDS_STRIDE) + wrow * LDS_STRIDE + 32 * BLK);                    \
+    }                                                                                                      \
+  } while (0)
+#define RS_AMOVE(S2)                                                                                       \
+  do {                                                                                                     \
+    if constexpr (!DW) {                                                                                   \
+      u32x4* ad_ = reinterpret_cast<u32x4*>(adst + (S2) * (BM * LDS_STRIDE));                             \
+      _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) ad_[i_] = xv[S2][i_];                               \
+    }                                                                                                      \
+  } while (0)
+#define RS_ALOAD(S2, s)                                                                                    \
+  do {                                                                                                     \
+    if constexpr (!DW) {                                                                                   \
+      _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) xv[S2][i_] = arow[(s) * 8 + i_];                    \
+    }                                                                                                      \
+  } while (0)
+  // raw stage handling at the end of step s's work: store stage (s / 8) + 1
+  // at step s % 8 == 6, then request stage (s / 8) + 2
+#define RS_STAGE(s)                                                                                        \
+  do {                                                                                                     \
+    if constexpr (DW) {                                                                                    \
+      if (((s) & 7) == 6 && (s) + 2 < nk) {                                                                \
+        const int nb_ = (((s) >> 3) + 1) & 1;                                                              \
+        rs_store<B, NT>(st, raw + nb_ * RS_ROWS * RS_RAW, scl + nb_ * RS_ROWS * RS_SCL, ts, lane, h);       \
+        if (8 * (((s) >> 3) + 2) < nk) rs_load<B, NT>(st, t, n0, U, K, 4 * (((s) >> 3) + 2), lane, h);     \
+      }                                                                                                    \
+    }                                                                                                      \
+  } while (0)
+#define RS_STEP(P, s)                                                                                      \
+  do {                                                                                                     \
+    half8 fa[2][4], fb[2][NT][C];                                                                          \
+    read_frags_rs<NT, C>(As + (P) * (BM * LDS_STRIDE), Ws + (P) * (RS_ROWS * LDS_STRIDE), lane, wm, wn, fa, fb); \
+    RS_DECODE(1 - (P), (s) + 1);                                                                           \
+    RS_AMOVE(1 - (P));                                                                                     \
+    RS_ALOAD(1 - (P), min((s) + 3, nk - 1));                                                               \
+    RS_STAGE(s);                                                                                           \
+    mfmas_rs<NT, C>(fa, fb, acc);                                                                          \
+    __syncthreads();                                                                                       \
+  } while (0)
+  // prologue: stage 0 stored, stage 1 requested; steps 0 (decoded) and 1 (loaded)
+  if constexpr (DW) {
+    rs_load<B, NT>(st, t, n0, U, K, 0, lane, h);
+    rs_store<B, NT>(st, raw, scl, ts, lane, h);
+    if (8 < nk) rs_load<B, NT>(st, t, n0, U, K, 4, lane, h);
+  }
+  RS_ALOAD(0, 0);
+  RS_ALOAD(1, min(1, nk - 1));
+  __syncthreads();
+  RS_DECODE(0, 0);
+  RS_AMOVE(0);
+  RS_ALOAD(0, min(2, nk - 1));
+  __syncthreads();
+  for (int s0 = 0; s0 < nk; s0 += 2) {
+    RS_STEP(0, s0);
+    RS_STEP(1, s0 + 1);
+  }
+#undef RS_DECODE
+#undef RS_AMOVE
+#undef RS_ALOAD
+#undef RS_STAGE
+#undef RS_STEP
+}
+
+// activations of tile row tid / 2 (half tid % 2) for the movers (tid = t - 256)
+__device__ __forceinline__ void rs_mover(int tid, int* ar, int* ah) {
+  const int at = tid & 255;
+  *ar = at >> 1;
+  *ah = at & 1;
+}
+
+__device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
+                               const TensorDev tu, _Float16* lds) {
+  _Float16* As = lds;
+  _Float16* Ws = lds + 2 * BM * LDS_STRIDE;
+  uint32_t* raw = reinterpret_cast<uint32_t*>(Ws + 2 * RS_ROWS * LDS_STRIDE);
+  uint32_t* scl = raw + 2 * RS_ROWS * RS_RAW;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
+  const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
+  const bool dw = __builtin_amdgcn_readfirstlane(wave) < 4;
+  const int tt = wave & 1, h = (wave >> 1) & 1, blk = (wave >> 1) & 1;
+  const TensorDev t = tt ? tu : tg;
+  const int bits = __builtin_amdgcn_readfirstlane(t.bits);
+  int ar, ah;
+  rs_mover(tid, &ar, &ah);
+  int tok = 0;
+  if (m0 + ar < sl.M) tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
+  const MOEQ_GLOBAL u32x4* arow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + 4 * ah;
+  _Float16* adst = As + ar * LDS_STRIDE + 32 * ah;
+
+  f32x4v acc[2][4][1];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[q][i][0] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  const int nk = H / BK;
+#define GURS(B, BL) gemm_loop_rs<2, 1, B, BL, true>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc)
+  if (!dw) {
+    gemm_loop_rs<2, 1, 2, 0, false>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc);
+  } else if (bits == 2) {
+    if (blk) GURS(2, 1); else GURS(2, 0);
+  } else if (bits == 3) {
+    if (blk) GURS(3, 1); else GURS(3, 0);
+  } else {
+    if (blk) GURS(4, 1); else GURS(4, 0);
+  }
+#undef GURS
+
+  // epilogue: undo the activation prescale, SwiGLU, store h, track row maxima
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = wm * 64 + 16 * i + (lane >> 4) * 4 + j;
+      const bool ok = m0 + r < sl.M;
+      float sc = 1.0f;
+      if (ok) {
+        const int tk = sl.shared >= 0 ? m0 + r : perm[sl.base + m0 + r] / a.k;
+        sc = __builtin_amdgcn_ldexpf(1.0f, xexp[tk]);
+      }
+      MOEQ_GLOBAL float* hout = (MOEQ_GLOBAL float*)(a.h + (size_t)(sl.base + m0 + r) * I);
+      const int col = n0 + wn * 16 + (lane & 15);
+      const float hv = silu(acc[0][i][0][j] * sc) * (acc[1][i][0][j] * sc);
+      if (ok) hout[col] = hv;
+      float rmax = fabsf(hv);
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
+      if (ok && (lane & 15) == 0) atomicMax(a.rowmax + sl.base + m0 + r, __float_as_uint(rmax));
+    }
+  }
+}
+
+// grid = m-tiles x (I / 64); tiles whose gate and up tensors are 2-4 bits wide
+__global__ __launch_bounds__(512, 1) void gateup_rs_kernel(DecodeArgs a) {
+  extern __shared__ _Float16 lds_h[];
+  const int nN = a.I / 64;
+  const int L = xcd_logical(blockIdx.x, gridDim.x);
+  const int mt = L / nN, nt = L % nN;
+  if (mt >= a.tiles[0]) return;
+  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
+  const int m0 = a.tiles[2 + 2 * mt];
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  if (tg.bits > 4 || tu.bits > 4) return;
+  gateup_rs_body(gemm_args(a), sl, m0, nt * 64, tg, tu, lds_h);
+}
+
 }  // namespace
 
 int prefill_max_mtiles(int n, int k, int S, int n_kept) {
@@ -650,7 +948,7 @@ hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
   const int grid = a.max_mtiles * (a.I / BN);
   static bool attr_n = false, attr_w = false;
-  e = launch_gemm(gateup_gemm8_kernel<false>, attr_n, grid, lds, s, a);
+  e = launch_gemm(gateup_rs_kernel, attr_n, a.max_mtiles * (a.I / 64), RS_LDS, s, a);
   if (e == hipSuccess && a.wide_gateup) e = launch_gemm(gateup_gemm8_kernel<true>, attr_w, grid, lds, s, a);
   return e;
 }
