@@ -134,18 +134,29 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
   const float* lg = rp.logits + (size_t)t * rp.E_row;
   float s[EPL], b[EPL];
+  // every load is issued before the first is used (one memory round trip;
+  // lanes past E read expert 0 and discard it)
+  float lv[EPL], bv[EPL];
+  bool kv[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    const int e = lane * EPL + i;
+    const int eo = e < E ? (rp.kept_ids ? rp.kept_ids[e] : e) : 0;  // original expert id
+    lv[i] = lg[eo];
+    bv[i] = rp.bias[eo];
+    kv[i] = rp.kept_ids || rp.mask[eo];
+  }
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
     s[i] = 0.0f;
     b[i] = -INFINITY;
     if (e < E) {
-      const int eo = rp.kept_ids ? rp.kept_ids[e] : e;  // original expert id
       // sigmoid evaluated in double precision, rounded once to float
-      float v = (float)(1.0 / (1.0 + exp(-(double)lg[eo])));
+      float v = (float)(1.0 / (1.0 + exp(-(double)lv[i])));
       if (!(v == v)) v = 0.0f;  // a NaN logit must not leave the index range undefined
       s[i] = v;
-      if (rp.kept_ids || rp.mask[eo]) b[i] = v + rp.bias[eo];
+      if (kv[i]) b[i] = v + bv[i];
     }
   }
 
@@ -364,6 +375,33 @@ __global__ __launch_bounds__(small_threads<EPL>()) void route_bucket_small_kerne
   }
 }
 
+// ---- one token: one wavefront routes it and writes the buckets directly ----
+// Every chosen expert holds one assignment: offsets[e] is the number of
+// chosen ids below e, the active list is the chosen ids in ascending order,
+// and perm at an id's ascending rank is its slot.  The result equals the
+// counting sort's.
+template <int EPL>
+__global__ __launch_bounds__(64) void route_bucket_one_kernel(RouterParams rp, Workspace ws) {
+  __shared__ float gs_l[64];
+  __shared__ int32_t ids[kMaxTopK];
+  route_token_wave<EPL>(rp, 0, gs_l, ws.idx, ws.w, ids);
+  wave_sync();
+  const int lane = threadIdx.x, k = rp.k, E = rp.E_row;
+  if (lane < k) {
+    const int mine = ids[lane];
+    int r = 0;
+    for (int j = 0; j < k; ++j) r += ids[j] < mine;
+    ws.active[1 + r] = mine;
+    ws.perm[r] = lane;
+  }
+  for (int e = lane; e <= E; e += 64) {
+    int c = 0;
+    for (int j = 0; j < k; ++j) c += ids[j] < e;
+    ws.offsets[e] = c;
+  }
+  if (lane == 0) ws.active[0] = k;
+}
+
 // ---- large batches: one token per wavefront ----
 template <int EPL>
 __global__ __launch_bounds__(256) void route_tokens_kernel(RouterParams rp, int n, int32_t* idx,
@@ -432,6 +470,16 @@ __global__ __launch_bounds__(256) void bucket_scatter_kernel(const int32_t* idx,
 hipError_t launch_route_bucket_small(const RouterParams& rp, const int32_t* idx_in, int n,
                                      const Workspace& ws, hipStream_t s) {
   // lanes own enough experts for both the router's and the buckets' id range
+  if (!idx_in && n == 1) {
+    switch (experts_per_lane(rp.E_row)) {
+      case 1: route_bucket_one_kernel<1><<<1, 64, 0, s>>>(rp, ws); break;
+      case 2: route_bucket_one_kernel<2><<<1, 64, 0, s>>>(rp, ws); break;
+      case 4: route_bucket_one_kernel<4><<<1, 64, 0, s>>>(rp, ws); break;
+      case 8: route_bucket_one_kernel<8><<<1, 64, 0, s>>>(rp, ws); break;
+      default: route_bucket_one_kernel<16><<<1, 64, 0, s>>>(rp, ws); break;
+    }
+    return hipGetLastError();
+  }
   switch (experts_per_lane(rp.E_row)) {
     case 1: route_bucket_small_kernel<1><<<1, small_threads<1>(), 0, s>>>(rp, idx_in, n, ws); break;
     case 2: route_bucket_small_kernel<2><<<1, small_threads<2>(), 0, s>>>(rp, idx_in, n, ws); break;
