@@ -288,13 +288,13 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     wo = align_up(wo + bytes, 256);
     return at;
   };
-  const int max_mtiles = prefill_max_mtiles(T, k, S, n_kept);
+  const int max_mtiles = prefill_max_mtiles(T, k, S, n_kept), max_small = prefill_max_small(T, k, S, n_kept);
   const size_t o_idx = ws_take(nk * 4), o_w = ws_take(nk * 4), o_off = ws_take((size_t)(E + 1) * 4),
                o_perm = ws_take(nk * 4), o_act = ws_take((size_t)(E + 1) * 4),
                o_cc = ws_take(chunks * E * 4), o_rank = ws_take(nk * 4),
                o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4),
                o_xexp = ws_take((size_t)T * 4), o_rmax = ws_take(rows_h * 4),
-               o_tiles = ws_take((size_t)(1 + 2 * max_mtiles) * 4),
+               o_tiles = ws_take((size_t)(3 + 4 * max_mtiles + 2 * max_small) * 4),
                o_x16 = ws_take((size_t)T * H * 2), o_h16 = ws_take(rows_h * I * 2);
 
   // ---- device work ----
@@ -402,6 +402,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->ws.xexp = (int32_t*)(w + o_xexp);
   L->ws.rowmax = (uint32_t*)(w + o_rmax);
   L->ws.tiles = (int32_t*)(w + o_tiles);
+  L->ws.tiles_small = L->ws.tiles + 1 + 2 * max_mtiles;
+  L->ws.tiles_all = L->ws.tiles_small + 1 + 2 * max_small;
   L->ws.x16 = (uint16_t*)(w + o_x16);
   L->ws.h16 = (uint16_t*)(w + o_h16);
   *out = L;
@@ -466,6 +468,9 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.rowmax = L->ws.rowmax;
   a.tiles = L->ws.tiles;
   a.max_mtiles = prefill_max_mtiles(n, a.k, a.S, L->n_kept);
+  a.tiles_small = L->ws.tiles_small;
+  a.tiles_all = L->ws.tiles_all;
+  a.max_small = prefill_max_small(n, a.k, a.S, L->n_kept);
   a.x16 = L->ws.x16;
   a.h16 = L->ws.h16;
   a.wide_gateup = L->wide_gateup;

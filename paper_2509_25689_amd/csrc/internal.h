@@ -73,7 +73,9 @@ struct Workspace {
   float* partial;      // [(T*k + T*S) x H] per-assignment expert outputs, t*k + j then shared
   int32_t* xexp;       // [T]     per-token exponent e: x * 2^-e fits binary16
   uint32_t* rowmax;    // [T*k + T*S] max |h| of each activation row (float bits)
-  int32_t* tiles;      // [1 + 2*max_mtiles] count, then (slot, first row) per m-tile
+  int32_t* tiles;      // [1 + 2*max_mtiles] count, then (slot, first row) per 128-row m-tile
+  int32_t* tiles_small;  // [1 + 2*max_small] the same for the 64-row tiles of bucket remainders
+  int32_t* tiles_all;  // [1 + 2*max_mtiles] every bucket in 128-row tiles, slot order
   uint16_t* x16;       // [T x H]  binary16 x * 2^-xexp (many-token path)
   uint16_t* h16;       // [(T*k + T*S) x I] binary16 h * 2^-(row exponent) (many-token path)
 };
@@ -110,6 +112,9 @@ struct DecodeArgs {
   uint32_t* rowmax;
   int32_t* tiles;
   int32_t max_mtiles;
+  int32_t* tiles_small;
+  int32_t max_small;
+  int32_t* tiles_all;
   const uint16_t* x16;
   uint16_t* h16;
   // slots with a 5/6/8-bit gate or up (down) tensor: 0 none, 1 shared
@@ -132,6 +137,8 @@ hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm,
 // prefill.hip
 constexpr int kGemmBM = 128;  // tokens per grouped-GEMM m-tile
 int prefill_max_mtiles(int n, int k, int S, int n_kept);
+// 64-row tiles: at most one per bucket (its remainder of 1..64 rows)
+int prefill_max_small(int n, int k, int S, int n_kept);
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s);
 

@@ -4,8 +4,9 @@
 // multiplies its bucket of tokens by its weights, so the layer becomes a set
 // of independent GEMMs of very different heights (routing is skewed).  The
 // bucketing permutation lists each expert's tokens contiguously; a small
-// kernel cuts every bucket into m-tiles of kGemmBM rows and writes the tile
-// list, so the GEMM grids never depend on a host synchronization.
+// kernel cuts every bucket into m-tiles of kGemmBM (128) rows, a remainder
+// of at most 64 rows into a 64-row tile for the gate/up GEMM, and writes the
+// tile lists, so the GEMM grids never depend on a host synchronization.
 //
 // Arithmetic: activations (bf16, exact in binary16 after a per-token
 // power-of-two prescale), dequantized weights fp16(d * (c - z)) (one rounding)
@@ -19,8 +20,9 @@
 // arrangement, each owning 64 rows x 32 columns of 16 x 16 MFMA tiles.  LDS
 // holds two decoded K steps and registers the raw data of the next two, so
 // the decode of one step and the loads of later ones overlap the current
-// step's MFMAs.  Workgroup ids are remapped so that consecutive tiles of one
-// expert land on one XCD and share its L2.
+// step's MFMAs.  Workgroups are mapped to tiles from the tile count on the
+// device: each XCD takes an equal run of consecutive m-tiles (one expert's
+// tiles share its L2), whatever the worst-case size of the grid.
 #include "internal.h"
 #include "layout.h"
 
@@ -36,10 +38,19 @@ constexpr int BM = kGemmBM, BN = 128, BK = 64;
 // halves per LDS row: 16 halves of padding (measured best of 8, 16, 24, 40)
 constexpr int LDS_STRIDE = BK + 16;
 
-// ---- tile list: slot order = shared experts, then active experts ----
+// ---- tile lists: slot order = shared experts, then active experts ----
+// For the gate/up GEMM of 2-4-bit tensors a bucket of M rows becomes M / 128
+// full 128-row tiles; a remainder of more than 64 rows takes one more
+// 128-row tile, one of 1..64 rows a 64-row tile in the second list.  The
+// third list cuts every bucket into ceil(M / 128) 128-row tiles (the GEMMs
+// without a 64-row variant), large and small buckets interleaved in slot
+// order, so every XCD's share mixes both.
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
-  __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];
+  __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];   // 128-row tiles
+  __shared__ int32_t scnt[kMaxShared + kMaxExperts + 1];  // 64-row tile (0 or 1)
   __shared__ int32_t off[kMaxShared + kMaxExperts + 2];
+  __shared__ int32_t soff[kMaxShared + kMaxExperts + 2];
+  __shared__ int32_t aoff[kMaxShared + kMaxExperts + 2];
   const int tid = threadIdx.x;
   const int nslots = a.S + a.active[0];
   for (int s = tid; s < nslots; s += 1024) {
@@ -50,30 +61,50 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
       const int e = a.active[1 + s - a.S];
       M = a.offsets[e + 1] - a.offsets[e];
     }
-    cnt[s] = (M + BM - 1) / BM;
+    const int r = M % BM;
+    cnt[s] = M / BM + (r > BM / 2 ? 1 : 0);
+    scnt[s] = r > 0 && r <= BM / 2 ? 1 : 0;
   }
   // rows of h whose running maxima the gate/up epilogue accumulates
   const int rows = a.n * (a.k + a.S);
   for (int r = tid; r < rows; r += 1024) a.rowmax[r] = 0u;
   __syncthreads();
   if (tid == 0) {
-    int run = 0;
+    int run = 0, srun = 0, arun = 0;
     for (int s = 0; s < nslots; ++s) {
       off[s] = run;
+      soff[s] = srun;
+      aoff[s] = arun;
       run += cnt[s];
+      srun += scnt[s];
+      arun += cnt[s] + scnt[s];
     }
-    off[nslots] = run;
     a.tiles[0] = min(run, a.max_mtiles);
+    a.tiles_small[0] = min(srun, a.max_small);
+    a.tiles_all[0] = min(arun, a.max_mtiles);
   }
   __syncthreads();
-  for (int s = tid; s < nslots; s += 1024)
-    for (int i = 0; i < cnt[s]; ++i) {
+  for (int s = tid; s < nslots; s += 1024) {
+    const int nb = cnt[s];
+    for (int i = 0; i < nb; ++i) {
       const int t = off[s] + i;
       if (t < a.max_mtiles) {
         a.tiles[1 + 2 * t] = s;
         a.tiles[2 + 2 * t] = i * BM;
       }
     }
+    if (scnt[s] && soff[s] < a.max_small) {
+      a.tiles_small[1 + 2 * soff[s]] = s;
+      a.tiles_small[2 + 2 * soff[s]] = nb * BM;
+    }
+    for (int i = 0; i < nb + scnt[s]; ++i) {
+      const int t = aoff[s] + i;
+      if (t < a.max_mtiles) {
+        a.tiles_all[1 + 2 * t] = s;
+        a.tiles_all[2 + 2 * t] = i * BM;
+      }
+    }
+  }
 }
 
 struct SlotInfo {
@@ -97,15 +128,23 @@ __device__ __forceinline__ SlotInfo slot_of(const DecodeArgs& a, int s) {
   return r;
 }
 
-// Workgroup id -> logical id: the hardware deals workgroups to the 8 XCDs
-// round-robin; consecutive logical ids are made to share an XCD.
-__device__ __forceinline__ int xcd_logical(int hw, int total) {
-  constexpr int X = 8;
-  const int xcd = hw % X, idx = hw / X;
-  const int per = total / X, extra = total % X;
-  // XCDs [0, extra) own per + 1 ids, the rest own per
-  return xcd < extra ? xcd * (per + 1) + idx : extra * (per + 1) + (xcd - extra) * per + idx;
+// Workgroup -> (m-tile, n-tile) for T m-tiles of nN n-tiles each.  The
+// hardware deals workgroup ids to the 8 XCDs round-robin; XCD x takes the
+// m-tiles [x B, x B + B), B = ceil(T / 8), all n-tiles of an m-tile in a row,
+// so one m-tile's activations stay in one L2 and every XCD gets the same
+// share of the T tiles present, however large the grid (which covers
+// 8 ceil(Tmax / 8) m-tiles).  False for a workgroup without a tile.
+constexpr int kXcds = 8;
+__device__ __forceinline__ bool tile_of_wg(int hw, int T, int nN, int* mt, int* nt) {
+  const int x = hw % kXcds, j = hw / kXcds;
+  const int B = (T + kXcds - 1) / kXcds;
+  const int lm = j / nN;
+  if (lm >= B) return false;
+  *mt = x * B + lm;
+  *nt = j % nN;
+  return *mt < T;
 }
+inline int tile_grid(int max_tiles, int nN) { return (max_tiles + kXcds - 1) / kXcds * kXcds * nN; }
 
 // Row-base pointer of a tensor row in the device layout.
 __device__ __forceinline__ const MOEQ_GLOBAL u32x4* row_chunks(const TensorDev& t, int bits, int row) {
@@ -509,11 +548,11 @@ template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.I / BN;
-  const int L = xcd_logical(blockIdx.x, gridDim.x);
-  const int mt = L / nN, nt = L % nN;
-  if (mt >= a.tiles[0]) return;
-  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
-  const int m0 = a.tiles[2 + 2 * mt];
+  int mt, nt, slot, m0;
+  if (!tile_of_wg(blockIdx.x, a.tiles_all[0], nN, &mt, &nt)) return;
+  slot = a.tiles_all[1 + 2 * mt];
+  m0 = a.tiles_all[2 + 2 * mt];
+  const SlotInfo sl = slot_of(a, slot);
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   if ((tg.bits > 4 || tu.bits > 4) != WIDE) return;
@@ -608,11 +647,11 @@ template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.H / BN;
-  const int L = xcd_logical(blockIdx.x, gridDim.x);
-  const int mt = L / nN, nt = L % nN;
-  if (mt >= a.tiles[0]) return;
-  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
-  const int m0 = a.tiles[2 + 2 * mt];
+  int mt, nt, slot, m0;
+  if (!tile_of_wg(blockIdx.x, a.tiles_all[0], nN, &mt, &nt)) return;
+  slot = a.tiles_all[1 + 2 * mt];
+  m0 = a.tiles_all[2 + 2 * mt];
+  const SlotInfo sl = slot_of(a, slot);
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
   if ((td.bits > 4) != WIDE) return;
@@ -644,9 +683,12 @@ constexpr int RS_ROWS = 128;
 constexpr int RS_RAW = 4 * 16 + 4;   // dwords per staged row: 4 chunk planes x 4 units (+ padding)
 constexpr int RS_SCL = 10;           // dwords per staged row of scales: 16 binary16 (+ padding; even, so
                                      // the 8-byte stores stay aligned)
-constexpr size_t RS_LDS = (size_t)2 * (BM + RS_ROWS) * LDS_STRIDE * 2 + (size_t)2 * RS_ROWS * RS_RAW * 4 +
-                          (size_t)2 * RS_ROWS * RS_SCL * 4;
-static_assert(RS_LDS <= 160 * 1024, "the raw-staged tile must fit the LDS of a compute unit");
+// LDS of a tile of bmt tokens: A [2][bmt], W [2][128], raw and scale stages
+constexpr size_t rs_lds(int bmt) {
+  return (size_t)2 * (bmt + RS_ROWS) * LDS_STRIDE * 2 + (size_t)2 * RS_ROWS * RS_RAW * 4 +
+         (size_t)2 * RS_ROWS * RS_SCL * 4;
+}
+static_assert(rs_lds(BM) <= 160 * 1024, "the raw-staged tile must fit the LDS of a compute unit");
 
 // one raw stage (4 units) of this lane: 2B chunk pieces and 2 scale pieces
 template <int B>
@@ -712,15 +754,17 @@ __device__ __forceinline__ RawBlk rs_block(const uint32_t* raw, const uint32_t* 
   return r;
 }
 
-template <int NT, int C>
+// MI: 16-row MFMA tiles per wave along the tokens (4 for 128-token tiles, 2
+// for 64-token tiles)
+template <int NT, int C, int MI>
 __device__ __forceinline__ void read_frags_rs(const _Float16* A, const _Float16* W, int lane, int wm, int wn,
-                                              half8 (&fa)[2][4], half8 (&fb)[2][NT][C]) {
+                                              half8 (&fa)[2][MI], half8 (&fb)[2][NT][C]) {
   constexpr int RPT = RS_ROWS / NT;
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
     const int kof = kk * 32 + (lane >> 4) * 8;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) fa[kk][i] = lds_frag(A + (wm * 64 + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
+    for (int i = 0; i < MI; ++i) fa[kk][i] = lds_frag(A + (wm * 16 * MI + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -729,9 +773,9 @@ __device__ __forceinline__ void read_frags_rs(const _Float16* A, const _Float16*
   }
 }
 
-template <int NT, int C>
-__device__ __forceinline__ void mfmas_rs(const half8 (&fa)[2][4], const half8 (&fb)[2][NT][C],
-                                         f32x4v (&acc)[NT][4][C]) {
+template <int NT, int C, int MI>
+__device__ __forceinline__ void mfmas_rs(const half8 (&fa)[2][MI], const half8 (&fb)[2][NT][C],
+                                         f32x4v (&acc)[NT][MI][C]) {
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
@@ -739,27 +783,28 @@ __device__ __forceinline__ void mfmas_rs(const half8 (&fa)[2][4], const half8 (&
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
           acc[t][i][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[kk][i], fb[kk][t][c], acc[t][i][c], 0, 0, 0);
 }
 
 // One K loop.  DW: this wave stages and decodes weights of width B (block
 // half BLK of its rows; its tensor t, index h among the tensor's waves),
-// else it moves 4 pieces of activations per step.  LDS: A [2][BM], W
+// else it moves MI pieces of activations per step.  LDS: A [2][32 MI], W
 // [2][128] (binary16 rows of LDS_STRIDE), raw [2][128][RS_RAW], scales
 // [2][128][RS_SCL].  Raw stage t (K steps 8t .. 8t + 7) is stored to LDS at
 // step 8t - 2 and requested one stage earlier, at step 8t - 10 (the prologue
 // loads stage 0 and requests stage 1), so its loads have a whole stage to
 // arrive; step s + 1 is decoded during step s.
-template <int NT, int C, int B, int BLK, bool DW>
+template <int NT, int C, int B, int BLK, bool DW, int MI>
 __device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, int n0, int U, int K,
                                              const MOEQ_GLOBAL u32x4* arow, _Float16* adst, _Float16* As, _Float16* Ws,
                                              uint32_t* raw, uint32_t* scl, int lane, int wm, int wn, int nk,
-                                             f32x4v (&acc)[NT][4][C]) {
+                                             f32x4v (&acc)[NT][MI][C]) {
+  constexpr int ABUF = 32 * MI * LDS_STRIDE;  // halves per A buffer
   const int wrow = tt * 64 + lane;     // decode row: rows 64 (w % 2) + lane
   const int ts = NT == 2 ? tt : 0;     // the staged tensor of this wave
   RsStage<B> st;
-  u32x4 xv[2][4];
+  u32x4 xv[2][MI];
   // decode step s into W buffer s % 2 (S2: s % 2, compile-time)
 #define RS_DECODE(S2, s)                                                                                   \
   do {                                                                                                     \
@@ -774,14 +819,14 @@ __device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, 
 #define RS_AMOVE(S2)                                                                                       \
   do {                                                                                                     \
     if constexpr (!DW) {                                                                                   \
-      u32x4* ad_ = reinterpret_cast<u32x4*>(adst + (S2) * (BM * LDS_STRIDE));                             \
-      _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) ad_[i_] = xv[S2][i_];                               \
+      u32x4* ad_ = reinterpret_cast<u32x4*>(adst + (S2) * ABUF);                                          \
+      _Pragma("unroll") for (int i_ = 0; i_ < MI; ++i_) ad_[i_] = xv[S2][i_];                              \
     }                                                                                                      \
   } while (0)
 #define RS_ALOAD(S2, s)                                                                                    \
   do {                                                                                                     \
     if constexpr (!DW) {                                                                                   \
-      _Pragma("unroll") for (int i_ = 0; i_ < 4; ++i_) xv[S2][i_] = arow[(s) * 8 + i_];                    \
+      _Pragma("unroll") for (int i_ = 0; i_ < MI; ++i_) xv[S2][i_] = arow[(s) * 8 + i_];                   \
     }                                                                                                      \
   } while (0)
   // raw stage handling at the end of step s's work: store stage (s / 8) + 1
@@ -798,13 +843,13 @@ __device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, 
   } while (0)
 #define RS_STEP(P, s)                                                                                      \
   do {                                                                                                     \
-    half8 fa[2][4], fb[2][NT][C];                                                                          \
-    read_frags_rs<NT, C>(As + (P) * (BM * LDS_STRIDE), Ws + (P) * (RS_ROWS * LDS_STRIDE), lane, wm, wn, fa, fb); \
+    half8 fa[2][MI], fb[2][NT][C];                                                                         \
+    read_frags_rs<NT, C, MI>(As + (P) * ABUF, Ws + (P) * (RS_ROWS * LDS_STRIDE), lane, wm, wn, fa, fb);   \
     RS_DECODE(1 - (P), (s) + 1);                                                                           \
     RS_AMOVE(1 - (P));                                                                                     \
     RS_ALOAD(1 - (P), min((s) + 3, nk - 1));                                                               \
     RS_STAGE(s);                                                                                           \
-    mfmas_rs<NT, C>(fa, fb, acc);                                                                          \
+    mfmas_rs<NT, C, MI>(fa, fb, acc);                                                                      \
     __syncthreads();                                                                                       \
   } while (0)
   // prologue: stage 0 stored, stage 1 requested; steps 0 (decoded) and 1 (loaded)
@@ -831,17 +876,14 @@ __device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, 
 #undef RS_STEP
 }
 
-// activations of tile row tid / 2 (half tid % 2) for the movers (tid = t - 256)
-__device__ __forceinline__ void rs_mover(int tid, int* ar, int* ah) {
-  const int at = tid & 255;
-  *ar = at >> 1;
-  *ah = at & 1;
-}
-
+// Tile of BMT tokens (128 or 64).  The 256 movers take piece t % TPR of tile
+// row t / TPR (TPR = 2 or 4 movers per row, MI 16-byte pieces each per step).
+template <int BMT>
 __device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
                                const TensorDev tu, _Float16* lds) {
+  constexpr int MI = BMT / 32, TPR = 8 / MI;
   _Float16* As = lds;
-  _Float16* Ws = lds + 2 * BM * LDS_STRIDE;
+  _Float16* Ws = lds + 2 * BMT * LDS_STRIDE;
   uint32_t* raw = reinterpret_cast<uint32_t*>(Ws + 2 * RS_ROWS * LDS_STRIDE);
   uint32_t* scl = raw + 2 * RS_ROWS * RS_RAW;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -853,22 +895,22 @@ __device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int 
   const int tt = wave & 1, h = (wave >> 1) & 1, blk = (wave >> 1) & 1;
   const TensorDev t = tt ? tu : tg;
   const int bits = __builtin_amdgcn_readfirstlane(t.bits);
-  int ar, ah;
-  rs_mover(tid, &ar, &ah);
+  const int ar = (tid & 255) / TPR, aq = (tid & 255) % TPR;
   int tok = 0;
   if (m0 + ar < sl.M) tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
-  const MOEQ_GLOBAL u32x4* arow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + 4 * ah;
-  _Float16* adst = As + ar * LDS_STRIDE + 32 * ah;
+  const MOEQ_GLOBAL u32x4* arow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + MI * aq;
+  _Float16* adst = As + ar * LDS_STRIDE + 8 * MI * aq;
 
-  f32x4v acc[2][4][1];
+  f32x4v acc[2][MI][1];
 #pragma unroll
   for (int q = 0; q < 2; ++q)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[q][i][0] = f32x4v{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < MI; ++i) acc[q][i][0] = f32x4v{0.f, 0.f, 0.f, 0.f};
   const int nk = H / BK;
-#define GURS(B, BL) gemm_loop_rs<2, 1, B, BL, true>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc)
+#define GURS(B, BL) \
+  gemm_loop_rs<2, 1, B, BL, true, MI>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc)
   if (!dw) {
-    gemm_loop_rs<2, 1, 2, 0, false>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc);
+    gemm_loop_rs<2, 1, 2, 0, false, MI>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc);
   } else if (bits == 2) {
     if (blk) GURS(2, 1); else GURS(2, 0);
   } else if (bits == 3) {
@@ -880,10 +922,10 @@ __device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int 
 
   // epilogue: undo the activation prescale, SwiGLU, store h, track row maxima
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < MI; ++i) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = wm * 64 + 16 * i + (lane >> 4) * 4 + j;
+      const int r = wm * 16 * MI + 16 * i + (lane >> 4) * 4 + j;
       const bool ok = m0 + r < sl.M;
       float sc = 1.0f;
       if (ok) {
@@ -902,19 +944,21 @@ __device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int 
   }
 }
 
-// grid = m-tiles x (I / 64); tiles whose gate and up tensors are 2-4 bits wide
+// grid = m-tiles x (I / 64); tiles whose gate and up tensors are 2-4 bits
+// wide, from the 128-row list (BMT = 128) or the 64-row list (BMT = 64)
+template <int BMT>
 __global__ __launch_bounds__(512, 1) void gateup_rs_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.I / 64;
-  const int L = xcd_logical(blockIdx.x, gridDim.x);
-  const int mt = L / nN, nt = L % nN;
-  if (mt >= a.tiles[0]) return;
-  const SlotInfo sl = slot_of(a, a.tiles[1 + 2 * mt]);
-  const int m0 = a.tiles[2 + 2 * mt];
+  const int32_t* tl = BMT == BM ? a.tiles : a.tiles_small;
+  int mt, nt;
+  if (!tile_of_wg(blockIdx.x, tl[0], nN, &mt, &nt)) return;
+  const SlotInfo sl = slot_of(a, tl[1 + 2 * mt]);
+  const int m0 = tl[2 + 2 * mt];
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   if (tg.bits > 4 || tu.bits > 4) return;
-  gateup_rs_body(gemm_args(a), sl, m0, nt * 64, tg, tu, lds_h);
+  gateup_rs_body<BMT>(gemm_args(a), sl, m0, nt * 64, tg, tu, lds_h);
 }
 
 }  // namespace
@@ -923,6 +967,11 @@ int prefill_max_mtiles(int n, int k, int S, int n_kept) {
   const long long nk = (long long)n * k;
   const long long routed = (nk + BM - 1) / BM + (nk < n_kept ? nk : n_kept);
   return (int)(routed + (long long)S * ((n + BM - 1) / BM));
+}
+
+int prefill_max_small(int n, int k, int S, int n_kept) {
+  const long long nk = (long long)n * k;
+  return (int)((nk < n_kept ? nk : n_kept) + S);
 }
 
 namespace {
@@ -946,9 +995,11 @@ hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
-  const int grid = a.max_mtiles * (a.I / BN);
-  static bool attr_n = false, attr_w = false;
-  e = launch_gemm(gateup_rs_kernel, attr_n, a.max_mtiles * (a.I / 64), RS_LDS, s, a);
+  const int grid = tile_grid(a.max_mtiles, a.I / BN);
+  static bool attr_n = false, attr_s = false, attr_w = false;
+  e = launch_gemm(gateup_rs_kernel<BM>, attr_n, tile_grid(a.max_mtiles, a.I / 64), rs_lds(BM), s, a);
+  if (e == hipSuccess)
+    e = launch_gemm(gateup_rs_kernel<BM / 2>, attr_s, tile_grid(a.max_small, a.I / 64), rs_lds(BM / 2), s, a);
   if (e == hipSuccess && a.wide_gateup) e = launch_gemm(gateup_gemm8_kernel<true>, attr_w, grid, lds, s, a);
   return e;
 }
@@ -959,7 +1010,7 @@ hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
-  const int grid = a.max_mtiles * (a.H / BN);
+  const int grid = tile_grid(a.max_mtiles, a.H / BN);
   static bool attr_n = false, attr_w = false;
   e = launch_gemm(down_gemm8_kernel<false>, attr_n, grid, lds, s, a);
   if (e == hipSuccess && a.wide_down) e = launch_gemm(down_gemm8_kernel<true>, attr_w, grid, lds, s, a);

@@ -184,6 +184,25 @@ def test_forward_tiny(gpu_lib, tiny, n, path):
     _forward_check(gpu_lib, data, L, n, "fwd-tiny", path)
 
 
+@pytest.mark.parametrize("n", [64, 65, 128, 129, 192, 193])
+@pytest.mark.parametrize("which", ["tiny", "tiny_mixed"])
+def test_prefill_tile_edges(request, gpu_lib, which, n):
+    """Every token routed to the same two kept experts, so those buckets and
+    the shared expert's hold n rows each: one 64-row tile (n = 64), one
+    128-row tile of 65 or 128 rows, a 128-row tile plus a 64-row tile of 1
+    or 64 rows (129, 192), two 128-row tiles (193); grouped-GEMM path."""
+    data, L = request.getfixturevalue(which)
+    shape = data.shape
+    kept = np.nonzero(data.mask)[0]
+    per = shape.n_experts // shape.n_group
+    pair = [int(e) for e in kept if e // per == kept[0] // per][:2]
+    logits = (0.1 * synth.normal_logits(n, shape.n_experts, "tile-edges", n)).astype(np.float32)
+    logits[:, pair] += 8.0
+    ridx, _ = _route_oracle(shape, data.mask, logits)
+    assert (np.sort(ridx, axis=1) == np.array(sorted(pair))).all()
+    _forward_check(gpu_lib, data, L, n, "tile-edges", gpu_lib.MOEQ_PATH_PREFILL, logits=logits)
+
+
 @pytest.mark.parametrize("path", [1, 2])
 def test_forward_tiny_mixed_bits(gpu_lib, tiny_mixed, path):
     data, L = tiny_mixed
