@@ -40,10 +40,10 @@ constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against 
 // kGateUpBuf (kDownBuf) register buffers, i.e. NBUF - 1 steps of codes in
 // flight while one is reduced; MinBlocks bounds registers for occupancy.
 #ifndef MOEQ_GATEUP_STEPS
-#define MOEQ_GATEUP_STEPS 4
+#define MOEQ_GATEUP_STEPS 8
 #endif
 #ifndef MOEQ_GATEUP_BUF
-#define MOEQ_GATEUP_BUF 1
+#define MOEQ_GATEUP_BUF 2
 #endif
 #ifndef MOEQ_DOWN_STEPS
 #define MOEQ_DOWN_STEPS 4
@@ -57,10 +57,19 @@ constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against 
 #ifndef MOEQ_DOWN_MINBLOCKS
 #define MOEQ_DOWN_MINBLOCKS 4
 #endif
+// the down kernel for 2-64 tokens (the values above serve one token)
+#ifndef MOEQ_DOWNM_STEPS
+#define MOEQ_DOWNM_STEPS 4
+#endif
+#ifndef MOEQ_DOWNM_BUF
+#define MOEQ_DOWNM_BUF 1
+#endif
 constexpr int kGateUpSteps = MOEQ_GATEUP_STEPS, kGateUpBuf = MOEQ_GATEUP_BUF;
 static_assert(MOEQ_GATEUP_STEPS % MOEQ_GATEUP_BUF == 0 && MOEQ_DOWN_STEPS % MOEQ_DOWN_BUF == 0,
               "steps per wave must be a multiple of the pipeline depth");
 constexpr int kDownSteps = MOEQ_DOWN_STEPS, kDownBuf = MOEQ_DOWN_BUF;
+constexpr int kDownStepsM = MOEQ_DOWNM_STEPS, kDownBufM = MOEQ_DOWNM_BUF;
+static_assert(MOEQ_DOWNM_STEPS % MOEQ_DOWNM_BUF == 0, "steps per wave must be a multiple of the pipeline depth");
 constexpr int kGateUpMinBlocks = MOEQ_GATEUP_MINBLOCKS, kDownMinBlocks = MOEQ_DOWN_MINBLOCKS;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -914,9 +923,10 @@ hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const int slots = a.S + a.max_active;
   const int U = a.I / kUnit;
   const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
-  const int rows_wg = 4 * (64 / LPR) * kDownSteps;
+  constexpr int RW = TM == 1 ? kDownSteps : kDownStepsM, NB = TM == 1 ? kDownBuf : kDownBufM;
+  const int rows_wg = 4 * (64 / LPR) * RW;
   dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);
-  return launch_lds(down_kernel<LPR, TM, kDownSteps, kDownBuf>, grid, lds, s, a);
+  return launch_lds(down_kernel<LPR, TM, RW, NB>, grid, lds, s, a);
 }
 
 template <int TM>

@@ -22,7 +22,7 @@ constexpr int kMaxTopK = 32;
 constexpr int kMaxShared = 4;
 constexpr int kChunk = 64;          // tokens per bucketing chunk (one bit per token in a 64-bit mask)
 constexpr int kDecodeMaxTokens = 64;
-constexpr int kDefaultDecodeMax = 32;
+constexpr int kDefaultDecodeMax = 64;
 
 // One stored tensor in the device layout.
 //   codes:  rows * (K/128) units of 16*bits bytes.  Row r's unit u, 16-byte
