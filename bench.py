@@ -37,13 +37,13 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 
 # HBM bytes per gate/up launch at batch 1 from rocprofv3 FETCH_SIZE + WRITE_SIZE,
 # each scaled by the same counter's reading for a plain 1 GiB copy (factors
-# 2.0 and 1.0; see profiles/gateup_kernel_decode_b1_traffic.md).  Valid only for
+# 2.0 and 1.0; see profiles/gateup1_kernel_decode_b1_traffic.md).  Valid only for
 # the kernel sources the counters were taken on, identified by their sha256:
 # any change to them reports traffic as null until the counters are retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 126870430,
+    "bytes": 126895415,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "beb91eb8cc3fed367d676affc762d7c55c64afa26bc114d2054d93b714e15e11",
+        "paper_2509_25689_amd/csrc/decode.hip": "649954892e495e963a010fba1163a6a9ff63fa6abb99e4084dd2bc4791a206b6",
         "paper_2509_25689_amd/csrc/layout.h": "60e009a556d1f9a60b3c0e727bd3d2b64bc5a2426b4bfaa43f5eb982ccdfcea7",
     },
 }
