@@ -287,6 +287,7 @@ __global__ __launch_bounds__(256, TM == 1 ? kGateUpMinBlocks : 2) void gateup_ke
   extern __shared__ uint32_t smem[];
   const Slot sl = slot_info(a, blockIdx.y);
   if (sl.M < 0) return;
+  if (sl.M == 1) return;  // one-token buckets go to gateup1_kernel
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   switch (tg.bits * 8 + tu.bits) {
@@ -472,7 +473,7 @@ __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// One token: gate/up + SwiGLU with 16 lanes per row pair.  Lanes 0-7 of a
+// Buckets of one token: gate/up + SwiGLU with 16 lanes per row pair.  Lanes 0-7 of a
 // 16-lane group stream the gate row and lanes 8-15 the up row; lane j of a
 // half walks the units j, j + 8, j + 16, ... of its row, so all lanes are
 // busy for any number of units, and the per-row work (sums, activation,
@@ -603,11 +604,11 @@ __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl,
   if ((lane & 15) == 15 && row < I) a.h[(size_t)sl.base * a.I + row] = silu(other) * v;
 }
 
-// grid = (I / 16, S + max_active), 256 threads; n = 1
+// grid = (I / 16, S + max_active), 256 threads; the buckets of one token
 __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
+  if (sl.M != 1) return;  // the buckets of one token, of any batch
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   const int U = a.H / kUnit;
@@ -947,17 +948,17 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 
 }  // namespace
 
+// Gate/up: buckets of one token (every bucket when n = 1) take the
+// one-token kernel, the others (n > 1) the kernel that stages 4 tokens at a
+// time.  Down: one kernel per batch size (measured: splitting it the same way
+// gains nothing at 16 tokens and costs 3 % at 64).
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
-  hipError_t e;
-  if (a.n == 1) {
-    const int U = a.H / kUnit;
-    const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
-    dim3 grid((a.I + 15) / 16, a.S + a.max_active);
-    gateup1_kernel<<<grid, 256, lds, s>>>(a);
-    e = hipGetLastError();
-  } else {
-    e = launch_gateup_tm<4>(a, s);
-  }
+  const int U = a.H / kUnit;
+  const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
+  dim3 grid((a.I + 15) / 16, a.S + a.max_active);
+  gateup1_kernel<<<grid, 256, lds, s>>>(a);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && a.n > 1) e = launch_gateup_tm<4>(a, s);
   return e == hipSuccess ? launch_wide_gateup(a, s) : e;
 }
 
