@@ -41,9 +41,9 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 # the kernel sources the counters were taken on, identified by their sha256:
 # any change to them reports traffic as null until the counters are retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 126895415,
+    "bytes": 127174550,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "649954892e495e963a010fba1163a6a9ff63fa6abb99e4084dd2bc4791a206b6",
+        "paper_2509_25689_amd/csrc/decode.hip": "4f1eb0c51f3e0aa6df3d98fe639e0439f4e2cc9982787cd67dbf3f86011b60da",
         "paper_2509_25689_amd/csrc/layout.h": "60e009a556d1f9a60b3c0e727bd3d2b64bc5a2426b4bfaa43f5eb982ccdfcea7",
     },
 }
@@ -464,6 +464,7 @@ def sweep_leg(torch, np, moeq, synth, hip, steps):
                                  "tokens_per_s": round(r["tokens_per_s"], 1), "us_per_step": round(r["ms_per_step"] * 1e3, 2),
                                  "distinct_experts": round(r["distinct_experts_per_step"], 1),
                                  "GBps": round(r["GBps"], 1), "hbm_frac": round(r["GBps"] / HBM_PEAK_GBPS, 4)})
+                    print(f"sweep point {len(rows)}/54: {rows[-1]}", file=sys.stderr, flush=True)
             layer[0].close()
     return rows
 
