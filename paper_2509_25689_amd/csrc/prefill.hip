@@ -542,8 +542,10 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
   }
 }
 
-// WIDE = false takes the tiles whose gate and up tensors are 2-4 bits wide,
-// WIDE = true those with a 5, 6 or 8-bit gate or up tensor
+// Launched with WIDE = true: the tiles with a 5, 6 or 8-bit gate or up
+// tensor (the other of the two may be narrower).  The 2-4-bit tiles take the
+// raw-staged gateup_rs_kernel; WIDE = false, their register-path variant, is
+// not launched.
 template <bool WIDE>
 __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
