@@ -221,6 +221,19 @@ def test_forward_v3_decode_batch16_sampled(gpu_lib, v3_decode):
     _forward_check(gpu_lib, data, L, 16, "fwd-v3-b16", gpu_lib.MOEQ_PATH_AUTO, sample=[0, 7, 15])
 
 
+@pytest.mark.parametrize("n,kind", [(48, "normal"), (64, "zipf")])
+def test_forward_v3_auto_gemv_sampled(gpu_lib, v3_prefill, n, kind):
+    """33-64 tokens on the automatic path (the GEMV path by default): buckets
+    of one token through the one-token gate/up kernel, the others through
+    the 4-token kernels, mixed 2/3/4-bit widths."""
+    data, L = v3_prefill
+    E = data.shape.n_experts
+    logits = (synth.normal_logits(n, E, "fwd-v3-auto", n) if kind == "normal"
+              else synth.zipf_logits(n, data.mask, "fwd-v3-auto", n))
+    _forward_check(gpu_lib, data, L, n, "fwd-v3-auto", gpu_lib.MOEQ_PATH_AUTO, logits=logits,
+                   sample=[0, n // 2, n - 1])
+
+
 def test_forward_v3_prefill_sampled(gpu_lib, v3_prefill):
     data, L = v3_prefill
     n = 2048
