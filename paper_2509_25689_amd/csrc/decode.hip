@@ -221,7 +221,7 @@ __device__ __forceinline__ void compute_gateup(const GateUpRows<BG, BU>& b, bool
   }
 }
 
-template <int BG, int BU, int LPR, int TM, int RW, int NBUF>
+template <int BG, int BU, int LPR, int TM, int RW, int NBUF, int NW>
 __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
                                             const TensorDev& tu, uint32_t* smem) {
   const int H = a.H, I = a.I, U = H / kUnit;
@@ -233,7 +233,7 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane / LPR, u = lane % LPR;
   const bool uok = u < U;
-  const int row0 = blockIdx.x * (4 * GPW * RW) + wave * (GPW * RW) + grp;  // + step * GPW
+  const int row0 = blockIdx.x * (NW * GPW * RW) + wave * (GPW * RW) + grp;  // + step * GPW
 
   GateUpRows<BG, BU> buf[NBUF];
   for (int m0 = 0; m0 < sl.M; m0 += TM) {
@@ -249,7 +249,7 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, 
     for (int m = 0; m < mc; ++m) {
       const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
       const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
-      for (int q = threadIdx.x; q < H / 8; q += 256) {
+      for (int q = threadIdx.x; q < H / 8; q += NW * 64) {
         const u32x4 v = src[q];
         float s = 0.0f;
         s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
@@ -281,9 +281,10 @@ __device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, 
   }
 }
 
-// grid = (row tiles of I, S + max_active), 256 threads
-template <int LPR, int TM, int RW, int NBUF>
-__global__ __launch_bounds__(256, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
+// grid = (row tiles of I, S + max_active), NW waves per workgroup (one
+// staging of the tokens' activations shared by NW waves)
+template <int LPR, int TM, int RW, int NBUF, int NW>
+__global__ __launch_bounds__(NW * 64, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   const Slot sl = slot_info(a, blockIdx.y);
   if (sl.M < 0) return;
@@ -291,15 +292,15 @@ __global__ __launch_bounds__(256, TM == 1 ? kGateUpMinBlocks : 2) void gateup_ke
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   switch (tg.bits * 8 + tu.bits) {
-    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RW, NBUF>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
     default: break;
   }
 }
@@ -863,12 +864,12 @@ __global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
 
 // launches a kernel whose dynamic LDS may exceed the 64 KiB default
 template <typename K>
-hipError_t launch_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const DecodeArgs& a) {
+hipError_t launch_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const DecodeArgs& a, int threads = 256) {
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  kernel<<<grid, 256, lds, s>>>(a);
+  kernel<<<grid, threads, lds, s>>>(a);
   return hipGetLastError();
 }
 
@@ -909,14 +910,26 @@ hipError_t launch_wide_down(const DecodeArgs& a, hipStream_t s) {
 // Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
 // rows of one slot.
 
-template <int LPR, int TM>
-hipError_t launch_gateup_lpr_tm(const DecodeArgs& a, hipStream_t s) {
+template <int LPR, int TM, int NW>
+hipError_t launch_gateup_lpr_tm_nw(const DecodeArgs& a, hipStream_t s) {
   const int slots = a.S + a.max_active;
   const int U = a.H / kUnit;
   const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
-  const int rows_wg = 4 * (64 / LPR) * kGateUpSteps;
+  const int rows_wg = NW * (64 / LPR) * kGateUpSteps;
   dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
-  return launch_lds(gateup_kernel<LPR, TM, kGateUpSteps, kGateUpBuf>, grid, lds, s, a);
+  return launch_lds(gateup_kernel<LPR, TM, kGateUpSteps, NW == 8 ? 1 : kGateUpBuf, NW>, grid, lds, s, a, NW * 64);
+}
+
+// From MOEQ_GATEUP_WIDE_FROM tokens on, workgroups of 8 waves (one register
+// buffer each) share one staging of the 4 tokens' activations: measured
+// faster from 32 tokens (-2 % at 32, -4 % at 48 and 64), slower below.
+#ifndef MOEQ_GATEUP_WIDE_FROM
+#define MOEQ_GATEUP_WIDE_FROM 32
+#endif
+template <int LPR, int TM>
+hipError_t launch_gateup_lpr_tm(const DecodeArgs& a, hipStream_t s) {
+  return a.n >= MOEQ_GATEUP_WIDE_FROM ? launch_gateup_lpr_tm_nw<LPR, TM, 8>(a, s)
+                                      : launch_gateup_lpr_tm_nw<LPR, TM, 4>(a, s);
 }
 
 template <int LPR, int TM>
