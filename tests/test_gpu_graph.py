@@ -85,3 +85,38 @@ def test_graph_replay_v3(gpu_lib, v3_layer, n):
     forward, 16 tokens, and 48 tokens (8-wave gate/up workgroups)."""
     data, L = v3_layer
     _check_replays(gpu_lib, L, data.shape, n, gpu_lib.MOEQ_PATH_AUTO, f"graph-v3-{n}")
+
+
+@pytest.mark.parametrize("n", [1, 8, 40])
+def test_graph_replay_router_gate(gpu_lib, n):
+    """Forwards that compute their logits from the layer's router weight
+    (no logits given): the gate kernel for few and for many tokens, then
+    routing, in one captured graph."""
+    data = layers.quantized_layer(synth.TINY, "all4", "graph-gate")
+    shape = data.shape
+    L = gpu_lib.Layer(shape, data.mask, data.routed(), data.shared(), max_tokens=64)
+    try:
+        L.set_router_weight(synth.router_weight(shape.n_experts, shape.hidden, "graph-gate-wr"))
+        x, _ = _inputs(shape, n, f"graph-gate-{n}")
+        xo, _ = _inputs(shape, n, f"graph-gate-{n}-other")
+        y_ref = L.forward(x)
+        y, y_other = torch.empty_like(y_ref), torch.empty_like(y_ref)
+        torch.cuda.synchronize()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            L.forward(x, y=y)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            L.forward(x, y=y)
+        for r in range(3):
+            y.zero_()
+            L.forward(xo, y=y_other)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(y, y_ref), (n, r)
+    finally:
+        L.close()
