@@ -76,6 +76,10 @@ struct moeq_layer {
   void* ws_mem = nullptr;
   Workspace ws{};
   hipEvent_t stage_events[MOEQ_STAGE_EVENTS] = {};
+  // a second stream (default priority) and two events: for 2-64 tokens the
+  // gate/up GEMVs of one-token buckets and of larger buckets run side by side
+  hipStream_t aux = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   bool timing = false;
 };
 
@@ -83,6 +87,9 @@ namespace {
 
 void release(moeq_layer* L) {
   if (!L) return;
+  if (L->aux) hipStreamDestroy(L->aux);
+  if (L->fork_ev) hipEventDestroy(L->fork_ev);
+  if (L->join_ev) hipEventDestroy(L->join_ev);
   hipFree(L->store);
   hipFree(L->desc);
   hipFree(L->mask);
@@ -406,6 +413,10 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->ws.tiles_all = L->ws.tiles_small + 1 + 2 * max_small;
   L->ws.x16 = (uint16_t*)(w + o_x16);
   L->ws.h16 = (uint16_t*)(w + o_h16);
+  if ((he = hipStreamCreateWithFlags(&L->aux, hipStreamNonBlocking)) != hipSuccess) return bail(he, "hipStreamCreate");
+  if ((he = hipEventCreateWithFlags(&L->fork_ev, hipEventDisableTiming)) != hipSuccess ||
+      (he = hipEventCreateWithFlags(&L->join_ev, hipEventDisableTiming)) != hipSuccess)
+    return bail(he, "hipEventCreate");
   *out = L;
   return ok();
 }
@@ -489,7 +500,21 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   }
   if (e == hipSuccess) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
   mark(1);
-  if (e == hipSuccess) e = prefill ? launch_gateup_prefill(a, s) : launch_gateup_decode(a, s);
+  if (e == hipSuccess) {
+    if (prefill) {
+      e = launch_gateup_prefill(a, s);
+    } else if (n > 1) {
+      // fork: the buckets of 2-64 tokens on the layer's second stream, then join
+      if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(L->aux, L->fork_ev, 0);
+      if (e == hipSuccess) e = launch_gateup_decode_multi(a, L->aux);
+      if (e == hipSuccess) e = hipEventRecord(L->join_ev, L->aux);
+      if (e == hipSuccess) e = launch_gateup_decode_single(a, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, L->join_ev, 0);
+    } else {
+      e = launch_gateup_decode(a, s);
+    }
+  }
   mark(2);
   if (e == hipSuccess) e = prefill ? launch_down_prefill(a, s) : launch_down_decode(a, s);
   mark(3);

@@ -965,14 +965,21 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 // one-token kernel, the others (n > 1) the kernel that stages 4 tokens at a
 // time.  Down: one kernel per batch size (measured: splitting it the same way
 // gains nothing at 16 tokens and costs 3 % at 64).
-hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s) {
   const int U = a.H / kUnit;
   const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
   dim3 grid((a.I + 15) / 16, a.S + a.max_active);
   gateup1_kernel<<<grid, 256, lds, s>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e == hipSuccess && a.n > 1) e = launch_gateup_tm<4>(a, s);
+  const hipError_t e = hipGetLastError();
   return e == hipSuccess ? launch_wide_gateup(a, s) : e;
+}
+
+hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2) { return launch_gateup_tm<4>(a, s2); }
+
+hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
+  hipError_t e = launch_gateup_decode_single(a, s);
+  if (e == hipSuccess && a.n > 1) e = launch_gateup_decode_multi(a, s);
+  return e;
 }
 
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {

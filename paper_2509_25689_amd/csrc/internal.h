@@ -122,6 +122,11 @@ struct DecodeArgs {
   int32_t wide_gateup, wide_down;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
+// the same work split over two streams: the one-token buckets (and the wide
+// kernels) on s, the buckets of 2-64 tokens on s2 (n > 1; the caller orders
+// s2 after the routing and joins it back into s)
+hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2);
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // gate.hip: logits = x W_r^T (bf16 x [n x H], float32 W_r [E x H]); up to
