@@ -155,8 +155,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
  *   y        DEVICE float32 [n_tokens x hidden]; fully overwritten
  * Borrowed pointers must stay valid until the stream work completes.  No
  * allocation, no memset, no host synchronization: safe to capture in a HIP
- * graph.  For 2..64 tokens on the decode path part of the work runs on a
- * second stream the layer owns, ordered after `stream` by an event and
+ * graph.  For 2..64 tokens on the decode path, and on the prefill path,
+ * part of the work runs on a second stream the layer owns, ordered after
+ * `stream` by an event and
  * joined back into `stream` by another before the forward's last kernels, so
  * all of it completes in `stream` order (a capture records the fork and
  * join).  Deterministic: identical inputs give bitwise-identical y.

@@ -502,7 +502,14 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   mark(1);
   if (e == hipSuccess) {
     if (prefill) {
-      e = launch_gateup_prefill(a, s);
+      // fork after the tile lists: the 64-row tiles on the second stream
+      e = launch_prefill_tiles(a, s);
+      if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(L->aux, L->fork_ev, 0);
+      if (e == hipSuccess) e = launch_gateup_prefill_small(a, L->aux);
+      if (e == hipSuccess) e = hipEventRecord(L->join_ev, L->aux);
+      if (e == hipSuccess) e = launch_gateup_prefill_big(a, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, L->join_ev, 0);
     } else if (n > 1) {
       // fork: the buckets of 2-64 tokens on the layer's second stream, then join
       if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);

@@ -145,6 +145,11 @@ int prefill_max_mtiles(int n, int k, int S, int n_kept);
 // 64-row tiles: at most one per bucket (its remainder of 1..64 rows)
 int prefill_max_small(int n, int k, int S, int n_kept);
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
+// the same in parts: the tile lists, then the 128-row (and 5/6/8-bit) tiles
+// and the 64-row tiles, which the forward runs on two streams side by side
+hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_gateup_prefill_big(const DecodeArgs& a, hipStream_t s);
+hipError_t launch_gateup_prefill_small(const DecodeArgs& a, hipStream_t s2);
 hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s);
 
 }  // namespace moeq

@@ -992,17 +992,29 @@ hipError_t launch_gemm(K kernel, bool& attr, int grid, size_t lds, hipStream_t s
 
 }  // namespace
 
-hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
+hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s) {
   prefill_tiles_kernel<<<1, 1024, 0, s>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_gateup_prefill_big(const DecodeArgs& a, hipStream_t s) {
   const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
   const int grid = tile_grid(a.max_mtiles, a.I / BN);
-  static bool attr_n = false, attr_s = false, attr_w = false;
-  e = launch_gemm(gateup_rs_kernel<BM>, attr_n, tile_grid(a.max_mtiles, a.I / 64), rs_lds(BM), s, a);
-  if (e == hipSuccess)
-    e = launch_gemm(gateup_rs_kernel<BM / 2>, attr_s, tile_grid(a.max_small, a.I / 64), rs_lds(BM / 2), s, a);
+  static bool attr_n = false, attr_w = false;
+  hipError_t e = launch_gemm(gateup_rs_kernel<BM>, attr_n, tile_grid(a.max_mtiles, a.I / 64), rs_lds(BM), s, a);
   if (e == hipSuccess && a.wide_gateup) e = launch_gemm(gateup_gemm8_kernel<true>, attr_w, grid, lds, s, a);
+  return e;
+}
+
+hipError_t launch_gateup_prefill_small(const DecodeArgs& a, hipStream_t s2) {
+  static bool attr_s = false;
+  return launch_gemm(gateup_rs_kernel<BM / 2>, attr_s, tile_grid(a.max_small, a.I / 64), rs_lds(BM / 2), s2, a);
+}
+
+hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
+  hipError_t e = launch_prefill_tiles(a, s);
+  if (e == hipSuccess) e = launch_gateup_prefill_big(a, s);
+  if (e == hipSuccess) e = launch_gateup_prefill_small(a, s);
   return e;
 }
 
