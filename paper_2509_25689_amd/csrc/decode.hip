@@ -21,9 +21,11 @@
 // fixed order, so results are deterministic.
 //
 // gate/up kernel: writes h (float32) for every assignment in bucket order.
-// down kernel: the activations h are split into bfloat16 hi + lo parts
-// (about 16 significant bits) and the result, times the token's routing
-// weight, is written as one partial row per (token, slot).
+// down kernel: the activations h are rounded to binary16 after a power-of-two
+// prescale per block of 32 (11 significant bits at any magnitude), the codes
+// unpacked to binary16 pairs, the dot products run on v_dot2_f32_f16, and the
+// result, times the token's routing weight, is written as one partial row per
+// (token, slot).
 // combine kernel: y_t = sum_j partial(t, j) (j in slot order) + shared.
 #include "internal.h"
 #include "layout.h"
@@ -33,6 +35,7 @@ namespace moeq {
 namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against LDS bank conflicts
 
@@ -75,6 +78,9 @@ constexpr int kGateUpMinBlocks = MOEQ_GATEUP_MINBLOCKS, kDownMinBlocks = MOEQ_DO
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
                                          __builtin_bit_cast(bf16x2, b), c, false);
+}
+__device__ __forceinline__ float dot2h(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a), __builtin_bit_cast(f16x2, b), c, false);
 }
 
 // Which expert and tokens a slot covers.
@@ -140,11 +146,30 @@ __device__ __forceinline__ float block_dot(const uint32_t (&p)[16], const uint32
   return fmaf(ds, fmaf(-192.0f, X, acc), acc_out);
 }
 
-// block q's scale (binary16, 4 per unit in sc) times 2^(b-7)
-template <int B>
+// block q's scale (binary16, 4 per unit in sc) times 2^(b-7), or times
+// 2^(b-10) for the binary16 pairs (X = 3)
+template <int B, int X = 0>
 __device__ __forceinline__ float block_scale(u32x2 sc, int q) {
   const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
-  return half_to_float(s16) * (1.0f / (float)(1 << (7 - B)));
+  return half_to_float(s16) * (1.0f / (float)(1 << (7 + X - B)));
+}
+
+// The same contribution from binary16 code pairs and the token's 16 binary16
+// activation dwords at xl, prescaled by 2^-e; xf = (X of the prescaled
+// values, 2^e):  d 2^(b-10) 2^e (dot - 1536 X).
+__device__ __forceinline__ float block_dot_h(const uint32_t (&p)[16], const uint32_t* xl, float ds, float2 xf,
+                                             float acc_out) {
+  float acc = 0.0f;
+  const u32x4* x4 = reinterpret_cast<const u32x4*>(xl);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const u32x4 xv = x4[c];
+    acc = dot2h(p[4 * c + 0], xv.x, acc);
+    acc = dot2h(p[4 * c + 1], xv.y, acc);
+    acc = dot2h(p[4 * c + 2], xv.z, acc);
+    acc = dot2h(p[4 * c + 3], xv.w, acc);
+  }
+  return fmaf(ds * xf.y, fmaf(-1536.0f, xf.x, acc), acc_out);
 }
 
 template <int CTRL, int ROW_MASK = 0xF>
@@ -322,21 +347,21 @@ __device__ __forceinline__ void load_down(DownRows<BD>& b, const TensorDev& td, 
 
 template <int BD, int LPR, int TM>
 __device__ __forceinline__ void compute_down(const DownRows<BD>& b, bool active, const uint32_t* xu,
-                                             const float* su4, int xts, int sts, int lo, int mc, int u,
+                                             const float2* su4, int xts, int sts, int mc, int u,
                                              const Slot sl, int m0, int row, const DecodeArgs& a) {
   float o[TM];
 #pragma unroll
   for (int m = 0; m < TM; ++m) o[m] = 0.0f;
   if (active) {
-    const PairConsts pk = pair_consts();
+    const PairConsts pk = pair_consts_h();
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       uint32_t p[16];
-      block_pairs<BD>(b.w + q * BD, pk, p);
-      const float dd = block_scale<BD>(b.s, q);
+      block_pairs<BD, 3>(b.w + q * BD, pk, p);
+      const float dd = block_scale<BD, 3>(b.s, q);
 #pragma unroll
       for (int m = 0; m < TM; ++m)
-        if (m < mc) o[m] = block_dot<2>(p, xu + m * xts + 16 * q, lo, dd, su4[m * sts + q], o[m]);
+        if (m < mc) o[m] = block_dot_h(p, xu + m * xts + 16 * q, dd, su4[m * sts + q], o[m]);
     }
   }
 #pragma unroll
@@ -363,9 +388,9 @@ template <int BD, int LPR, int TM, int RW, int NBUF>
 __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot sl, const TensorDev& td,
                                           uint32_t* smem) {
   const int H = a.H, I = a.I, U = I / kUnit;
-  const int xts = 2 * U * kXStride, sts = U * 4, lo = U * kXStride;
+  const int xts = U * kXStride, sts = U * 4;  // per-token LDS strides (dwords, float pairs)
   uint32_t* xl = smem;
-  float* xs = reinterpret_cast<float*>(smem + TM * xts);
+  float2* xs = reinterpret_cast<float2*>(smem + TM * xts);
 
   constexpr int GPW = 64 / LPR;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -381,36 +406,41 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot sl, co
     for (int st = 0; st < NBUF; ++st)
       if (st < RW && uok && row0 + st * GPW < H) load_down(buf[st], td, row0 + st * GPW, U, u, I);
     __syncthreads();
-    // stage h rows as bfloat16 hi + lo pairs; block sums of hi + lo
+    // stage h rows as binary16: each block of 32 (four threads' chunks) is
+    // prescaled by 2^-e, e from its largest magnitude so that it lands in
+    // [2^14, 2^15) (no overflow, 11 significant bits at any scale; e >= -100
+    // keeps 2^-e finite for an all-zero block); per block (X, 2^e)
     for (int m = 0; m < mc; ++m) {
       const MOEQ_GLOBAL f32x4* src = gptr(reinterpret_cast<const f32x4*>(a.h + (size_t)(sl.base + m0 + m) * I));
       for (int q = threadIdx.x; q < I / 8; q += 256) {
         const f32x4 v0 = src[2 * q], v1 = src[2 * q + 1];
         const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-        uint32_t hi[4], lw[4];
+        float am = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) am = fmaxf(am, fabsf(f[i]));
+        am = fmaxf(am, __shfl_xor(am, 1, 64));
+        am = fmaxf(am, __shfl_xor(am, 2, 64));
+        const int e = max((int)((__float_as_uint(am) >> 23) & 0xFFu) - 141, -100);
+        const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
+        uint32_t hv[4];
         float s = 0.0f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const uint32_t h0 = bf16_rne(f[2 * i]), h1 = bf16_rne(f[2 * i + 1]);
-          const uint32_t l0 = bf16_rne(f[2 * i] - __uint_as_float(h0 << 16));
-          const uint32_t l1 = bf16_rne(f[2 * i + 1] - __uint_as_float(h1 << 16));
-          hi[i] = h0 | h1 << 16;
-          lw[i] = l0 | l1 << 16;
-          s += __uint_as_float(h0 << 16) + __uint_as_float(l0 << 16);
-          s += __uint_as_float(h1 << 16) + __uint_as_float(l1 << 16);
+          const _Float16 h0 = (_Float16)(f[2 * i] * sc), h1 = (_Float16)(f[2 * i + 1] * sc);
+          hv[i] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | (uint32_t)__builtin_bit_cast(uint16_t, h1) << 16;
+          s += (float)h0 + (float)h1;
         }
         s += __shfl_xor(s, 1, 64);
         s += __shfl_xor(s, 2, 64);
         const int uu = q >> 4, cq = q & 15;
         uint32_t* dst = xl + m * xts + uu * kXStride + cq * 4;
-        *reinterpret_cast<u32x4*>(dst) = u32x4{hi[0], hi[1], hi[2], hi[3]};
-        *reinterpret_cast<u32x4*>(dst + lo) = u32x4{lw[0], lw[1], lw[2], lw[3]};
-        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
+        *reinterpret_cast<u32x4*>(dst) = u32x4{hv[0], hv[1], hv[2], hv[3]};
+        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = make_float2(s, __builtin_amdgcn_ldexpf(1.0f, e));
       }
     }
     __syncthreads();
     const uint32_t* xu = xl + u * kXStride;
-    const float* su4 = xs + u * 4;
+    const float2* su4 = xs + u * 4;
 #pragma unroll 1
     for (int g0 = 0; g0 < RW; g0 += NBUF) {
       asm volatile("" ::: "memory");
@@ -418,7 +448,7 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot sl, co
       for (int b = 0; b < NBUF; ++b) {
         const int st = g0 + b;
         const int r = row0 + st * GPW;
-        if (r < H) compute_down<BD, LPR, TM>(buf[b], uok, xu, su4, xts, sts, lo, mc, u, sl, m0, r, a);
+        if (r < H) compute_down<BD, LPR, TM>(buf[b], uok, xu, su4, xts, sts, mc, u, sl, m0, r, a);
         const int rn = row0 + (st + NBUF) * GPW;
         if (st + NBUF < RW && uok && rn < H) load_down(buf[b], td, rn, U, u, I);
       }
@@ -936,7 +966,7 @@ template <int LPR, int TM>
 hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const int slots = a.S + a.max_active;
   const int U = a.I / kUnit;
-  const size_t lds = (size_t)TM * (2 * U * kXStride + U * 4) * 4;
+  const size_t lds = (size_t)TM * (U * kXStride + U * 8) * 4;
   constexpr int RW = TM == 1 ? kDownSteps : kDownStepsM, NB = TM == 1 ? kDownBuf : kDownBufM;
   const int rows_wg = 4 * (64 / LPR) * RW;
   dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);

@@ -213,7 +213,10 @@ def test_forward_v3_decode_batch1(gpu_lib, v3_decode):
     data, L = v3_decode
     for i in range(3):
         err = _forward_check(gpu_lib, data, L, 1, f"fwd-v3-b1-{i}", gpu_lib.MOEQ_PATH_AUTO)
-        assert err.max() < 1e-4        # float32 accumulation of exact products
+        # h enters the down products in binary16 (relative rounding 2^-11 per
+        # element after a power-of-two prescale per block), everything else
+        # is exact products with float32 accumulation: about 2e-4
+        assert err.max() < 1e-3
 
 
 def test_forward_v3_decode_batch16_sampled(gpu_lib, v3_decode):
@@ -322,7 +325,7 @@ def test_route_v3_k6(v3_k6, n):
 def test_forward_v3_k6_decode(gpu_lib, v3_k6):
     data, L = v3_k6
     err = _forward_check(gpu_lib, data, L, 1, "fwd-k6-b1", gpu_lib.MOEQ_PATH_AUTO)
-    assert err.max() < 1e-4
+    assert err.max() < 1e-3     # h in binary16 in the 2-4-bit down GEMV: about 2e-4
     _forward_check(gpu_lib, data, L, 16, "fwd-k6-b16", gpu_lib.MOEQ_PATH_AUTO, sample=[0, 9, 15])
 
 

@@ -136,7 +136,7 @@ def test_forward_tiny_wide(gpu_lib, tiny_wide, n, path):
 def test_forward_v3_shared_wide_decode(gpu_lib, v3_shared_wide):
     data, L = v3_shared_wide
     err = _forward_check(gpu_lib, data, L, 1, "fwd-v3-shw-b1", gpu_lib.MOEQ_PATH_AUTO)
-    assert err.max() < 1e-4
+    assert err.max() < 1e-3     # h in binary16 in the 2-4-bit down GEMV: about 2e-4
     _forward_check(gpu_lib, data, L, 16, "fwd-v3-shw-b16", gpu_lib.MOEQ_PATH_AUTO, sample=[0, 9, 15])
 
 
