@@ -41,10 +41,10 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 # the kernel sources the counters were taken on, identified by their sha256:
 # any change to them reports traffic as null until the counters are retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 127166563,
+    "bytes": 127679063,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "16261a16408dc56fd5d4c9d5f285a000ba8b72cd1c59000ac42e03813eed1059",
-        "paper_2509_25689_amd/csrc/layout.h": "af1ccceb1a620aa5674175609bd65aa23eebb15bfa73cde55efd58e296c12dfb",
+        "paper_2509_25689_amd/csrc/decode.hip": "8927dee43ce1f632bdd8b4e1e4d4da0563d21cd2448367c2e837f0b7b52cd6b1",
+        "paper_2509_25689_amd/csrc/layout.h": "dbc3980ea27988d4bf02afa1c0972c44e3b89fce29981c7bc725f8c626ae5203",
     },
 }
 

@@ -15,17 +15,22 @@
 // packed codes, see layout.h).  The weights of the wave's rows are loaded to
 // registers once and reused for every token of the expert's bucket, whose
 // activations are staged in LDS in chunks of TM tokens together with their
-// per-block sums.  The dot products run on v_dot2_f32_bf16 with float32
-// accumulation; the per-block scale and zero point are applied once per
-// block; the group reduces its partial sums with cross-lane shuffles in a
+// per-block sums.  The dot products accumulate in float32; the per-block
+// scale and zero point are applied once per block; the group reduces its partial sums with cross-lane shuffles in a
 // fixed order, so results are deterministic.
 //
 // gate/up kernel: writes h (float32) for every assignment in bucket order.
-// down kernel: the activations h are rounded to binary16 after a power-of-two
-// prescale per block of 32 (11 significant bits at any magnitude), the codes
-// unpacked to binary16 pairs, the dot products run on v_dot2_f32_f16, and the
-// result, times the token's routing weight, is written as one partial row per
-// (token, slot).
+// Arithmetic of the 2-4-bit kernels.  The one-token gate/up kernel and the
+// down kernel stage their activations (x, exactly, and h) in binary16 after a
+// power-of-two prescale per block of 32 (11 significant bits at any
+// magnitude), mask the code pairs out of the packed dwords as binary16
+// subnormals (layout.h) and run the dot products on v_dot2_f32_f16.  The
+// gate/up kernel for buckets of 2-64 tokens stages x in bfloat16 as given and
+// multiplies it with the codes unpacked to bfloat16 (v_dot2_f32_bf16): there,
+// converting four tokens' x per workgroup costs more than the cheaper unpack
+// saves.
+// down kernel: the result, times the token's routing weight, is written as
+// one partial row per (token, slot).
 // combine kernel: y_t = sum_j partial(t, j) (j in slot order) + shared.
 #include "internal.h"
 #include "layout.h"
@@ -146,30 +151,79 @@ __device__ __forceinline__ float block_dot(const uint32_t (&p)[16], const uint32
   return fmaf(ds, fmaf(-192.0f, X, acc), acc_out);
 }
 
-// block q's scale (binary16, 4 per unit in sc) times 2^(b-7), or times
-// 2^(b-10) for the binary16 pairs (X = 3)
-template <int B, int X = 0>
+// block q's scale (binary16, 4 per unit in sc) times 2^(b-7)
+template <int B>
 __device__ __forceinline__ float block_scale(u32x2 sc, int q) {
   const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
-  return half_to_float(s16) * (1.0f / (float)(1 << (7 + X - B)));
+  return half_to_float(s16) * (1.0f / (float)(1 << (7 - B)));
 }
 
-// The same contribution from binary16 code pairs and the token's 16 binary16
-// activation dwords at xl, prescaled by 2^-e; xf = (X of the prescaled
-// values, 2^e):  d 2^(b-10) 2^e (dot - 1536 X).
-__device__ __forceinline__ float block_dot_h(const uint32_t (&p)[16], const uint32_t* xl, float ds, float2 xf,
-                                             float acc_out) {
-  float acc = 0.0f;
+// block q's scale (binary16, 4 per unit in sc) times 2^24, for subnormal pairs
+__device__ __forceinline__ float block_scale_sub(u32x2 sc, int q) {
+  const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
+  return half_to_float(s16) * 16777216.0f;
+}
+
+// One block's contribution for one token from its subnormal code pairs p
+// (pair P = c * 2^(k_P - 24)), the token's 16 binary16 activation dwords at xl
+// (prescaled by 2^-e) and xf = (X, 2^e), X the sum of the staged values:
+//   d 2^e (2^24 sum_k 2^-k dot_k - z X) = (d 2^24) 2^e (dot - z 2^-24 X).
+template <int B>
+__device__ __forceinline__ float block_dot_sub(const uint32_t (&p)[16], const uint32_t* xl, float ds, float2 xf,
+                                               float acc_out) {
+  constexpr int NC = sub_classes<B>(), ST = sub_step<B>();
+  float acc[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) acc[c] = 0.0f;
   const u32x4* x4 = reinterpret_cast<const u32x4*>(xl);
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const u32x4 xv = x4[c];
-    acc = dot2h(p[4 * c + 0], xv.x, acc);
-    acc = dot2h(p[4 * c + 1], xv.y, acc);
-    acc = dot2h(p[4 * c + 2], xv.z, acc);
-    acc = dot2h(p[4 * c + 3], xv.w, acc);
+    acc[sub_shift<B>(4 * c + 0) / ST] = dot2h(p[4 * c + 0], xv.x, acc[sub_shift<B>(4 * c + 0) / ST]);
+    acc[sub_shift<B>(4 * c + 1) / ST] = dot2h(p[4 * c + 1], xv.y, acc[sub_shift<B>(4 * c + 1) / ST]);
+    acc[sub_shift<B>(4 * c + 2) / ST] = dot2h(p[4 * c + 2], xv.z, acc[sub_shift<B>(4 * c + 2) / ST]);
+    acc[sub_shift<B>(4 * c + 3) / ST] = dot2h(p[4 * c + 3], xv.w, acc[sub_shift<B>(4 * c + 3) / ST]);
   }
-  return fmaf(ds * xf.y, fmaf(-1536.0f, xf.x, acc), acc_out);
+  float dot = acc[NC - 1];
+#pragma unroll
+  for (int c = NC - 2; c >= 0; --c) dot = fmaf(dot, 1.0f / (float)(1 << ST), acc[c]);
+  constexpr float zs = (float)(1 << (B - 1)) * 0x1p-24f;
+  return fmaf(ds * xf.y, fmaf(-zs, xf.x, dot), acc_out);
+}
+
+// One thread's 16-byte piece (8 values) of a block of 32, whose four pieces
+// are held by four consecutive threads of one wave (all active): binary16
+// after the block's power-of-two prescale 2^-e, e from the block's largest
+// magnitude so that it lands in [2^14, 2^15) (no overflow, 11 significant
+// bits at any scale; e >= -100 keeps 2^-e finite for an all-zero block).
+// The piece goes to dst; the block's first thread (first) writes
+// (X, 2^e) to *xf, X the sum of the staged values.
+__device__ __forceinline__ void stage_piece(const float (&f)[8], uint32_t* dst, float2* xf, bool first) {
+  float am = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) am = fmaxf(am, fabsf(f[i]));
+  am = fmaxf(am, __shfl_xor(am, 1, 64));
+  am = fmaxf(am, __shfl_xor(am, 2, 64));
+  const int e = max((int)((__float_as_uint(am) >> 23) & 0xFFu) - 141, -100);
+  const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
+  uint32_t hv[4];
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const _Float16 h0 = (_Float16)(f[2 * i] * sc), h1 = (_Float16)(f[2 * i + 1] * sc);
+    hv[i] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | (uint32_t)__builtin_bit_cast(uint16_t, h1) << 16;
+    sum += (float)h0 + (float)h1;
+  }
+  sum += __shfl_xor(sum, 1, 64);
+  sum += __shfl_xor(sum, 2, 64);
+  *reinterpret_cast<u32x4*>(dst) = u32x4{hv[0], hv[1], hv[2], hv[3]};
+  if (first) *xf = make_float2(sum, __builtin_amdgcn_ldexpf(1.0f, e));
+}
+
+// the 8 bfloat16 values of a 16-byte piece as float
+__device__ __forceinline__ void bf16x8_to_f32(const u32x4 v, float (&f)[8]) {
+  f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+  f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
 }
 
 template <int CTRL, int ROW_MASK = 0xF>
@@ -353,15 +407,14 @@ __device__ __forceinline__ void compute_down(const DownRows<BD>& b, bool active,
 #pragma unroll
   for (int m = 0; m < TM; ++m) o[m] = 0.0f;
   if (active) {
-    const PairConsts pk = pair_consts_h();
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       uint32_t p[16];
-      block_pairs<BD, 3>(b.w + q * BD, pk, p);
-      const float dd = block_scale<BD, 3>(b.s, q);
+      block_pairs_sub<BD>(b.w + q * BD, p);
+      const float dd = block_scale_sub(b.s, q);
 #pragma unroll
       for (int m = 0; m < TM; ++m)
-        if (m < mc) o[m] = block_dot_h(p, xu + m * xts + 16 * q, dd, su4[m * sts + q], o[m]);
+        if (m < mc) o[m] = block_dot_sub<BD>(p, xu + m * xts + 16 * q, dd, su4[m * sts + q], o[m]);
     }
   }
 #pragma unroll
@@ -406,36 +459,14 @@ __device__ __forceinline__ void down_body(const DecodeArgs& a, const Slot sl, co
     for (int st = 0; st < NBUF; ++st)
       if (st < RW && uok && row0 + st * GPW < H) load_down(buf[st], td, row0 + st * GPW, U, u, I);
     __syncthreads();
-    // stage h rows as binary16: each block of 32 (four threads' chunks) is
-    // prescaled by 2^-e, e from its largest magnitude so that it lands in
-    // [2^14, 2^15) (no overflow, 11 significant bits at any scale; e >= -100
-    // keeps 2^-e finite for an all-zero block); per block (X, 2^e)
+    // stage h rows in binary16 with per-block prescales
     for (int m = 0; m < mc; ++m) {
       const MOEQ_GLOBAL f32x4* src = gptr(reinterpret_cast<const f32x4*>(a.h + (size_t)(sl.base + m0 + m) * I));
       for (int q = threadIdx.x; q < I / 8; q += 256) {
         const f32x4 v0 = src[2 * q], v1 = src[2 * q + 1];
         const float f[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-        float am = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) am = fmaxf(am, fabsf(f[i]));
-        am = fmaxf(am, __shfl_xor(am, 1, 64));
-        am = fmaxf(am, __shfl_xor(am, 2, 64));
-        const int e = max((int)((__float_as_uint(am) >> 23) & 0xFFu) - 141, -100);
-        const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
-        uint32_t hv[4];
-        float s = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const _Float16 h0 = (_Float16)(f[2 * i] * sc), h1 = (_Float16)(f[2 * i + 1] * sc);
-          hv[i] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | (uint32_t)__builtin_bit_cast(uint16_t, h1) << 16;
-          s += (float)h0 + (float)h1;
-        }
-        s += __shfl_xor(s, 1, 64);
-        s += __shfl_xor(s, 2, 64);
         const int uu = q >> 4, cq = q & 15;
-        uint32_t* dst = xl + m * xts + uu * kXStride + cq * 4;
-        *reinterpret_cast<u32x4*>(dst) = u32x4{hv[0], hv[1], hv[2], hv[3]};
-        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = make_float2(s, __builtin_amdgcn_ldexpf(1.0f, e));
+        stage_piece(f, xl + m * xts + uu * kXStride + cq * 4, xs + m * sts + uu * 4 + (cq >> 2), (cq & 3) == 0);
       }
     }
     __syncthreads();
@@ -526,13 +557,12 @@ __device__ __forceinline__ void load_unit_buf(UnitBuf<B>& b, const TensorDev& t,
 
 // d * sum (c - z) x over one 128-weight unit, for the token staged at xu / su4
 template <int B>
-__device__ __forceinline__ float unit_dot(const UnitBuf<B>& b, const uint32_t* xu, const float* su4, float acc) {
-  const PairConsts pk = pair_consts();
+__device__ __forceinline__ float unit_dot(const UnitBuf<B>& b, const uint32_t* xu, const float2* su4, float acc) {
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint32_t p[16];
-    block_pairs<B>(b.w + q * B, pk, p);
-    acc = block_dot<1>(p, xu + 16 * q, 0, block_scale<B>(b.s, q), su4[q], acc);
+    block_pairs_sub<B>(b.w + q * B, p);
+    acc = block_dot_sub<B>(p, xu + 16 * q, block_scale_sub(b.s, q), su4[q], acc);
   }
   return acc;
 }
@@ -554,7 +584,7 @@ __device__ __forceinline__ float half_sum8(float v) {
 #endif
 template <int B>
 __device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U, int j, int H, const uint32_t* xl,
-                                              const float* xs, const UnitBuf<B>& first) {
+                                              const float2* xs, const UnitBuf<B>& first) {
   constexpr int NB = MOEQ_GU1_DEPTH;
   const int UPL = (U + 7) / 8;
   UnitBuf<B> buf[NB];
@@ -579,21 +609,17 @@ __device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U
   return acc;
 }
 
-// the token's x with per-block sums (16-byte pieces, 4 per block) into LDS
-__device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uint32_t* xl, float* xs) {
+// the token's x into LDS in binary16 with per-block prescales (16-byte
+// pieces, 4 per block)
+__device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uint32_t* xl, float2* xs) {
   const int H = a.H;
   const int t = sl.shared >= 0 ? 0 : a.perm[sl.base] / a.k;
   const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
   for (int q = threadIdx.x; q < H / 8; q += 256) {
-    const u32x4 v = src[q];
-    float s = 0.0f;
-    s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
-    s += bf16_lo(v.z); s += bf16_hi(v.z); s += bf16_lo(v.w); s += bf16_hi(v.w);
-    s += __shfl_xor(s, 1, 64);
-    s += __shfl_xor(s, 2, 64);
+    float f[8];
+    bf16x8_to_f32(src[q], f);
     const int uu = q >> 4, cq = q & 15;
-    *reinterpret_cast<u32x4*>(xl + uu * kXStride + cq * 4) = v;
-    if ((cq & 3) == 0) xs[uu * 4 + (cq >> 2)] = s;
+    stage_piece(f, xl + uu * kXStride + cq * 4, xs + uu * 4 + (cq >> 2), (cq & 3) == 0);
   }
 }
 
@@ -601,7 +627,7 @@ __device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uin
 // latency overlaps the weight traffic.
 template <int BG, int BU>
 __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
-                                             const TensorDev& tu, uint32_t* xl, float* xs) {
+                                             const TensorDev& tu, uint32_t* xl, float2* xs) {
   const int H = a.H, I = a.I, U = H / kUnit;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = blockIdx.x * 16 + wave * 4 + (lane >> 4);
@@ -644,7 +670,7 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
   if (!tg.codes || !tu.codes) return;
   const int U = a.H / kUnit;
   uint32_t* xl = smem;
-  float* xs = reinterpret_cast<float*>(smem + U * kXStride);
+  float2* xs = reinterpret_cast<float2*>(smem + U * kXStride);
   switch (tg.bits * 8 + tu.bits) {
     case 2 * 8 + 2: gateup1_body<2, 2>(a, sl, tg, tu, xl, xs); break;
     case 2 * 8 + 3: gateup1_body<2, 3>(a, sl, tg, tu, xl, xs); break;
@@ -997,7 +1023,7 @@ hipError_t launch_down_tm(const DecodeArgs& a, hipStream_t s) {
 // gains nothing at 16 tokens and costs 3 % at 64).
 hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s) {
   const int U = a.H / kUnit;
-  const size_t lds = (size_t)(U * kXStride + U * 4) * 4;
+  const size_t lds = (size_t)(U * kXStride + U * 8) * 4;
   dim3 grid((a.I + 15) / 16, a.S + a.max_active);
   gateup1_kernel<<<grid, 256, lds, s>>>(a);
   const hipError_t e = hipGetLastError();

@@ -25,13 +25,6 @@
 //   sum_i (128 + 2^(7-b) c_i) x_i = 2^(7-b) * sum_i (c_i - z) x_i + 192 * sum_i x_i
 // with z = 2^(b-1), a block's contribution is
 //   d * 2^(b-7) * (dot - 192 * X),     X = sum of the block's 32 activations.
-//
-// For widths 2-4 the same pairs can also be built as binary16 values
-// 1024 + c * 2^(10-b) (exponent of 1024, code pair at the top of the 10-bit
-// mantissa: every shift 3 bits further left), for v_dot2_f32_f16; then
-//   sum_i (1024 + 2^(10-b) c_i) x_i = 2^(10-b) * sum_i (c_i - z) x_i + 1536 * X.
-// In both forms the offset is 2^b code steps, so the float32 accumulation
-// loses the same few bits to the cancellation.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -63,7 +56,7 @@ __device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t c) {
   return r;
 }
 
-// Masks and the bfloat16 (or binary16) base held in registers for and_or.
+// Masks and the bfloat16 base held in registers for and_or.
 struct PairConsts {
   uint32_t base, m2, m3, m4, b30, b31, b32;
 };
@@ -79,18 +72,6 @@ __device__ __forceinline__ PairConsts pair_consts() {
   asm("v_mov_b32 %0, 0x00400040" : "=v"(k.b32));
   return k;
 }
-// the binary16 form: base 1024.0, every mask 3 bits higher
-__device__ __forceinline__ PairConsts pair_consts_h() {
-  PairConsts k;
-  asm("v_mov_b32 %0, 0x64006400" : "=v"(k.base));
-  asm("v_mov_b32 %0, 0x03000300" : "=v"(k.m2));
-  asm("v_mov_b32 %0, 0x03800380" : "=v"(k.m3));
-  asm("v_mov_b32 %0, 0x03C003C0" : "=v"(k.m4));
-  asm("v_mov_b32 %0, 0x00800080" : "=v"(k.b30));
-  asm("v_mov_b32 %0, 0x01000100" : "=v"(k.b31));
-  asm("v_mov_b32 %0, 0x02000200" : "=v"(k.b32));
-  return k;
-}
 
 // shift a dword left (s > 0) or right (s < 0); s is a compile-time constant
 template <int S>
@@ -102,57 +83,60 @@ __device__ __forceinline__ uint32_t shl(uint32_t v) {
 }
 
 // The 16 code pairs of one block (P = pair index = weights 2P, 2P+1), each as
-// two bfloat16 values 128 + c * 2^(7-b) (X = 0, constants of pair_consts) or,
-// for b <= 4, two binary16 values 1024 + c * 2^(10-b) (X = 3, pair_consts_h).
-template <int X>
-__device__ __forceinline__ void pairs4(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
-  // mask m4: bits [3+X,7+X) of each half
+// two bfloat16 values 128 + c * 2^(7-b).
+template <int B>
+__device__ __forceinline__ void block_pairs(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]);
+
+template <>
+__device__ __forceinline__ void block_pairs<4>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m4: bits [3,7) of each half
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
-    p[4 * d + 0] = and_or(shl<3 + X>(w[d]), k.m4, k.base);
-    p[4 * d + 1] = and_or(shl<-1 + X>(w[d]), k.m4, k.base);
-    p[4 * d + 2] = and_or(shl<-5 + X>(w[d]), k.m4, k.base);
-    p[4 * d + 3] = and_or(shl<-9 + X>(w[d]), k.m4, k.base);
+    p[4 * d + 0] = and_or(shl<3>(w[d]), k.m4, k.base);
+    p[4 * d + 1] = and_or(shl<-1>(w[d]), k.m4, k.base);
+    p[4 * d + 2] = and_or(shl<-5>(w[d]), k.m4, k.base);
+    p[4 * d + 3] = and_or(shl<-9>(w[d]), k.m4, k.base);
   }
 }
 
-template <int X>
-__device__ __forceinline__ void pairs2(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
-  // mask m2: bits [5+X,7+X) of each half
+template <>
+__device__ __forceinline__ void block_pairs<2>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m2: bits [5,7) of each half
 #pragma unroll
   for (int d = 0; d < 2; ++d) {
-    p[8 * d + 0] = and_or(shl<5 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 1] = and_or(shl<3 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 2] = and_or(shl<1 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 3] = and_or(shl<-1 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 4] = and_or(shl<-3 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 5] = and_or(shl<-5 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 6] = and_or(shl<-7 + X>(w[d]), k.m2, k.base);
-    p[8 * d + 7] = and_or(shl<-9 + X>(w[d]), k.m2, k.base);
+    p[8 * d + 0] = and_or(shl<5>(w[d]), k.m2, k.base);
+    p[8 * d + 1] = and_or(shl<3>(w[d]), k.m2, k.base);
+    p[8 * d + 2] = and_or(shl<1>(w[d]), k.m2, k.base);
+    p[8 * d + 3] = and_or(shl<-1>(w[d]), k.m2, k.base);
+    p[8 * d + 4] = and_or(shl<-3>(w[d]), k.m2, k.base);
+    p[8 * d + 5] = and_or(shl<-5>(w[d]), k.m2, k.base);
+    p[8 * d + 6] = and_or(shl<-7>(w[d]), k.m2, k.base);
+    p[8 * d + 7] = and_or(shl<-9>(w[d]), k.m2, k.base);
   }
 }
 
-template <int X>
-__device__ __forceinline__ void pairs3(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
-  // mask m3: bits [4+X,7+X) of each half
+template <>
+__device__ __forceinline__ void block_pairs<3>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+  // mask m3: bits [4,7) of each half
 #pragma unroll
   for (int d = 0; d < 3; ++d) {
-    p[5 * d + 0] = and_or(shl<4 + X>(w[d]), k.m3, k.base);
-    p[5 * d + 1] = and_or(shl<1 + X>(w[d]), k.m3, k.base);
-    p[5 * d + 2] = and_or(shl<-2 + X>(w[d]), k.m3, k.base);
-    p[5 * d + 3] = and_or(shl<-5 + X>(w[d]), k.m3, k.base);
-    p[5 * d + 4] = and_or(shl<-8 + X>(w[d]), k.m3, k.base);
+    p[5 * d + 0] = and_or(shl<4>(w[d]), k.m3, k.base);
+    p[5 * d + 1] = and_or(shl<1>(w[d]), k.m3, k.base);
+    p[5 * d + 2] = and_or(shl<-2>(w[d]), k.m3, k.base);
+    p[5 * d + 3] = and_or(shl<-5>(w[d]), k.m3, k.base);
+    p[5 * d + 4] = and_or(shl<-8>(w[d]), k.m3, k.base);
   }
-  uint32_t t = and_or(shl<-11 + X>(w[0]), k.b30, k.base);
-  t = and_or(shl<-10 + X>(w[1]), k.b31, t);
-  p[15] = and_or(shl<-9 + X>(w[2]), k.b32, t);
+  uint32_t t = and_or(shl<-11>(w[0]), k.b30, k.base);
+  t = and_or(shl<-10>(w[1]), k.b31, t);
+  p[15] = and_or(shl<-9>(w[2]), k.b32, t);
 }
 
 // 5-bit blocks: dword d (0..4) holds pairs 3d + f (f = 0..2), the even code
 // of a pair at bits [5f, 5f+5) of the low half, the odd one in the high half;
 // pair 15 (codes 30, 31) is spread over bit 15 (code 30) and bit 31 (code 31)
 // of the five dwords, bit q of each code in dword q.
-__device__ __forceinline__ void pairs5(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+template <>
+__device__ __forceinline__ void block_pairs<5>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
   uint32_t m5, b0, b1;
   asm("v_mov_b32 %0, 0x007C007C" : "=v"(m5));  // bits [2,7) of each half
   asm("v_mov_b32 %0, 0x00040004" : "=v"(b0));
@@ -175,7 +159,8 @@ __device__ __forceinline__ void pairs5(const uint32_t* w, const PairConsts& k, u
 // [6f, 6f+6) of each half; pairs 12 + m (m = 0..3) keep their codes' low
 // four bits in bits [12,16) of each half of dword m and their top two bits in
 // bits [12 + 2(m&1), 14 + 2(m&1)) of each half of dword 4 + m/2.
-__device__ __forceinline__ void pairs6(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
+template <>
+__device__ __forceinline__ void block_pairs<6>(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
   uint32_t m6, lo4;
   asm("v_mov_b32 %0, 0x007E007E" : "=v"(m6));   // bits [1,7) of each half
   asm("v_mov_b32 %0, 0x001E001E" : "=v"(lo4));  // bits [1,5)
@@ -191,16 +176,68 @@ __device__ __forceinline__ void pairs6(const uint32_t* w, const PairConsts& k, u
   p[15] = and_or(shl<-9>(w[5]), k.m2, and_or(shl<-11>(w[3]), lo4, k.base));
 }
 
-template <int B, int X = 0>
-__device__ __forceinline__ void block_pairs(const uint32_t* w, const PairConsts& k, uint32_t (&p)[16]) {
-  static_assert(X == 0 || (X == 3 && B <= 4), "binary16 pairs exist for widths 2-4");
-  if constexpr (B == 2) pairs2<X>(w, k, p);
-  else if constexpr (B == 3) pairs3<X>(w, k, p);
-  else if constexpr (B == 4) pairs4<X>(w, k, p);
-  else if constexpr (B == 5) pairs5(w, k, p);
-  else {
-    static_assert(B == 6, "block_pairs: widths 2-6 (8 bits are two 4-bit planes)");
-    pairs6(w, k, p);
+// Code pairs as binary16 subnormals (widths 2-4, the 2-64-token and
+// one-token GEMVs): a dword masked so that only one code pair remains, at bit
+// offset k of each half, with the exponent fields zero, is two binary16 values
+// c * 2^(k - 24), exact, for v_dot2_f32_f16 (which keeps subnormal inputs).
+// The layout puts several pairs at offsets inside the 10-bit mantissa, so most
+// pairs need a mask alone and the others one shift per dword:
+//   b = 4: offsets 0, 4 of w and of w >> 8           (k = 0, 4, 0, 4)
+//   b = 3: offsets 0, 3, 6 of w and 0, 3 of w >> 9  (k = 0, 3, 6, 0, 3);
+//          the spare pair 15 is gathered at offset 0
+//   b = 2: offsets 0, 2, 4, 6, 8 of w and 0, 2, 4 of w >> 10
+// The dot of a block keeps one sum per offset k and scales the sums by 2^-k
+// when the block is done; there is no offset to cancel.
+template <int B>
+constexpr int sub_shift(int P) {  // k of pair P (0..15)
+  if constexpr (B == 4) return (P & 1) ? 4 : 0;
+  if constexpr (B == 3) return P == 15 ? 0 : (P % 5 == 1 || P % 5 == 4) ? 3 : (P % 5 == 2) ? 6 : 0;
+  return P % 8 < 5 ? 2 * (P % 8) : 2 * (P % 8 - 5);
+}
+template <int B>
+constexpr int sub_step() { return B == 4 ? 4 : B == 3 ? 3 : 2; }  // offsets are multiples of it
+template <int B>
+constexpr int sub_classes() { return B == 4 ? 2 : B == 3 ? 3 : 5; }  // distinct offsets
+
+template <int B>
+__device__ __forceinline__ void block_pairs_sub(const uint32_t* w, uint32_t (&p)[16]) {
+  static_assert(B >= 2 && B <= 4, "subnormal pairs exist for widths 2-4");
+  if constexpr (B == 4) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t s = w[d] >> 8;
+      p[4 * d + 0] = w[d] & 0x000F000Fu;
+      p[4 * d + 1] = w[d] & 0x00F000F0u;
+      p[4 * d + 2] = s & 0x000F000Fu;
+      p[4 * d + 3] = s & 0x00F000F0u;
+    }
+  } else if constexpr (B == 3) {
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+      const uint32_t s = w[d] >> 9;
+      p[5 * d + 0] = w[d] & 0x00070007u;
+      p[5 * d + 1] = w[d] & 0x00380038u;
+      p[5 * d + 2] = w[d] & 0x01C001C0u;
+      p[5 * d + 3] = s & 0x00070007u;
+      p[5 * d + 4] = s & 0x00380038u;
+    }
+    // bit q of codes 30 and 31 is bit 15 / 31 of dword q
+    uint32_t t = (w[0] >> 15) & 0x00010001u;
+    t = and_or(w[1] >> 14, 0x00020002u, t);
+    p[15] = and_or(w[2] >> 13, 0x00040004u, t);
+  } else {
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const uint32_t s = w[d] >> 10;
+      p[8 * d + 0] = w[d] & 0x00030003u;
+      p[8 * d + 1] = w[d] & 0x000C000Cu;
+      p[8 * d + 2] = w[d] & 0x00300030u;
+      p[8 * d + 3] = w[d] & 0x00C000C0u;
+      p[8 * d + 4] = w[d] & 0x03000300u;
+      p[8 * d + 5] = s & 0x00030003u;
+      p[8 * d + 6] = s & 0x000C000Cu;
+      p[8 * d + 7] = s & 0x00300030u;
+    }
   }
 }
 
