@@ -644,9 +644,11 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
 }
 
 // WIDE = false takes the tiles whose down tensor is 2-4 bits wide, WIDE = true
-// the 5, 6 and 8-bit ones
+// the 5, 6 and 8-bit ones.  Four waves per SIMD (128 registers): two
+// workgroups share a compute unit (2 x 80 KB of LDS) and overlap their K-step
+// chains.
 template <bool WIDE>
-__global__ __launch_bounds__(512, 1) void down_gemm8_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.H / BN;
   int mt, nt, slot, m0;
