@@ -218,13 +218,15 @@ __device__ __forceinline__ void interleave_hint() {
 
 // ---------------------------------------------------------------------------
 // h -> binary16 rows prescaled by 2^-e, e from the row's maximum |h|, so
-// that the largest value stays below 2^15 (one rounding to nearest even).
+// that the largest value lands in [2^14, 2^15) at any magnitude (one rounding
+// to nearest even; e >= -100 keeps 2^-e finite for an all-zero row).  The
+// down epilogue recomputes the same e.
 // One wave per row of h.
 __global__ __launch_bounds__(256) void h16_kernel(const float* h, const uint32_t* rowmax, int rows, int I,
                                                  uint16_t* h16) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= rows) return;
-  const int e = max(0, (int)((rowmax[row] >> 23) & 0xFFu) - 127 - 14);
+  const int e = max((int)((rowmax[row] >> 23) & 0xFFu) - 127 - 14, -100);
   const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
   const MOEQ_GLOBAL f32x4v* src = gptr(reinterpret_cast<const f32x4v*>(h + (size_t)row * I));
   MOEQ_GLOBAL u32x2* dst = (MOEQ_GLOBAL u32x2*)(h16 + (size_t)row * I);
@@ -622,7 +624,7 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
     for (int j = 0; j < 4; ++j) {
       const int rr = wm * 64 + 16 * i + (lane >> 4) * 4 + j;
       if (m0 + rr >= sl.M) continue;
-      const int e = max(0, (int)((rowmax[sl.base + m0 + rr] >> 23) & 0xFFu) - 127 - 14);
+      const int e = max((int)((rowmax[sl.base + m0 + rr] >> 23) & 0xFFu) - 127 - 14, -100);
       int prow;
       float wv;
       if (sl.shared >= 0) {

@@ -100,9 +100,10 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
                                  float* w_g, int32_t* idx_s) {
   const int lane = threadIdx.x & 63;
   if (rp.x) {
-    // binary exponent prescale for half precision: x * 2^-e < 2^15, and the
-    // prescaled binary16 copy of the row (exact unless it falls below the
-    // binary16 normal range, then rounded to nearest even)
+    // binary exponent prescale for half precision: e puts the row's largest
+    // |x| in [2^14, 2^15) (e >= -100 keeps 2^-e finite for an all-zero row),
+    // and the prescaled binary16 copy of the row (exact unless a value lies
+    // more than 2^28 below the largest, then rounded to nearest even)
     const MOEQ_GLOBAL u32x4* xr = gptr(reinterpret_cast<const u32x4*>(rp.x + (size_t)t * rp.H));
     const int C = rp.H / 8;
     uint32_t mx = 0;
@@ -114,7 +115,7 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
-    const int e = max(0, (int)((mx >> 7) & 0xFFu) - 127 - 14);
+    const int e = max((int)((mx >> 7) & 0xFFu) - 127 - 14, -100);
     if (lane == 0) rp.xexp[t] = e;
     const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
     MOEQ_GLOBAL u32x4* hr = (MOEQ_GLOBAL u32x4*)(rp.x16 + (size_t)t * rp.H);

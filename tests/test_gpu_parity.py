@@ -368,3 +368,38 @@ def test_route_regrouped(regrouped, n):
 def test_forward_regrouped(gpu_lib, regrouped, path):
     data, L = regrouped
     _forward_check(gpu_lib, data, L, 24, "fwd-regroup", path, sample=[0, 11, 23])
+
+
+def _scaled_bits(bits, s):
+    """bfloat16 bit patterns times 2^s, exactly (the exponent field moves;
+    the draws stay far from the bfloat16 range limits)."""
+    f = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64) * 2.0 ** s
+    out = (f.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal((out.astype(np.uint32) << 16).view(np.float32).astype(np.float64), f)
+    return out
+
+
+@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("s", [-20, -8, 6, 12])
+def test_forward_activation_magnitudes(gpu_lib, tiny_mixed, path, s):
+    """x scaled by 2^s, far from N(0, 1): the activations enter the GEMVs and
+    GEMMs in binary16 after power-of-two prescales (per block of 32 on the
+    decode path, per token / per h row on the grouped-GEMM path), and h
+    reaches about 2^(2s) times its usual size.  The layer must stay within
+    the tolerance at every scale, on both paths and all 2/3/4-bit widths."""
+    data, L = tiny_mixed
+    shape = data.shape
+    n = 3 if path == 1 else 40
+    bits = _scaled_bits(synth.activations(n, shape.hidden, "fwd-mag", f"s{s}", path), s)
+    logits = synth.normal_logits(n, shape.n_experts, "fwd-mag", f"s{s}", path)
+    L.set_path(path)
+    try:
+        y = L.forward(_dev(bits.view(np.int16), torch.bfloat16), _dev(logits))
+        torch.cuda.synchronize()
+    finally:
+        L.set_path(gpu_lib.MOEQ_PATH_AUTO)
+    idx, w = _route_oracle(shape, data.mask, logits)
+    ref = layers.oracle_forward(data, bits, idx, w)
+    assert np.all(np.isfinite(y.cpu().numpy()))
+    err = moe.token_errors(y.cpu().numpy(), ref)
+    assert err.max() <= TOL, (s, path, err.max())
