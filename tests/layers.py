@@ -65,3 +65,12 @@ def oracle_forward(data, x_bits, idx, w):
         return cache[e]
     shared = [data.dequant("s", s) for s in range(data.shape.n_shared)]
     return moe.moe_forward(x_bits, idx, w, routed, shared)
+
+
+def scaled_bits(bits, s):
+    """bfloat16 bit patterns times 2^s, exactly (the exponent field moves;
+    the draws stay far from the bfloat16 range limits)."""
+    f = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64) * 2.0 ** s
+    out = (f.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal((out.astype(np.uint32) << 16).view(np.float32).astype(np.float64), f)
+    return out

@@ -370,14 +370,6 @@ def test_forward_regrouped(gpu_lib, regrouped, path):
     _forward_check(gpu_lib, data, L, 24, "fwd-regroup", path, sample=[0, 11, 23])
 
 
-def _scaled_bits(bits, s):
-    """bfloat16 bit patterns times 2^s, exactly (the exponent field moves;
-    the draws stay far from the bfloat16 range limits)."""
-    f = (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64) * 2.0 ** s
-    out = (f.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
-    assert np.array_equal((out.astype(np.uint32) << 16).view(np.float32).astype(np.float64), f)
-    return out
-
 
 @pytest.mark.parametrize("path", [1, 2])
 @pytest.mark.parametrize("s", [-20, -8, 6, 12])
@@ -390,7 +382,7 @@ def test_forward_activation_magnitudes(gpu_lib, tiny_mixed, path, s):
     data, L = tiny_mixed
     shape = data.shape
     n = 3 if path == 1 else 40
-    bits = _scaled_bits(synth.activations(n, shape.hidden, "fwd-mag", f"s{s}", path), s)
+    bits = layers.scaled_bits(synth.activations(n, shape.hidden, "fwd-mag", f"s{s}", path), s)
     logits = synth.normal_logits(n, shape.n_experts, "fwd-mag", f"s{s}", path)
     L.set_path(path)
     try:

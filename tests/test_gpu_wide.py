@@ -154,3 +154,30 @@ def test_forward_v3_routed_wide(gpu_lib, v3_routed_wide, n, path):
     data, L = v3_routed_wide
     sample = None if n == 1 else [0, n // 2, n - 1]
     _forward_check(gpu_lib, data, L, n, "fwd-v3-rw", path, sample=sample)
+
+
+@pytest.mark.parametrize("path", [1, 2])
+@pytest.mark.parametrize("s", [-20, 12])
+def test_forward_wide_activation_magnitudes(gpu_lib, tiny_wide, path, s):
+    """x scaled by 2^s on the layer with every width of {2,3,4,5,6,8}: the
+    5/6/8-bit kernels (bfloat16 activations, h as hi + lo parts on the decode
+    path; the same binary16 prescales as the 2-4-bit GEMMs on the grouped-GEMM
+    path) stay within the tolerance far from N(0, 1) activations."""
+    data, L = tiny_wide
+    shape = data.shape
+    n = 3 if path == 1 else 40
+    bits = layers.scaled_bits(synth.activations(n, shape.hidden, "fwd-wide-mag", f"s{s}", path), s)
+    logits = synth.normal_logits(n, shape.n_experts, "fwd-wide-mag", f"s{s}", path)
+    L.set_path(path)
+    try:
+        y = L.forward(_dev(bits.view(np.int16), torch.bfloat16), _dev(logits))
+        torch.cuda.synchronize()
+    finally:
+        L.set_path(gpu_lib.MOEQ_PATH_AUTO)
+    idx, w = router.route(logits, data.mask, n_group=shape.n_group, topk_group=shape.topk_group,
+                          top_k=shape.top_k, group_topn=shape.group_topn, norm_topk=shape.norm_topk,
+                          routed_scale=shape.routed_scale)
+    ref = layers.oracle_forward(data, bits, idx, w)
+    assert np.all(np.isfinite(y.cpu().numpy()))
+    err = moe.token_errors(y.cpu().numpy(), ref)
+    assert err.max() <= TOL, (s, path, err.max())
