@@ -161,6 +161,14 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
  * joined back into `stream` by another before the forward's last kernels, so
  * all of it completes in `stream` order (a capture records the fork and
  * join).  Deterministic: identical inputs give bitwise-identical y.
+ * Arithmetic: code values are exact; products accumulate in float32.  x and
+ * the SwiGLU activations h enter the products in binary16 after power-of-two
+ * prescales that put the largest magnitude of each group in [2^14, 2^15).
+ * The groups are blocks of 32 on the decode path, except x of the buckets of
+ * 2-64 tokens, which stays bfloat16.  On the prefill path they are tokens for
+ * x and rows for h.  x is therefore exact; h is rounded once to 11
+ * significant bits.  The per-token error max|y - y_exact| / max|y_exact| is
+ * about 2e-4 on synthetic layers.
  * Errors: INVALID_ARG, CAPACITY (n_tokens > max_tokens), DEVICE. */
 moeq_status moeq_forward(moeq_layer* layer, const void* x, const float* logits,
                          int32_t n_tokens, float* y, void* stream);
