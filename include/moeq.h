@@ -166,8 +166,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
  * prescales that put the largest magnitude of each group in [2^14, 2^15).
  * The groups are blocks of 32 on the decode path, except x of the buckets of
  * 2-64 tokens, which stays bfloat16.  On the prefill path they are tokens for
- * x and rows for h.  x is therefore exact; h is rounded once to 11
- * significant bits.  The per-token error max|y - y_exact| / max|y_exact| is
+ * x and rows for h.  x is therefore exact, except values more than 2^28
+ * below their group's largest.  h is rounded once to 11 significant bits.  The per-token error max|y - y_exact| / max|y_exact| is
  * about 2e-4 on synthetic layers.
  * Errors: INVALID_ARG, CAPACITY (n_tokens > max_tokens), DEVICE. */
 moeq_status moeq_forward(moeq_layer* layer, const void* x, const float* logits,
