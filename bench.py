@@ -65,13 +65,15 @@ def gateup_traffic():
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=6400)
-    p.add_argument("--warmup", type=int, default=640)
+    p.add_argument("--steps", type=int, default=2560, help="timed batch-1 forwards (exactly this many)")
+    p.add_argument("--warmup", type=int, default=256, help="untimed forwards before the timed ones")
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--layers", type=int, default=4, help="independently seeded layers rotated per step")
     p.add_argument("--sets", type=int, default=64, help="input sets (x, logits) per layer")
     p.add_argument("--kernel-steps", type=int, default=256, help="eager forwards timed per stage")
-    p.add_argument("--cpu-steps", type=int, default=2, help="oracle forwards in the CPU baseline (0 = skip)")
+    p.add_argument("--cpu-steps", type=int, default=3,
+                   help="oracle forwards per timed group in the CPU baseline; the value is the median of 3 "
+                        "groups (0 = skip)")
     p.add_argument("--prefill-steps", type=int, default=10, help="2048-token prefill forwards timed (0 = skip)")
     p.add_argument("--b16-steps", type=int, default=2560, help="16-token decode steps timed (0 = skip)")
     p.add_argument("--k6-steps", type=int, default=2560,
@@ -80,11 +82,16 @@ def parse():
                    help="batch-1 decode steps timed with logits from the router gate (0 = skip)")
     p.add_argument("--wide-steps", type=int, default=2560,
                    help="batch-1 decode steps timed with a 6-bit shared expert (0 = skip)")
-    p.add_argument("--mode", choices=("all", "decode", "prefill", "copy", "stack", "sweep"), default="all",
+    p.add_argument("--stack-steps", type=int, default=580,
+                   help="timed layer forwards of the 58-layer stack leg (0 = skip)")
+    p.add_argument("--peak-reps", type=int, default=5, help="timed launches of each peak probe (0 = skip)")
+    p.add_argument("--mode", choices=("all", "decode", "prefill", "copy", "stack", "sweep", "peaks"),
+                   default="all",
                    help="all: batch-1 decode line with 16-token, prefill and CPU legs; decode / prefill: "
                         "one leg only (for profiling); copy: a plain 1 GiB device copy whose HBM counters "
                         "calibrate the profiler's byte counts; stack: 58 independent layers; sweep: kept "
-                        "experts x widths x tokens x routing on the decode path")
+                        "experts x widths x tokens x routing on the decode path; peaks: measured streaming-read "
+                        "and MFMA rates")
     return p.parse_args()
 
 
@@ -128,6 +135,14 @@ class Hip:
 
     def destroy(self, e):
         self.lib.hipEventDestroy(e)
+
+    def graph_upload(self, graph_exec, stream):
+        """Upload an instantiated graph before it is timed, so that its first
+        replay does not carry the upload."""
+        fn = self.lib.hipGraphUpload
+        fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        fn.restype = ctypes.c_int
+        assert fn(graph_exec, stream) == 0
 
 
 def build_layer(torch, moeq, synth, shape, plan, key, max_tokens):
@@ -221,6 +236,43 @@ def copy_calibration(torch, hip, nbytes=1 << 30, reps=4):
             "GBps_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}
 
 
+def peaks_leg(torch, hip, reps, read_bytes=4 << 30, mfma_wgs=2048, mfma_iters=4000):
+    """Measured roofline denominators on this GPU: a streaming read of
+    read_bytes (larger than every cache) with 16-byte coalesced loads, and a
+    register-only binary16 MFMA loop over 8 workgroups of 4 waves per compute
+    unit.  Median and best of `reps` timed launches after two untimed ones."""
+    import statistics
+    from paper_2509_25689_amd import peaks
+    lib = peaks.load()
+    stream = torch.cuda.current_stream().cuda_stream
+    src = torch.randint(0, 1 << 30, (read_bytes // 4,), dtype=torch.int32, device="cuda")
+    sink = torch.empty(lib.moeq_peaks_read_workgroups(read_bytes), dtype=torch.int32, device="cuda")
+    fsink = torch.empty(mfma_wgs * 256, dtype=torch.float32, device="cuda")
+    read_ms, mfma_ms = [], []
+    for i in range(reps + 2):
+        e = [hip.event() for _ in range(4)]
+        hip.record(e[0], stream)
+        assert lib.moeq_peaks_stream_read(src.data_ptr(), read_bytes, sink.data_ptr(), stream) == 0
+        hip.record(e[1], stream)
+        hip.record(e[2], stream)
+        assert lib.moeq_peaks_mfma(mfma_wgs, mfma_iters, fsink.data_ptr(), stream) == 0
+        hip.record(e[3], stream)
+        torch.cuda.synchronize()
+        if i >= 2:
+            read_ms.append(hip.elapsed_ms(e[0], e[1]))
+            mfma_ms.append(hip.elapsed_ms(e[2], e[3]))
+        for x in e:
+            hip.destroy(x)
+    del src
+    flops = lib.moeq_peaks_mfma_flops(mfma_wgs, mfma_iters)
+    gbps = [read_bytes / (m * 1e-3) / 1e9 for m in read_ms]
+    tflops = [flops / (m * 1e-3) / 1e12 for m in mfma_ms]
+    return {"stream_read_GBps_median": round(statistics.median(gbps), 1), "stream_read_GBps_best": round(max(gbps), 1),
+            "stream_read_bytes": read_bytes,
+            "mfma_f16_TFLOPs_median": round(statistics.median(tflops), 1), "mfma_f16_TFLOPs_best": round(max(tflops), 1),
+            "mfma_workgroups": mfma_wgs, "mfma_iters": mfma_iters, "reps": reps}
+
+
 def cpu_baseline(shape, steps, batch):
     """The oracle, as it stands, on `steps` forwards of the same workload shape.
 
@@ -246,8 +298,8 @@ def cpu_baseline(shape, steps, batch):
         codes, scales = synth.random_packed(rows, K, bits, key, kind, e, p)
         return dict(bits=bits, codes=codes, scales=scales)
 
-    xs = [synth.activations(batch, shape.hidden, key, "x", i) for i in range(steps)]
-    lgs = [synth.normal_logits(batch, shape.n_experts, key, "l", i) for i in range(steps)]
+    xs = [synth.activations(batch, shape.hidden, key, "x", i) for i in range(3 * steps)]
+    lgs = [synth.normal_logits(batch, shape.n_experts, key, "l", i) for i in range(3 * steps)]
     # untimed: materialise the packed tensors the sample touches
     need = set()
     for lg in lgs:
@@ -258,42 +310,46 @@ def cpu_baseline(shape, steps, batch):
     shared_t = [tuple(packed("s", s, p) for p in range(3)) for s in range(shape.n_shared)]
     Ks = [shape.rows_cols(p)[1] for p in range(3)]
 
-    t0 = time.perf_counter()
-    for i in range(steps):
+    def forward(i):
         idx, w = router.route(lgs[i], mask, n_group=shape.n_group, topk_group=shape.topk_group,
                               top_k=shape.top_k, routed_scale=shape.routed_scale)
         bucket.bucket(idx, shape.n_experts)
         shared = [tuple(moe.dequant_tensor(t, K) for t, K in zip(tr, Ks)) for tr in shared_t]
         moe.moe_forward(xs[i], idx, w,
                         lambda e: tuple(moe.dequant_tensor(t, K) for t, K in zip(store[e], Ks)), shared)
-    dt = time.perf_counter() - t0
+
+    group_s = []
+    for g in range(3):
+        t0 = time.perf_counter()
+        for i in range(g * steps, (g + 1) * steps):
+            forward(i)
+        group_s.append(time.perf_counter() - t0)
+    med = sorted(group_s)[1]
     cores = len(os.sched_getaffinity(0))
-    return {"value": steps * batch / dt, "unit": "tokens/s",
+    return {"value": steps * batch / med, "unit": "tokens/s",
             "cores": blas_threads if blas_threads else cores, "kind": "oracle",
-            "sample": f"{steps} forwards of {batch} token(s), same V3 shape and bit plan, "
-                      f"random packed codes; {dt:.1f} s; host cores visible {cores}"}
+            "sample": f"median of 3 groups of {steps} forwards of {batch} token(s) each (group times "
+                      f"{', '.join(f'{t:.2f}' for t in group_s)} s), same V3 shape and bit plan, random packed "
+                      f"codes; host cores visible {cores}"}
 
 
 def random_layer(torch, moeq, synth, shape, plan, key, max_tokens):
-    """A layer whose codes are uniform random bytes and whose scales are near the
-    block quantizer's typical d for N(0, 0.02) weights (about 2.2 sigma /
-    qmax, times U(0.8, 1.2)), generated directly on the GPU: used where
-    quantizing real draws would take too long (the 58-layer stack)."""
+    """A layer whose codes are uniform random bytes and whose scales are
+    spread around the block quantizer's typical d for N(0, 0.02) weights
+    (synth.device_random_packed, keyed per tensor), generated directly on the
+    GPU: used where quantizing real draws would take too long (the 58-layer
+    stack, the sweep)."""
     mask = synth.expert_mask(shape, key)
     bits_r, bits_s = synth.bit_plan(shape, plan, key)
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(synth.seed_int("bench-rand", key))
 
-    def tensor(bits, p):
+    def tensor(kind, e, p, bits):
         rows, K = shape.rows_cols(p)
-        codes = torch.randint(0, 256, (rows, K * bits // 8), generator=gen, device="cuda", dtype=torch.uint8)
-        qmax = (1 << (bits - 1)) - 1
-        d = (0.02 * 2.2 / qmax) * (0.8 + 0.4 * torch.rand((rows, K // 32), generator=gen, device="cuda"))
-        return dict(bits=bits, codes=codes, scales=d.to(torch.float16).view(torch.int16))
+        codes, scales = synth.device_random_packed(torch, rows, K, bits, key, kind, e, p)
+        return dict(bits=bits, codes=codes, scales=scales)
 
-    routed = {int(e): tuple(tensor(int(bits_r[e, p]), p) for p in range(3))
+    routed = {int(e): tuple(tensor("r", e, p, int(bits_r[e, p])) for p in range(3))
               for e in range(shape.n_experts) if mask[e]}
-    shared = [tuple(tensor(int(bits_s[s, p]), p) for p in range(3)) for s in range(shape.n_shared)]
+    shared = [tuple(tensor("s", s, p, int(bits_s[s, p])) for p in range(3)) for s in range(shape.n_shared)]
     torch.cuda.synchronize()
     layer = moeq.Layer(shape, mask, routed, shared, max_tokens=max_tokens, device_weights=True)
     del routed, shared
@@ -354,36 +410,39 @@ def decode_leg(torch, np, moeq, synth, hip, shape, layers, B, R, steps, warmup, 
         moeq.moeq_forward(layer.handle, xs[i].data_ptr(), 0 if gate else lgs[i].data_ptr(), B,
                           ys[i % NL].data_ptr(), stream)
 
+    # one eager forward per layer before any capture (first-use set-up of
+    # the library's kernels happens outside a graph)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        for i in range(n_sets):
+        for i in range(NL):
             run_step(i, side.cuda_stream)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
 
-    def capture(count):
+    def capture(order):
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             st = torch.cuda.current_stream().cuda_stream
-            for i in range(count):
+            for i in order:
                 run_step(i % n_sets, st)
         return g
 
-    full = capture(n_sets)
-    reps = max(1, steps // n_sets)
-    steps = reps * n_sets
-    for _ in range(max(1, warmup // n_sets)):
-        full.replay()
+    # warm-up: `warmup` forwards, then exactly `steps` timed forwards that
+    # continue the rotation (forward i of the timed run uses set warmup + i)
+    if warmup > 0:
+        capture(list(range(warmup))).replay()
+    timed = capture([(warmup + i) % n_sets for i in range(steps)])
+    hip.graph_upload(timed.raw_cuda_graph_exec(), torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0.record()
-    for _ in range(reps):
-        full.replay()
+    timed.replay()
     t1.record()
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_per_step = total_ms / steps
+    del timed
 
     # per-stage kernel durations: timing-only events recorded by the library
     # between its kernels, over kernel_steps eager forwards
@@ -492,8 +551,12 @@ def main():
               flush=True)
         return
     if args.mode == "stack":
-        print(json.dumps({"stack": stack_leg(torch, np, moeq, synth, hip, args.steps)}), flush=True)
+        print(json.dumps({"stack": stack_leg(torch, np, moeq, synth, hip, args.stack_steps)}), flush=True)
         return
+    if args.mode == "peaks":
+        print(json.dumps({"peaks": peaks_leg(torch, hip, max(1, args.peak_reps))}), flush=True)
+        return
+    peaks = peaks_leg(torch, hip, args.peak_reps) if args.mode == "all" and args.peak_reps > 0 else None
     if args.mode == "sweep":
         print(json.dumps({"sweep": sweep_leg(torch, np, moeq, synth, hip, args.steps)}), flush=True)
         return
@@ -515,7 +578,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f16",
+        "arithmetic": "binary16 operands (bf16 x exact after a power-of-two prescale per block of 32; exact "
+                      "code values; SwiGLU h rounded once to binary16 after a power-of-two prescale per block), "
+                      "float32 accumulation; router scores float64 rounded once to float32",
         "data": "synthetic",
         "config": {
             "workload": f"DeepSeek-V3-shape MoE layer decode, batch {B}: hidden 7168, inter 2048, "
@@ -537,6 +603,12 @@ def main():
                      "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": gateup_traffic() if B == 1 else None,
                      "bytes_per_launch": int(r["gu_launch_bytes"])},
     }
+    if peaks:
+        meas = peaks["stream_read_GBps_median"]
+        out["peaks_measured"] = peaks
+        out["roofline"]["peak_measured"] = meas
+        out["roofline"]["frac_of_measured_peak"] = round(r["gu_GBps"] / meas, 4)
+        out["hbm_frac_of_measured_read"] = round(r["GBps"] / meas, 4)
     if args.mode == "all" and args.gate_steps > 0:
         # the same layers, logits computed in the forward by the router gate x W_r^T
         rg = decode_leg(torch, np, moeq, synth, hip, shape, layers, 1, R, args.gate_steps, 64, 64, "bench-gate",
@@ -584,6 +656,14 @@ def main():
             L.close()
     if args.mode == "all" and args.prefill_steps > 0:
         out["prefill"] = prefill_bench(torch, np, moeq, synth, hip, args.prefill_steps)
+        if peaks:
+            m = peaks["mfma_f16_TFLOPs_median"]
+            out["prefill"]["mfma_peak_measured_TFLOPs"] = m
+            out["prefill"]["mfma_frac_of_measured_peak"] = round(out["prefill"]["tflops"] / m, 4)
+    if args.mode == "all" and args.stack_steps > 0:
+        out["stack"] = stack_leg(torch, np, moeq, synth, hip, args.stack_steps)
+        if peaks:
+            out["stack"]["frac_of_measured_read"] = round(out["stack"]["GBps"] / peaks["stream_read_GBps_median"], 4)
     if args.mode == "all" and args.cpu_steps > 0:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_steps, B)
     print(json.dumps(out), flush=True)

@@ -136,7 +136,9 @@ typedef struct {
  * must hold at least top_k kept experts (with regroup: topk_group groups of
  * kept / n_group experts must hold top_k) (else INVALID_ARG).
  * All weight data is copied and re-laid-out on the device; the caller may
- * free its buffers when this returns.  Synchronizes the device.
+ * free its buffers when this returns.  The copies and the re-layout run on
+ * the null stream, which create waits for before it returns (DEVICE weights
+ * must be complete in null-stream order).
  * Errors: INVALID_ARG (including widths outside {2,3,4,5,6,8}), UNSUPPORTED
  * (shapes), OUT_OF_MEMORY, DEVICE;
  * on error *out is set to NULL and nothing is leaked. */
@@ -156,11 +158,11 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
  * Borrowed pointers must stay valid until the stream work completes.  No
  * allocation, no memset, no host synchronization: safe to capture in a HIP
  * graph.  For 2..64 tokens on the decode path, and on the prefill path,
- * part of the work runs on a second stream the layer owns, ordered after
- * `stream` by an event and
- * joined back into `stream` by another before the forward's last kernels, so
- * all of it completes in `stream` order (a capture records the fork and
- * join).  Deterministic: identical inputs give bitwise-identical y.
+ * part of the work runs on an auxiliary stream (one per device, shared by
+ * the device's layers, default priority), ordered after `stream` by an event
+ * of the layer and joined back into `stream` by another before the forward's
+ * last kernels, so all of it completes in `stream` order (a capture records
+ * the fork and join).  Deterministic: identical inputs give bitwise-identical y.
  * Arithmetic: code values are exact; products accumulate in float32.  x and
  * the SwiGLU activations h enter the products in binary16 after power-of-two
  * prescales that put the largest magnitude of each group in [2^14, 2^15).
@@ -199,7 +201,8 @@ moeq_status moeq_set_router_weight(moeq_layer* layer, const float* w, int32_t lo
 moeq_status moeq_router_logits(moeq_layer* layer, const void* x, int32_t n_tokens, float* logits,
                                void* stream);
 
-/* Frees everything the layer owns after synchronizing the device.  NULL-safe. */
+/* Frees everything the layer owns after synchronizing the device (the handle
+ * does not know every stream its calls ran on).  NULL-safe. */
 void moeq_destroy(moeq_layer* layer);
 
 /* Text for the calling thread's last failing call ("" if none). */
@@ -233,6 +236,26 @@ moeq_status moeq_bucket(moeq_layer* layer, const int32_t* idx, int32_t n_tokens,
  *   out      DEVICE float32 [rows x K] */
 moeq_status moeq_dequant(moeq_layer* layer, int32_t expert, int32_t proj, float* out,
                          void* stream);
+
+/* Diagnostic: one stored tensor through one of the decoders the products use
+ * (each width's code unpacking of Section 3.3's per-tensor formats), so each
+ * can be compared with the format's definition d * (c - 2^(b-1)).
+ *   decoder  MOEQ_DECODER_EXACT: the bfloat16-form unpacking (the matrix-vector
+ *            kernels for buckets of 2-64 tokens and for 5/6/8-bit tensors),
+ *            out = float32 [rows x K], exact (this is moeq_dequant);
+ *            MOEQ_DECODER_GEMV_SUBNORMAL: the binary16-subnormal code pairs
+ *            (the one-token gate/up and the 2-4-bit down matrix-vector
+ *            kernels), each code rebuilt from its pair value c * 2^(k-24),
+ *            out = float32 [rows x K], exact; widths 2-4 only (else
+ *            UNSUPPORTED);
+ *            MOEQ_DECODER_GEMM_F16: the grouped GEMMs' weight decoder, out =
+ *            binary16 bit patterns (uint16) [rows x K] of d * (c - 2^(b-1))
+ *            rounded once to nearest even, the value the matrix cores use
+ *   expert, proj as for moeq_dequant; out DEVICE
+ * Errors: INVALID_ARG, UNSUPPORTED, DEVICE. */
+enum { MOEQ_DECODER_EXACT = 0, MOEQ_DECODER_GEMV_SUBNORMAL = 1, MOEQ_DECODER_GEMM_F16 = 2 };
+moeq_status moeq_dequant_as(moeq_layer* layer, int32_t expert, int32_t proj, int32_t decoder, void* out,
+                            void* stream);
 
 /* Quantize a float32 matrix into the canonical format (Section 3.3's
  * "quantize to the base precision" step, in this library's block format):

@@ -145,6 +145,22 @@ def random_packed(rows, K, bits, *key):
     return codes, scales.view(np.uint16)
 
 
+def device_random_packed(torch, rows, K, bits, *key, device="cuda"):
+    """``random_packed``'s distribution drawn on a GPU with torch's seeded
+    generator, for layers too large to draw on the host (the 58-layer stack,
+    the pruning/precision sweep): (codes uint8 ``[rows, K*bits/8]``, scales as
+    int16 binary16 bit patterns ``[rows, K/32]``), both device tensors.  The
+    same key gives the same tensor on every run, so a test can regenerate any
+    single tensor and copy it to the host."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed_int("packed-dev", *key))
+    codes = torch.randint(0, 256, (rows, K * bits // 8), generator=gen, device=device, dtype=torch.uint8)
+    typical = 0.06 / max(1, (1 << (bits - 1)) - 1)
+    u = torch.rand((rows, K // 32), generator=gen, device=device, dtype=torch.float32)
+    scales = ((0.5 + u) * typical).to(torch.float16).view(torch.int16)
+    return codes, scales
+
+
 def bf16_from_f32(a):
     """Round float32 to the nearest bfloat16 (ties to even); returns uint16 bit patterns."""
     u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)

@@ -35,11 +35,6 @@ def expert_ffn(x, w_gate, w_up, w_down):
     return (silu(g) * u) @ w_down.T
 
 
-def expert_hidden(x, w_gate, w_up):
-    """The SwiGLU activation ``h = silu(W_gate x) * (W_up x)``, ``[m, I]``."""
-    return silu(x @ w_gate.T) * (x @ w_up.T)
-
-
 def dequant_tensor(t, K):
     """A packed tensor dict ``{bits, codes, scales}`` -> float64 ``[R, K]``."""
     codes = quant.unpack(t["codes"], t["bits"], K)

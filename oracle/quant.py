@@ -84,6 +84,14 @@ def dequantize(codes, scales, bits):
     return (q.reshape(R, K // BLOCK, BLOCK) * d[:, :, None]).reshape(R, K)
 
 
+def dequantize_half(codes, scales, bits):
+    """The weights rounded once to binary16: ``half(d * (c - 2**(b-1)))`` as
+    uint16 bit patterns ``[R, K]`` (round to nearest, ties to even, from the
+    exact value).  This is what a binary16 matrix product sees of the
+    format's weights."""
+    return f64_to_half_bits(dequantize(codes, scales, bits))
+
+
 def pack(codes, bits):
     """codes ``[R, K]`` (each < 2**bits) -> packed bytes ``[R, K*bits/8]``."""
     codes = np.asarray(codes, dtype=np.uint8)

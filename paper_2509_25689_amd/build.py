@@ -1,7 +1,8 @@
-"""Build the HIP library ``libmoeq.so`` for gfx950, in-tree.
+"""Build the HIP libraries for gfx950, in-tree.
 
 Every source under ``csrc/`` is compiled with hipcc (one process per file, in
-parallel) and linked into ``paper_2509_25689_amd/libmoeq.so``.  Always
+parallel) and linked into ``paper_2509_25689_amd/libmoeq.so``; ``peaks/`` (the
+benchmark's measured roofline denominators) into ``libmoeq_peaks.so``.  Always
 recompiles: this is the "does it build" step."""
 import concurrent.futures
 import os
@@ -14,6 +15,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmoeq.so")
+PEAKS = os.path.join(PKG, "peaks")
+PEAKS_LIB = os.path.join(PKG, "libmoeq_peaks.so")
 ARCH = "gfx950"
 
 FLAGS = [
@@ -41,20 +44,29 @@ def _compile(src):
     return obj
 
 
-def build(verbose=False):
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC)
-                  if f.endswith((".hip", ".cpp")))
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = LIB + ".tmp"
+def _link(objs, lib):
+    tmp = lib + ".tmp"
     cmd = [hipcc(), "-shared", f"--offload-arch={ARCH}", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def _sources(d):
+    return sorted(os.path.join(d, f) for f in os.listdir(d) if f.endswith((".hip", ".cpp")))
+
+
+def build(verbose=False):
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = _sources(CSRC)
+    psrcs = _sources(PEAKS)
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs) + len(psrcs))) as ex:
+        objs = list(ex.map(_compile, srcs + psrcs))
+    _link(objs[:len(srcs)], LIB)
+    _link(objs[len(srcs):], PEAKS_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {PEAKS_LIB}")
     return LIB
 
 

@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -19,6 +20,26 @@ using namespace moeq;
 
 namespace {
 thread_local std::string g_last_error;
+
+// One auxiliary stream per device (default priority, non-blocking), shared by
+// every layer on that device and created on first use.  A forward forks part
+// of its work onto it and joins it back with the layer's own two events, so
+// layers never wait on each other's auxiliary work except by sharing this
+// queue.
+constexpr int kMaxDevices = 64;
+std::mutex g_aux_mu;
+hipStream_t g_aux[kMaxDevices] = {};
+
+hipError_t aux_stream(int dev, hipStream_t* out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_aux_mu);
+  if (!g_aux[dev]) {
+    const hipError_t e = hipStreamCreateWithFlags(&g_aux[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+  }
+  *out = g_aux[dev];
+  return hipSuccess;
+}
 }  // namespace
 
 moeq_status moeq::vset_error(moeq_status st, const char* fmt, va_list ap) {
@@ -76,8 +97,9 @@ struct moeq_layer {
   void* ws_mem = nullptr;
   Workspace ws{};
   hipEvent_t stage_events[MOEQ_STAGE_EVENTS] = {};
-  // a second stream (default priority) and two events: for 2-64 tokens the
-  // gate/up GEMVs of one-token buckets and of larger buckets run side by side
+  // the device's auxiliary stream (shared, not owned) and two events: for
+  // 2-64 tokens the gate/up GEMVs of one-token buckets and of larger buckets
+  // run side by side
   hipStream_t aux = nullptr;
   hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   bool timing = false;
@@ -87,7 +109,6 @@ namespace {
 
 void release(moeq_layer* L) {
   if (!L) return;
-  if (L->aux) hipStreamDestroy(L->aux);
   if (L->fork_ev) hipEventDestroy(L->fork_ev);
   if (L->join_ev) hipEventDestroy(L->join_ev);
   hipFree(L->store);
@@ -295,14 +316,14 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     wo = align_up(wo + bytes, 256);
     return at;
   };
-  const int max_mtiles = prefill_max_mtiles(T, k, S, n_kept), max_small = prefill_max_small(T, k, S, n_kept);
+  const int max_mtiles = prefill_max_mtiles(T, k, S, n_kept), max_rtiles = prefill_max_rtiles(T, k, S, n_kept);
   const size_t o_idx = ws_take(nk * 4), o_w = ws_take(nk * 4), o_off = ws_take((size_t)(E + 1) * 4),
                o_perm = ws_take(nk * 4), o_act = ws_take((size_t)(E + 1) * 4),
                o_cc = ws_take(chunks * E * 4), o_rank = ws_take(nk * 4),
                o_h = ws_take(rows_h * I * 4), o_part = ws_take(rows_h * H * 4),
                o_xexp = ws_take((size_t)T * 4), o_rmax = ws_take(rows_h * 4),
-               o_tiles = ws_take((size_t)(3 + 4 * max_mtiles + 2 * max_small) * 4),
-               o_x16 = ws_take((size_t)T * H * 2), o_h16 = ws_take(rows_h * I * 2);
+               o_tiles = ws_take((size_t)(1 + 2 * max_mtiles) * 4), o_rtiles = ws_take((size_t)(1 + 2 * max_rtiles) * 4),
+               o_x16 = ws_take((size_t)T * H * 2), o_h16 = ws_take(rows_h * I * 2), o_zero = ws_take(256);
 
   // ---- device work ----
   moeq_layer* L = new moeq_layer();
@@ -328,7 +349,7 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   }
   uint8_t* staging = nullptr;
   auto bail = [&](hipError_t e, const char* what) {
-    hipDeviceSynchronize();
+    hipStreamSynchronize(nullptr);
     hipFree(staging);
     release(L);
     return hip_fail(e, what);
@@ -392,7 +413,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
       (he = hipMemcpy(L->mask, expert_mask, E, hipMemcpyHostToDevice)) != hipSuccess ||
       (he = hipMemcpy(L->bias, bias_h.data(), sizeof(float) * E, hipMemcpyHostToDevice)) != hipSuccess)
     return bail(he, "hipMemcpy(tables)");
-  if ((he = hipDeviceSynchronize()) != hipSuccess) return bail(he, "create");
+  // every copy and repack kernel above ran on the null stream
+  if ((he = hipStreamSynchronize(nullptr)) != hipSuccess) return bail(he, "create");
   hipFree(staging);
   staging = nullptr;
 
@@ -408,12 +430,14 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   L->ws.partial = (float*)(w + o_part);
   L->ws.xexp = (int32_t*)(w + o_xexp);
   L->ws.rowmax = (uint32_t*)(w + o_rmax);
-  L->ws.tiles = (int32_t*)(w + o_tiles);
-  L->ws.tiles_small = L->ws.tiles + 1 + 2 * max_mtiles;
-  L->ws.tiles_all = L->ws.tiles_small + 1 + 2 * max_small;
+  L->ws.tiles_all = (int32_t*)(w + o_tiles);
+  L->ws.tiles_rd = (int32_t*)(w + o_rtiles);
   L->ws.x16 = (uint16_t*)(w + o_x16);
   L->ws.h16 = (uint16_t*)(w + o_h16);
-  if ((he = hipStreamCreateWithFlags(&L->aux, hipStreamNonBlocking)) != hipSuccess) return bail(he, "hipStreamCreate");
+  L->ws.zeros = (uint32_t*)(w + o_zero);
+  if ((he = hipMemset(L->ws.zeros, 0, 256)) != hipSuccess || (he = hipStreamSynchronize(nullptr)) != hipSuccess)
+    return bail(he, "hipMemset(zeros)");
+  if ((he = aux_stream(L->device, &L->aux)) != hipSuccess) return bail(he, "hipStreamCreate (auxiliary)");
   if ((he = hipEventCreateWithFlags(&L->fork_ev, hipEventDisableTiming)) != hipSuccess ||
       (he = hipEventCreateWithFlags(&L->join_ev, hipEventDisableTiming)) != hipSuccess)
     return bail(he, "hipEventCreate");
@@ -423,6 +447,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
 
 void moeq_destroy(moeq_layer* L) {
   if (!L) return;
+  // the handle does not know every stream its forwards ran on (nor does
+  // hipFree wait for them by itself on every runtime), so the whole device
+  // is drained before its memory is released
   hipDeviceSynchronize();
   release(L);
 }
@@ -477,13 +504,13 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.max_active = (int)(nk < L->n_kept ? nk : L->n_kept);
   a.xexp = L->ws.xexp;
   a.rowmax = L->ws.rowmax;
-  a.tiles = L->ws.tiles;
   a.max_mtiles = prefill_max_mtiles(n, a.k, a.S, L->n_kept);
-  a.tiles_small = L->ws.tiles_small;
   a.tiles_all = L->ws.tiles_all;
-  a.max_small = prefill_max_small(n, a.k, a.S, L->n_kept);
+  a.max_rtiles = prefill_max_rtiles(n, a.k, a.S, L->n_kept);
+  a.tiles_rd = L->ws.tiles_rd;
   a.x16 = L->ws.x16;
   a.h16 = L->ws.h16;
+  a.zeros = L->ws.zeros;
   a.wide_gateup = L->wide_gateup;
   a.wide_down = L->wide_down;
   const bool prefill =
@@ -502,14 +529,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   mark(1);
   if (e == hipSuccess) {
     if (prefill) {
-      // fork after the tile lists: the 64-row tiles on the second stream
       e = launch_prefill_tiles(a, s);
-      if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(L->aux, L->fork_ev, 0);
-      if (e == hipSuccess) e = launch_gateup_prefill_small(a, L->aux);
-      if (e == hipSuccess) e = hipEventRecord(L->join_ev, L->aux);
-      if (e == hipSuccess) e = launch_gateup_prefill_big(a, s);
-      if (e == hipSuccess) e = hipStreamWaitEvent(s, L->join_ev, 0);
+      if (e == hipSuccess) e = launch_gateup_prefill(a, s);
     } else if (n > 1) {
       // fork: the buckets of 2-64 tokens on the layer's second stream, then join
       if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);
@@ -630,9 +651,8 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
   uint8_t* all_kept = buf + o_mask;
   float* bias = (float*)(buf + o_bias);
   e = launch_fill_u8(all_kept, E, 1, s);
-  if (e == hipSuccess)
-    e = score_bias ? hipMemcpyAsync(bias, score_bias, (size_t)E * 4, hipMemcpyHostToDevice, s)
-                   : hipMemsetAsync(bias, 0, (size_t)E * 4, s);
+  // the bias travels in kernel arguments, so score_bias is free on return
+  if (e == hipSuccess) e = launch_store_host_floats(bias, score_bias, E, s);
   RouterParams rp{};
   rp.logits = logits;
   rp.mask = all_kept;
@@ -719,7 +739,14 @@ moeq_status moeq_bucket(moeq_layer* L, const int32_t* idx, int32_t n, int32_t* o
 }
 
 moeq_status moeq_dequant(moeq_layer* L, int32_t expert, int32_t proj, float* out, void* stream) {
+  return moeq_dequant_as(L, expert, proj, MOEQ_DECODER_EXACT, out, stream);
+}
+
+moeq_status moeq_dequant_as(moeq_layer* L, int32_t expert, int32_t proj, int32_t decoder, void* out,
+                            void* stream) {
   if (!L) return fail(MOEQ_ERR_INVALID_ARG, "layer is NULL");
+  if (decoder != MOEQ_DECODER_EXACT && decoder != MOEQ_DECODER_GEMV_SUBNORMAL && decoder != MOEQ_DECODER_GEMM_F16)
+    return fail(MOEQ_ERR_INVALID_ARG, "decoder %d is not one of MOEQ_DECODER_*", decoder);
   if (proj < 0 || proj > 2) return fail(MOEQ_ERR_INVALID_ARG, "proj %d outside 0..2", proj);
   const int E = L->cfg.n_experts, S = L->cfg.n_shared;
   int slot;
@@ -732,9 +759,17 @@ moeq_status moeq_dequant(moeq_layer* L, int32_t expert, int32_t proj, float* out
   const TensorDev& t = L->desc_host[(size_t)slot * 3 + proj];
   if (!t.codes) return fail(MOEQ_ERR_INVALID_ARG, "expert %d was pruned", expert);
   if (!out) return fail(MOEQ_ERR_INVALID_ARG, "out is NULL");
+  if (decoder == MOEQ_DECODER_GEMV_SUBNORMAL && t.bits > 4)
+    return fail(MOEQ_ERR_UNSUPPORTED, "the subnormal-pair decoder serves widths 2-4 (tensor has %d bits)", t.bits);
   moeq_status st = check_device(L);
   if (st != MOEQ_OK) return st;
-  hipError_t e = launch_dequant(t, out, (hipStream_t)stream);
+  hipError_t e;
+  if (decoder == MOEQ_DECODER_EXACT)
+    e = launch_dequant(t, (float*)out, (hipStream_t)stream);
+  else if (decoder == MOEQ_DECODER_GEMV_SUBNORMAL)
+    e = launch_dequant_sub(t, (float*)out, (hipStream_t)stream);
+  else
+    e = launch_dequant_gemm(t, (uint16_t*)out, (hipStream_t)stream);
   return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
 }
 

@@ -73,11 +73,12 @@ struct Workspace {
   float* partial;      // [(T*k + T*S) x H] per-assignment expert outputs, t*k + j then shared
   int32_t* xexp;       // [T]     per-token exponent e: x * 2^-e fits binary16
   uint32_t* rowmax;    // [T*k + T*S] max |h| of each activation row (float bits)
-  int32_t* tiles;      // [1 + 2*max_mtiles] count, then (slot, first row) per 128-row m-tile
-  int32_t* tiles_small;  // [1 + 2*max_small] the same for the 64-row tiles of bucket remainders
-  int32_t* tiles_all;  // [1 + 2*max_mtiles] every bucket in 128-row tiles, slot order
+  int32_t* tiles_all;  // [1 + 2*max_mtiles] count, then (slot, first row) of every bucket's
+                       // tiles of up to 128 rows, slot order
+  int32_t* tiles_rd;   // [1 + 2*max_rtiles] the same for tiles of up to 64 rows
   uint16_t* x16;       // [T x H]  binary16 x * 2^-xexp (many-token path)
   uint16_t* h16;       // [(T*k + T*S) x I] binary16 h * 2^-(row exponent) (many-token path)
+  uint32_t* zeros;     // [64]    zeroed at create, never written again
 };
 
 // ---- launchers (return hipSuccess or the launch error) ----
@@ -92,6 +93,8 @@ hipError_t launch_bucket_chunked(const int32_t* idx, int n, int k, int E, const 
 hipError_t launch_repack(const uint8_t* canon_codes, int rows, int K, int bits,
                          uint32_t* dev_codes, hipStream_t s);
 hipError_t launch_dequant(const TensorDev& t, float* out, hipStream_t s);
+// widths 2-4: the binary16-subnormal pair decoder rebuilt to float32
+hipError_t launch_dequant_sub(const TensorDev& t, float* out, hipStream_t s);
 hipError_t launch_quantize(const float* w, int rows, int K, int bits, uint8_t* codes,
                            uint16_t* scales, hipStream_t s);
 // decode.hip
@@ -110,13 +113,13 @@ struct DecodeArgs {
   // many-token path
   const int32_t* xexp;
   uint32_t* rowmax;
-  int32_t* tiles;
   int32_t max_mtiles;
-  int32_t* tiles_small;
-  int32_t max_small;
   int32_t* tiles_all;
+  int32_t max_rtiles;
+  int32_t* tiles_rd;
   const uint16_t* x16;
   uint16_t* h16;
+  const uint32_t* zeros;  // 256 zero bytes
   // slots with a 5/6/8-bit gate or up (down) tensor: 0 none, 1 shared
   // experts only, 2 routed experts too
   int32_t wide_gateup, wide_down;
@@ -136,20 +139,23 @@ hipError_t launch_router_gate(const uint16_t* x, const float* w, int n, int H, i
                               hipStream_t s);
 // prune.hip
 hipError_t launch_fill_u8(uint8_t* p, int n, uint8_t v, hipStream_t s);
+// dst[0..n) = src[0..n) (HOST floats, NULL = zeros), passed by value in the
+// kernel arguments: src may be reused as soon as this returns
+hipError_t launch_store_host_floats(float* dst, const float* src, int n, hipStream_t s);
 hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm, const float* w, int E, int n,
                                     double alpha, int keep, double* importance, uint8_t* mask, int32_t* counts,
                                     hipStream_t s);
 // prefill.hip
-constexpr int kGemmBM = 128;  // tokens per grouped-GEMM m-tile
+constexpr int kGemmBM = 128;  // tokens per m-tile of the LDS-decoded (5/6/8-bit) GEMMs
+constexpr int kRdTile = 64;   // tokens per tile of the register-decoded (2-4-bit) GEMMs
 int prefill_max_mtiles(int n, int k, int S, int n_kept);
-// 64-row tiles: at most one per bucket (its remainder of 1..64 rows)
-int prefill_max_small(int n, int k, int S, int n_kept);
-hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
-// the same in parts: the tile lists, then the 128-row (and 5/6/8-bit) tiles
-// and the 64-row tiles, which the forward runs on two streams side by side
+int prefill_max_rtiles(int n, int k, int S, int n_kept);
+// the tile list (and cleared h row maxima), then the gate/up GEMMs, then
+// h in binary16 and the down GEMMs
 hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s);
-hipError_t launch_gateup_prefill_big(const DecodeArgs& a, hipStream_t s);
-hipError_t launch_gateup_prefill_small(const DecodeArgs& a, hipStream_t s2);
+hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s);
+// the grouped GEMMs' weight decoder: binary16 d * (c - 2^(b-1)) bit patterns
+hipError_t launch_dequant_gemm(const TensorDev& t, uint16_t* out, hipStream_t s);
 
 }  // namespace moeq

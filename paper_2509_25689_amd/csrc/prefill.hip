@@ -4,25 +4,25 @@
 // multiplies its bucket of tokens by its weights, so the layer becomes a set
 // of independent GEMMs of very different heights (routing is skewed).  The
 // bucketing permutation lists each expert's tokens contiguously; a small
-// kernel cuts every bucket into m-tiles of kGemmBM (128) rows, a remainder
-// of at most 64 rows into a 64-row tile for the gate/up GEMM, and writes the
-// tile lists, so the GEMM grids never depend on a host synchronization.
+// kernel cuts every bucket into tiles of up to 128 tokens and writes the
+// tile list, so the GEMM grids never depend on a host synchronization.
 //
 // Arithmetic: activations (bf16, exact in binary16 after a per-token
 // power-of-two prescale), dequantized weights fp16(d * (c - z)) (one rounding)
 // and the SwiGLU activations h (binary16 after a per-row power-of-two
-// prescale) enter v_mfma_f32_16x16x32_f16 with float32 accumulation.  The
-// packed-weight tile of each K step is decoded once per workgroup into LDS.
+// prescale) enter v_mfma_f32_16x16x32_f16 with float32 accumulation.
 //
-// Workgroup tile: 128 rows (tokens) x 128 output features (per projection;
-// gate/up computes both projections of the same features so SwiGLU is fused
-// into the epilogue), K step 64, eight waves (two per SIMD) in a 2 x 4
-// arrangement, each owning 64 rows x 32 columns of 16 x 16 MFMA tiles.  LDS
-// holds two decoded K steps and registers the raw data of the next two, so
-// the decode of one step and the loads of later ones overlap the current
-// step's MFMAs.  Workgroups are mapped to tiles from the tile count on the
-// device: each XCD takes an equal run of consecutive m-tiles (one expert's
-// tiles share its L2), whatever the worst-case size of the grid.
+// 2-4-bit tensors (every tensor of the workloads measured here) take the
+// register-decoded GEMMs below: the packed weights are decoded in registers
+// straight into the matrix operand, tokens are the 16-wide side of the
+// matrix tiles.  Tiles with a 5, 6 or 8-bit tensor take the LDS-decoded
+// GEMMs (gateup_gemm8_kernel, down_gemm8_kernel): 128 tokens x 128 weight
+// rows per workgroup, the weight tile of each K step decoded once into LDS.
+// Workgroups are mapped to tiles from the tile count on the device: each XCD
+// takes an equal run of consecutive m-tiles (one expert's tiles share its
+// L2), whatever the worst-case size of the grid.
+#include <atomic>
+
 #include "internal.h"
 #include "layout.h"
 
@@ -38,19 +38,17 @@ constexpr int BM = kGemmBM, BN = 128, BK = 64;
 // halves per LDS row: 16 halves of padding (measured best of 8, 16, 24, 40)
 constexpr int LDS_STRIDE = BK + 16;
 
-// ---- tile lists: slot order = shared experts, then active experts ----
-// For the gate/up GEMM of 2-4-bit tensors a bucket of M rows becomes M / 128
-// full 128-row tiles; a remainder of more than 64 rows takes one more
-// 128-row tile, one of 1..64 rows a 64-row tile in the second list.  The
-// third list cuts every bucket into ceil(M / 128) 128-row tiles (the GEMMs
-// without a 64-row variant), large and small buckets interleaved in slot
-// order, so every XCD's share mixes both.
+// ---- tile lists: slot order = shared experts, then active experts; every
+// bucket of M rows becomes ceil(M / 128) tiles of up to 128 rows (tiles_all,
+// for the LDS-decoded GEMMs) and ceil(M / 64) tiles of up to 64 rows
+// (tiles_rd, for the register-decoded GEMMs), large and small buckets
+// interleaved in slot order, so every XCD's share mixes both.  Also clears
+// the running maxima of the h rows.
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
-  __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];   // 128-row tiles
-  __shared__ int32_t scnt[kMaxShared + kMaxExperts + 1];  // 64-row tile (0 or 1)
+  __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];
   __shared__ int32_t off[kMaxShared + kMaxExperts + 2];
-  __shared__ int32_t soff[kMaxShared + kMaxExperts + 2];
-  __shared__ int32_t aoff[kMaxShared + kMaxExperts + 2];
+  __shared__ int32_t cnt2[kMaxShared + kMaxExperts + 1];
+  __shared__ int32_t off2[kMaxShared + kMaxExperts + 2];
   const int tid = threadIdx.x;
   const int nslots = a.S + a.active[0];
   for (int s = tid; s < nslots; s += 1024) {
@@ -61,47 +59,38 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
       const int e = a.active[1 + s - a.S];
       M = a.offsets[e + 1] - a.offsets[e];
     }
-    const int r = M % BM;
-    cnt[s] = M / BM + (r > BM / 2 ? 1 : 0);
-    scnt[s] = r > 0 && r <= BM / 2 ? 1 : 0;
+    cnt[s] = (M + BM - 1) / BM;
+    cnt2[s] = (M + kRdTile - 1) / kRdTile;
   }
   // rows of h whose running maxima the gate/up epilogue accumulates
   const int rows = a.n * (a.k + a.S);
   for (int r = tid; r < rows; r += 1024) a.rowmax[r] = 0u;
   __syncthreads();
   if (tid == 0) {
-    int run = 0, srun = 0, arun = 0;
+    int run = 0, run2 = 0;
     for (int s = 0; s < nslots; ++s) {
       off[s] = run;
-      soff[s] = srun;
-      aoff[s] = arun;
+      off2[s] = run2;
       run += cnt[s];
-      srun += scnt[s];
-      arun += cnt[s] + scnt[s];
+      run2 += cnt2[s];
     }
-    a.tiles[0] = min(run, a.max_mtiles);
-    a.tiles_small[0] = min(srun, a.max_small);
-    a.tiles_all[0] = min(arun, a.max_mtiles);
+    a.tiles_all[0] = min(run, a.max_mtiles);
+    a.tiles_rd[0] = min(run2, a.max_rtiles);
   }
   __syncthreads();
   for (int s = tid; s < nslots; s += 1024) {
-    const int nb = cnt[s];
-    for (int i = 0; i < nb; ++i) {
+    for (int i = 0; i < cnt[s]; ++i) {
       const int t = off[s] + i;
-      if (t < a.max_mtiles) {
-        a.tiles[1 + 2 * t] = s;
-        a.tiles[2 + 2 * t] = i * BM;
-      }
-    }
-    if (scnt[s] && soff[s] < a.max_small) {
-      a.tiles_small[1 + 2 * soff[s]] = s;
-      a.tiles_small[2 + 2 * soff[s]] = nb * BM;
-    }
-    for (int i = 0; i < nb + scnt[s]; ++i) {
-      const int t = aoff[s] + i;
       if (t < a.max_mtiles) {
         a.tiles_all[1 + 2 * t] = s;
         a.tiles_all[2 + 2 * t] = i * BM;
+      }
+    }
+    for (int i = 0; i < cnt2[s]; ++i) {
+      const int t = off2[s] + i;
+      if (t < a.max_rtiles) {
+        a.tiles_rd[1 + 2 * t] = s;
+        a.tiles_rd[2 + 2 * t] = i * kRdTile;
       }
     }
   }
@@ -179,6 +168,7 @@ struct GemmArgs {
   float* h;
   float* partial;
   uint32_t* rowmax;
+  const uint32_t* zeros;
   int n, H, I, k;
 };
 
@@ -193,6 +183,7 @@ __device__ __forceinline__ GemmArgs gemm_args(const DecodeArgs& a) {
   g.h = a.h;
   g.partial = a.partial;
   g.rowmax = a.rowmax;
+  g.zeros = a.zeros;
   g.n = a.n;
   g.H = a.H;
   g.I = a.I;
@@ -463,7 +454,6 @@ __device__ __forceinline__ void gemm_loop8(const MOEQ_GLOBAL u32x4* rc, const MO
 #undef STEP8
 }
 
-template <bool WIDE>
 __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
                                   const TensorDev tu, _Float16* lds) {
   _Float16* As = lds;                            // [2][BM][LDS_STRIDE]
@@ -503,16 +493,14 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
     if (blk) GU8(2, 1); else GU8(2, 0);
   } else if (bits == 3) {
     if (blk) GU8(3, 1); else GU8(3, 0);
-  } else if (!WIDE || bits == 4) {
+  } else if (bits == 4) {
     if (blk) GU8(4, 1); else GU8(4, 0);
-  } else if constexpr (WIDE) {
-    if (bits == 5) {
-      if (blk) GU8(5, 1); else GU8(5, 0);
-    } else if (bits == 6) {
-      if (blk) GU8(6, 1); else GU8(6, 0);
-    } else {
-      if (blk) GU8(8, 1); else GU8(8, 0);
-    }
+  } else if (bits == 5) {
+    if (blk) GU8(5, 1); else GU8(5, 0);
+  } else if (bits == 6) {
+    if (blk) GU8(6, 1); else GU8(6, 0);
+  } else {
+    if (blk) GU8(8, 1); else GU8(8, 0);
   }
 #undef GU8
 
@@ -544,11 +532,8 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
   }
 }
 
-// Launched with WIDE = true: the tiles with a 5, 6 or 8-bit gate or up
-// tensor (the other of the two may be narrower).  The 2-4-bit tiles take the
-// raw-staged gateup_rs_kernel; WIDE = false, their register-path variant, is
-// not launched.
-template <bool WIDE>
+// The tiles with a 5, 6 or 8-bit gate or up tensor (the other of the two may
+// be narrower); 2-4-bit tiles take gateup_rd_kernel.
 __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.I / BN;
@@ -559,11 +544,10 @@ __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   const SlotInfo sl = slot_of(a, slot);
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
-  if ((tg.bits > 4 || tu.bits > 4) != WIDE) return;
-  gateup_gemm_body8<WIDE>(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
+  if (tg.bits <= 4 && tu.bits <= 4) return;
+  gateup_gemm_body8(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
 }
 
-template <bool WIDE>
 __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev td,
                                 _Float16* lds) {
   _Float16* As = lds;                        // [2][BM][LDS_STRIDE]
@@ -598,14 +582,6 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
 #define DN8(B, BL) gemm_loop8<1, B, BL, true, 0>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc)
   if (!wrole) {
     gemm_loop8<1, 4, 0, false, 4>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
-  } else if constexpr (!WIDE) {
-    if (bits == 2) {
-      if (blk) DN8(2, 1); else DN8(2, 0);
-    } else if (bits == 3) {
-      if (blk) DN8(3, 1); else DN8(3, 0);
-    } else {
-      if (blk) DN8(4, 1); else DN8(4, 0);
-    }
   } else {
     if (bits == 5) {
       if (blk) DN8(5, 1); else DN8(5, 0);
@@ -645,11 +621,9 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
   }
 }
 
-// WIDE = false takes the tiles whose down tensor is 2-4 bits wide, WIDE = true
-// the 5, 6 and 8-bit ones.  Four waves per SIMD (128 registers): two
-// workgroups share a compute unit (2 x 80 KB of LDS) and overlap their K-step
-// chains.
-template <bool WIDE>
+// The tiles whose down tensor is 5, 6 or 8 bits wide (2-4-bit tiles take
+// down_rd_kernel).  Four waves per SIMD (128 registers): two workgroups share
+// a compute unit (2 x 80 KB of LDS) and overlap their K-step chains.
 __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.H / BN;
@@ -660,365 +634,639 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
   const SlotInfo sl = slot_of(a, slot);
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
-  if ((td.bits > 4) != WIDE) return;
-  down_gemm_body8<WIDE>(gemm_args(a), sl, m0, nt * BN, td, lds_h);
+  if (td.bits <= 4) return;
+  down_gemm_body8(gemm_args(a), sl, m0, nt * BN, td, lds_h);
 }
 
 // ---------------------------------------------------------------------------
-// Raw-staged grouped GEMM for 2-4 bit weights.
+// Register-decoded grouped GEMM for 2-4-bit weights (gate/up with SwiGLU, and
+// down).
 //
-// In the kernels above every lane loads one 16-byte chunk of a different
-// weight row per K step: each load brings a whole cache line from L2 and
-// uses a quarter of it or less, and the line is gone before the same thread
-// needs its neighbour, so the L1 miss traffic, not the matrix cores, sets
-// the pace.  Here the decode waves load the packed codes (and scales) of 4
-// units (512 k, 8 K steps) of all 128 weight rows of the tile at once, 4
-// lanes per row and chunk plane (64 contiguous bytes), store them in LDS,
-// and each K step decodes its block from LDS into the binary16 tile.
+// Weights are the MFMA's first operand (32 weight rows x 16 k) and tokens
+// its second (16 k x 32 tokens) of v_mfma_f32_32x32x16_f16 (on gfx950 it
+// runs at twice the rate of the 16 x 16 x 32 shape), so a bucket of M tokens
+// costs ceil(M / 32) token tiles per 32 weight rows.  A workgroup of four
+// waves owns 256 weight rows and up to 64 tokens of one expert bucket; each
+// wave owns 64 weight rows (two row tiles) and all the tokens (two token
+// tiles), 2 x 2 accumulator tiles of 32 x 32.  Two workgroups share a
+// compute unit, so the two waves on a SIMD come from independent workgroups
+// and one's waits (loads, barriers) are covered by the other's work.
 //
-// Used for gate/up (the down GEMM, with a quarter of the K steps per tile,
-// measured faster with the per-thread loads above).  The loop is written for
-// NT tensors of 128 / NT rows each.  Tile: 128 tokens x 128 weight rows (64
-// features of each projection, rows 0-63 gate and 64-127 up).  Waves
-// 0-3 load and decode (wave w: rows 64 (w % 2) .. +63, block half w / 2 of
-// each half unit, so every wave works on one tensor and one width), waves
-// 4-7 move activations (32 values of tile row (t - 256) / 2 per step).
-// The eight waves share the MFMAs: 2 x 4 waves of 64 tokens x 16 features
-// per projection.
-constexpr int RS_ROWS = 128;
-constexpr int RS_RAW = 4 * 16 + 4;   // dwords per staged row: 4 chunk planes x 4 units (+ padding)
-constexpr int RS_SCL = 10;           // dwords per staged row of scales: 16 binary16 (+ padding; even, so
-                                     // the 8-byte stores stay aligned)
-// LDS of a tile of bmt tokens: A [2][bmt], W [2][128], raw and scale stages
-constexpr size_t rs_lds(int bmt) {
-  return (size_t)2 * (bmt + RS_ROWS) * LDS_STRIDE * 2 + (size_t)2 * RS_ROWS * RS_RAW * 4 +
-         (size_t)2 * RS_ROWS * RS_SCL * 4;
-}
-static_assert(rs_lds(BM) <= 160 * 1024, "the raw-staged tile must fit the LDS of a compute unit");
+// Weights never pass through LDS.  Lane l of a wave (row r = l % 32 of each
+// row tile, k-half g = l / 32) loads, for each K stage of 512 weights (4
+// units of 128), units 4U + 2g and 4U + 2g + 1 of its rows: the two lanes of
+// a row read 64 contiguous bytes per chunk plane.  It decodes them in
+// registers straight into the operand layout, binary16 d * (c - 2^(b-1))
+// with one rounding: at k step t (0..7) of sub-stage q (block q of each
+// unit), the 8 operand values of lane (r, g) are weights 32 q + 8 (t % 4) ..
+// + 7 of unit 4U + 2g + t / 4.  The activation operand of lane (c, g) must
+// hold the same k values, which the LDS tile provides: activations go through
+// LDS in sub-stages of 128 k values (block q of the stage's four units), 64
+// token rows of 16 pieces of 16 bytes, piece p = 4 u + m (unit u of the
+// stage, piece m of its block) stored at position p ^ (row % 16) of its row
+// (no bank conflicts for the 16-byte fragment reads).  Four LDS buffers:
+// sub-stage s + 2 is requested when s begins and stored when it ends.
+//
+// gate/up: waves 0 and 1 own 64 gate rows each, waves 2 and 3 the same
+// features' up rows (each wave works on one tensor, so on one width); the
+// up waves hand their accumulators to the gate waves through LDS for the
+// SwiGLU epilogue.  down: four waves of 64 output features of one tensor.
+// The K loop is instantiated per width and per token count (up to 32
+// tokens: one token tile, else two), so a small bucket does not spend
+// matrix instructions on an empty tile, and the loop has no branches.
+constexpr int RD_T = kRdTile;         // tokens per workgroup tile
+constexpr int RD_ROWS = 256;          // weight rows per workgroup
+constexpr int RD_WAVES = 4;
+constexpr int RD_THREADS = 64 * RD_WAVES;
+constexpr int RD_RT = 2;              // row tiles of 32 per wave
+constexpr int RD_WROWS = 32 * RD_RT;  // weight rows per wave
+constexpr int RD_SUB = RD_T * 256;    // bytes of one activation sub-stage
+constexpr int RD_NBUF = 4;            // activation sub-stages resident in LDS
+constexpr int RD_APT = RD_SUB / 16 / RD_THREADS;  // 16-byte staging pieces per thread and sub-stage
+constexpr size_t RD_LDS = (size_t)RD_NBUF * RD_SUB;
+static_assert(RD_WAVES * RD_WROWS == RD_ROWS, "the waves cover the workgroup's rows");
+static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * 2 * 64 * 64, "the SwiGLU hand-over must fit the activation buffers");
+static_assert(2 * RD_LDS <= 160 * 1024, "two workgroups share a compute unit's LDS");
 
-// one raw stage (4 units) of this lane: 2B chunk pieces and 2 scale pieces
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// this lane's unit of one weight row: B chunks of 16 bytes and the unit's
+// four binary16 scales
 template <int B>
-struct RsStage {
-  u32x4 c[2 * B];
-  u32x2 s[2];
+struct RdUnit {
+  u32x4 c[B];
+  u32x2 s;
 };
 
-// Piece m of a wave's tensor (RPT rows, WPT waves per tensor, h = this wave's
-// index among them): row ((lane / 4) + 16 m) mod RPT, unit lane % 4, chunk
-// plane m / (RPT / 16); the wave takes m = WPT i + h.
-template <int B, int NT>
-__device__ __forceinline__ void rs_load(RsStage<B>& st, const TensorDev& t, int n0, int U, int K, int u0, int lane,
-                                        int h) {
-  constexpr int RPT = RS_ROWS / NT, WPT = 4 / NT;
-  const int uu = min(u0 + (lane & 3), U - 1);
-#pragma unroll
-  for (int i = 0; i < 2 * B; ++i) {
-    const int m = WPT * i + h;
-    const int r = ((lane >> 2) + 16 * m) % RPT, j = m / (RPT / 16);
-    const MOEQ_GLOBAL u32x4* rc = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)(n0 + r) * B * U * 4));
-    st.c[i] = rc[(size_t)j * U + uu];
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int m = WPT * i + h;
-    const int r = ((lane >> 2) + 16 * m) % RPT;
-    st.s[i] = *gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)(n0 + r) * (K / kBlock)) + uu);
-  }
+template <int B>
+__device__ __forceinline__ uint32_t rd_dword(const RdUnit<B>& u, int i) {
+  return u.c[i >> 2][i & 3];
 }
 
-template <int B, int NT>
-__device__ __forceinline__ void rs_store(const RsStage<B>& st, uint32_t* raw, uint32_t* scl, int tt, int lane, int h) {
-  constexpr int RPT = RS_ROWS / NT, WPT = 4 / NT;
+// Loads unit `unit` of the row (chunk base rc, scale pairs rs); a unit past
+// the row (a partial last stage) is loaded clamped and given scale 0, so its
+// weights decode to exact zeros.
+template <int B>
+__device__ __forceinline__ void rd_load(RdUnit<B>& u, const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL u32x2* rs,
+                                        int Uk, int unit) {
+  const int uc = min(unit, Uk - 1);
 #pragma unroll
-  for (int i = 0; i < 2 * B; ++i) {
-    const int m = WPT * i + h;
-    const int r = ((lane >> 2) + 16 * m) % RPT, j = m / (RPT / 16);
-    *reinterpret_cast<u32x4*>(raw + (tt * RPT + r) * RS_RAW + j * 16 + (lane & 3) * 4) = st.c[i];
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int m = WPT * i + h;
-    const int r = ((lane >> 2) + 16 * m) % RPT;
-    *reinterpret_cast<u32x2*>(scl + (tt * RPT + r) * RS_SCL + (lane & 3) * 2) = st.s[i];
-  }
+  for (int j = 0; j < B; ++j) u.c[j] = __builtin_nontemporal_load(rc + (size_t)j * Uk + uc);
+  const u32x2 s = rs[uc];
+  u.s = unit < Uk ? s : u32x2{0u, 0u};
 }
 
-// Block Q of staged unit ul of LDS row `row` (the chunks it occupies and the
-// aligned pair of scales holding its own).
-template <int B, int Q>
-__device__ __forceinline__ RawBlk rs_block(const uint32_t* raw, const uint32_t* scl, int row, int ul) {
-  constexpr int c0 = (Q * B) >> 2;
-  constexpr bool two = ((Q * B) & 3) + B > 4;
-  RawBlk r;
-  const uint32_t* base = raw + row * RS_RAW + ul * 4;
-  r.a = *reinterpret_cast<const u32x4*>(base + c0 * 16);
-  if constexpr (two)
-    r.b = *reinterpret_cast<const u32x4*>(base + (c0 + 1) * 16);
-  else
-    r.b = u32x4{0u, 0u, 0u, 0u};
-  r.sc = scl[row * RS_SCL + ul * 2 + (Q >> 1)];
-  return r;
+struct RdConsts {
+  uint32_t base;  // binary16 1024 in both halves
+  uint32_t mask;  // the width's code mask in both halves
+  half2_t zb;     // -(1024 + 2^(b-1)) in both halves
+};
+
+template <int B>
+__device__ __forceinline__ RdConsts rd_consts() {
+  RdConsts k;
+  asm("v_mov_b32 %0, 0x64006400" : "=v"(k.base));
+  if constexpr (B == 4) asm("v_mov_b32 %0, 0x000F000F" : "=v"(k.mask));
+  if constexpr (B == 3) asm("v_mov_b32 %0, 0x00070007" : "=v"(k.mask));
+  if constexpr (B == 2) asm("v_mov_b32 %0, 0x00030003" : "=v"(k.mask));
+  const _Float16 zf = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
+  k.zb = half2_t{zf, zf};
+  return k;
 }
 
-// MI: 16-row MFMA tiles per wave along the tokens (4 for 128-token tiles, 2
-// for 64-token tiles)
-template <int NT, int C, int MI>
-__device__ __forceinline__ void read_frags_rs(const _Float16* A, const _Float16* W, int lane, int wm, int wn,
-                                              half8 (&fa)[2][MI], half8 (&fb)[2][NT][C]) {
-  constexpr int RPT = RS_ROWS / NT;
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int kof = kk * 32 + (lane >> 4) * 8;
-#pragma unroll
-    for (int i = 0; i < MI; ++i) fa[kk][i] = lds_frag(A + (wm * 16 * MI + 16 * i + (lane & 15)) * LDS_STRIDE + kof);
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-#pragma unroll
-      for (int c = 0; c < C; ++c)
-        fb[kk][t][c] = lds_frag(W + (t * RPT + wn * 16 * C + 16 * c + (lane & 15)) * LDS_STRIDE + kof);
-  }
+// code pair at bit offset S of each half of w -> binary16 d * (c - z) pair
+template <int S>
+__device__ __forceinline__ uint32_t rd_pair(uint32_t w, const RdConsts& k, half2_t d2) {
+  const uint32_t v = and_or(w >> S, k.mask, k.base);
+  const half2_t c = __builtin_bit_cast(half2_t, v) + k.zb;
+  return __builtin_bit_cast(uint32_t, c * d2);
 }
 
-template <int NT, int C, int MI>
-__device__ __forceinline__ void mfmas_rs(const half8 (&fa)[2][MI], const half8 (&fb)[2][NT][C],
-                                         f32x4v (&acc)[NT][MI][C]) {
-#pragma unroll
-  for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-    for (int c = 0; c < C; ++c)
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-          acc[t][i][c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[kk][i], fb[kk][t][c], acc[t][i][c], 0, 0, 0);
-}
-
-// One K loop.  DW: this wave stages and decodes weights of width B (block
-// half BLK of its rows; its tensor t, index h among the tensor's waves),
-// else it moves MI pieces of activations per step.  LDS: A [2][32 MI], W
-// [2][128] (binary16 rows of LDS_STRIDE), raw [2][128][RS_RAW], scales
-// [2][128][RS_SCL].  Raw stage t (K steps 8t .. 8t + 7) is stored to LDS at
-// step 8t - 2 and requested one stage earlier, at step 8t - 10 (the prologue
-// loads stage 0 and requests stage 1), so its loads have a whole stage to
-// arrive; step s + 1 is decoded during step s.
-template <int NT, int C, int B, int BLK, bool DW, int MI>
-__device__ __forceinline__ void gemm_loop_rs(const TensorDev& t, int tt, int h, int n0, int U, int K,
-                                             const MOEQ_GLOBAL u32x4* arow, _Float16* adst, _Float16* As, _Float16* Ws,
-                                             uint32_t* raw, uint32_t* scl, int lane, int wm, int wn, int nk,
-                                             f32x4v (&acc)[NT][MI][C]) {
-  constexpr int ABUF = 32 * MI * LDS_STRIDE;  // halves per A buffer
-  const int wrow = tt * 64 + lane;     // decode row: rows 64 (w % 2) + lane
-  const int ts = NT == 2 ? tt : 0;     // the staged tensor of this wave
-  RsStage<B> st;
-  u32x4 xv[2][MI];
-  // decode step s into W buffer s % 2 (S2: s % 2, compile-time)
-#define RS_DECODE(S2, s)                                                                                   \
-  do {                                                                                                     \
-    if constexpr (DW) {                                                                                    \
-      const int sb_ = ((s) >> 3) & 1, ul_ = ((s) >> 1) & 3;                                               \
-      const RawBlk rb_ = rs_block<B, 2 * (S2) + BLK>(raw + sb_ * RS_ROWS * RS_RAW, scl + sb_ * RS_ROWS * RS_SCL, \
-                                                     wrow, ul_);                                           \
-      decode_blk<B>(rb_, ((2 * (S2) + BLK) * B) & 3, BLK != 0,                                            \
-                    Ws + (S2) * (RS_ROWS * LDS_STRIDE) + wrow * LDS_STRIDE + 32 * BLK);                    \
-    }                                                                                                      \
-  } while (0)
-#define RS_AMOVE(S2)                                                                                       \
-  do {                                                                                                     \
-    if constexpr (!DW) {                                                                                   \
-      u32x4* ad_ = reinterpret_cast<u32x4*>(adst + (S2) * ABUF);                                          \
-      _Pragma("unroll") for (int i_ = 0; i_ < MI; ++i_) ad_[i_] = xv[S2][i_];                              \
-    }                                                                                                      \
-  } while (0)
-#define RS_ALOAD(S2, s)                                                                                    \
-  do {                                                                                                     \
-    if constexpr (!DW) {                                                                                   \
-      _Pragma("unroll") for (int i_ = 0; i_ < MI; ++i_) xv[S2][i_] = arow[(s) * 8 + i_];                   \
-    }                                                                                                      \
-  } while (0)
-  // raw stage handling at the end of step s's work: store stage (s / 8) + 1
-  // at step s % 8 == 6, then request stage (s / 8) + 2
-#define RS_STAGE(s)                                                                                        \
-  do {                                                                                                     \
-    if constexpr (DW) {                                                                                    \
-      if (((s) & 7) == 6 && (s) + 2 < nk) {                                                                \
-        const int nb_ = (((s) >> 3) + 1) & 1;                                                              \
-        rs_store<B, NT>(st, raw + nb_ * RS_ROWS * RS_RAW, scl + nb_ * RS_ROWS * RS_SCL, ts, lane, h);       \
-        if (8 * (((s) >> 3) + 2) < nk) rs_load<B, NT>(st, t, n0, U, K, 4 * (((s) >> 3) + 2), lane, h);     \
-      }                                                                                                    \
-    }                                                                                                      \
-  } while (0)
-#define RS_STEP(P, s)                                                                                      \
-  do {                                                                                                     \
-    half8 fa[2][MI], fb[2][NT][C];                                                                         \
-    read_frags_rs<NT, C, MI>(As + (P) * ABUF, Ws + (P) * (RS_ROWS * LDS_STRIDE), lane, wm, wn, fa, fb);   \
-    RS_DECODE(1 - (P), (s) + 1);                                                                           \
-    RS_AMOVE(1 - (P));                                                                                     \
-    RS_ALOAD(1 - (P), min((s) + 3, nk - 1));                                                               \
-    RS_STAGE(s);                                                                                           \
-    mfmas_rs<NT, C, MI>(fa, fb, acc);                                                                      \
-    __syncthreads();                                                                                       \
-  } while (0)
-  // prologue: stage 0 stored, stage 1 requested; steps 0 (decoded) and 1 (loaded)
-  if constexpr (DW) {
-    rs_load<B, NT>(st, t, n0, U, K, 0, lane, h);
-    rs_store<B, NT>(st, raw, scl, ts, lane, h);
-    if (8 < nk) rs_load<B, NT>(st, t, n0, U, K, 4, lane, h);
-  }
-  RS_ALOAD(0, 0);
-  RS_ALOAD(1, min(1, nk - 1));
-  __syncthreads();
-  RS_DECODE(0, 0);
-  RS_AMOVE(0);
-  RS_ALOAD(0, min(2, nk - 1));
-  __syncthreads();
-  for (int s0 = 0; s0 < nk; s0 += 2) {
-    RS_STEP(0, s0);
-    RS_STEP(1, s0 + 1);
-  }
-#undef RS_DECODE
-#undef RS_AMOVE
-#undef RS_ALOAD
-#undef RS_STAGE
-#undef RS_STEP
-}
-
-// Tile of BMT tokens (128 or 64).  The 256 movers take piece t % TPR of tile
-// row t / TPR (TPR = 2 or 4 movers per row, MI 16-byte pieces each per step).
-template <int BMT>
-__device__ void gateup_rs_body(const GemmArgs a, const SlotInfo sl, int m0, int n0, const TensorDev tg,
-                               const TensorDev tu, _Float16* lds) {
-  constexpr int MI = BMT / 32, TPR = 8 / MI;
-  _Float16* As = lds;
-  _Float16* Ws = lds + 2 * BMT * LDS_STRIDE;
-  uint32_t* raw = reinterpret_cast<uint32_t*>(Ws + 2 * RS_ROWS * LDS_STRIDE);
-  uint32_t* scl = raw + 2 * RS_ROWS * RS_RAW;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
-  const int H = a.H, I = a.I, U = H / kUnit;
-  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
-  const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
-  const bool dw = __builtin_amdgcn_readfirstlane(wave) < 4;
-  const int tt = wave & 1, h = (wave >> 1) & 1, blk = (wave >> 1) & 1;
-  const TensorDev t = tt ? tu : tg;
-  const int bits = __builtin_amdgcn_readfirstlane(t.bits);
-  const int ar = (tid & 255) / TPR, aq = (tid & 255) % TPR;
-  int tok = 0;
-  if (m0 + ar < sl.M) tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
-  const MOEQ_GLOBAL u32x4* arow = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H)) + MI * aq;
-  _Float16* adst = As + ar * LDS_STRIDE + 8 * MI * aq;
-
-  f32x4v acc[2][MI][1];
-#pragma unroll
-  for (int q = 0; q < 2; ++q)
-#pragma unroll
-    for (int i = 0; i < MI; ++i) acc[q][i][0] = f32x4v{0.f, 0.f, 0.f, 0.f};
-  const int nk = H / BK;
-#define GURS(B, BL) \
-  gemm_loop_rs<2, 1, B, BL, true, MI>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc)
-  if (!dw) {
-    gemm_loop_rs<2, 1, 2, 0, false, MI>(t, tt, h, n0, U, H, arow, adst, As, Ws, raw, scl, lane, wm, wn, nk, acc);
-  } else if (bits == 2) {
-    if (blk) GURS(2, 1); else GURS(2, 0);
-  } else if (bits == 3) {
-    if (blk) GURS(3, 1); else GURS(3, 0);
+// Operand piece M (weights 8M .. 8M + 7) of block Q of this lane's unit.
+template <int B, int Q, int M>
+__device__ __forceinline__ half8 rd_piece(const RdUnit<B>& u, const RdConsts& k) {
+  const uint32_t sp = Q < 2 ? u.s.x : u.s.y;
+  const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)((Q & 1) ? sp >> 16 : sp));
+  const half2_t d2 = {d, d};
+  uint32_t p[4];
+  if constexpr (B == 4) {
+    const uint32_t w = rd_dword(u, 4 * Q + M);
+    p[0] = rd_pair<0>(w, k, d2);
+    p[1] = rd_pair<4>(w, k, d2);
+    p[2] = rd_pair<8>(w, k, d2);
+    p[3] = rd_pair<12>(w, k, d2);
+  } else if constexpr (B == 2) {
+    const uint32_t w = rd_dword(u, 2 * Q + M / 2);
+    constexpr int o = 8 * (M & 1);
+    p[0] = rd_pair<o + 0>(w, k, d2);
+    p[1] = rd_pair<o + 2>(w, k, d2);
+    p[2] = rd_pair<o + 4>(w, k, d2);
+    p[3] = rd_pair<o + 6>(w, k, d2);
   } else {
-    if (blk) GURS(4, 1); else GURS(4, 0);
-  }
-#undef GURS
-
-  // epilogue: undo the activation prescale, SwiGLU, store h, track row maxima
+    // pairs 4M .. 4M + 3 of the block; pair P < 15 sits in dword P / 5 at
+    // offset 3 (P % 5), pair 15 is bit q of each code in bit 15 / 31 of dword q
 #pragma unroll
-  for (int i = 0; i < MI; ++i) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wm * 16 * MI + 16 * i + (lane >> 4) * 4 + j;
-      const bool ok = m0 + r < sl.M;
-      float sc = 1.0f;
-      if (ok) {
-        const int tk = sl.shared >= 0 ? m0 + r : perm[sl.base + m0 + r] / a.k;
-        sc = __builtin_amdgcn_ldexpf(1.0f, xexp[tk]);
+    for (int i = 0; i < 4; ++i) {
+      constexpr int dummy = 0;
+      (void)dummy;
+      const int P = 4 * M + i;
+      if (P < 15) {
+        const uint32_t w = rd_dword(u, 3 * Q + P / 5);
+        switch (P % 5) {
+          case 0: p[i] = rd_pair<0>(w, k, d2); break;
+          case 1: p[i] = rd_pair<3>(w, k, d2); break;
+          case 2: p[i] = rd_pair<6>(w, k, d2); break;
+          case 3: p[i] = rd_pair<9>(w, k, d2); break;
+          default: p[i] = rd_pair<12>(w, k, d2); break;
+        }
+      } else {
+        uint32_t m1, m2, m4;
+        asm("v_mov_b32 %0, 0x00010001" : "=v"(m1));
+        asm("v_mov_b32 %0, 0x00020002" : "=v"(m2));
+        asm("v_mov_b32 %0, 0x00040004" : "=v"(m4));
+        uint32_t t = and_or(rd_dword(u, 3 * Q) >> 15, m1, k.base);
+        t = and_or(rd_dword(u, 3 * Q + 1) >> 14, m2, t);
+        t = and_or(rd_dword(u, 3 * Q + 2) >> 13, m4, t);
+        const half2_t c = __builtin_bit_cast(half2_t, t) + k.zb;
+        p[i] = __builtin_bit_cast(uint32_t, c * d2);
       }
-      MOEQ_GLOBAL float* hout = (MOEQ_GLOBAL float*)(a.h + (size_t)(sl.base + m0 + r) * I);
-      const int col = n0 + wn * 16 + (lane & 15);
-      const float hv = silu(acc[0][i][0][j] * sc) * (acc[1][i][0][j] * sc);
-      if (ok) hout[col] = hv;
-      float rmax = fabsf(hv);
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
-      if (ok && (lane & 15) == 0) atomicMax(a.rowmax + sl.base + m0 + r, __float_as_uint(rmax));
     }
   }
+  return __builtin_bit_cast(half8, u32x4{p[0], p[1], p[2], p[3]});
 }
 
-// grid = m-tiles x (I / 64); tiles whose gate and up tensors are 2-4 bits
-// wide, from the 128-row list (BMT = 128) or the 64-row list (BMT = 64)
-template <int BMT>
-__global__ __launch_bounds__(512, 1) void gateup_rs_kernel(DecodeArgs a) {
-  extern __shared__ _Float16 lds_h[];
-  const int nN = a.I / 64;
-  const int32_t* tl = BMT == BM ? a.tiles : a.tiles_small;
+// The K loop of one wave.  ACT: the wave owns weight rows (else it only
+// stages activations, e.g. rows past the end of the tensor).  rc/rs: per row
+// tile, this lane's row chunk base and scale pairs; arow: the activation rows
+// this thread stages (row j * 16 + tid / 16 of the tile), as 16-byte pieces;
+// su/sm: the unit and piece of the thread's staging slot; zero: a zeroed
+// word (the scales of units past the row).
+template <int B, int NT, bool ACT>
+__device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD_RT],
+                                         const MOEQ_GLOBAL u32x2* const (&rs)[RD_RT], int Uk,
+                                         const MOEQ_GLOBAL u32x4* const (&arow)[RD_APT], int su, int sm,
+                                         const MOEQ_GLOBAL uint32_t* zero, char* lds, int tid, int lane,
+                                         f32x16 (&acc)[RD_RT][NT]) {
+  const int NS = (Uk + 3) / 4;      // K stages of 4 units
+  const int NSUB = 4 * NS;          // activation sub-stages
+  const int g = lane >> 5;
+  const RdConsts kc = rd_consts<B>();
+  RdUnit<B> raw[RD_RT][2];          // [row tile][unit 2g, 2g + 1 of the stage]
+  // fragment read offset of k step t (bytes within a sub-stage buffer):
+  // row c = lane % 32, piece (8 g + t) ^ (c % 16) = 8 (g ^ (c / 8 % 2)) + (t ^ (c % 8)),
+  // i.e. fbase ^ 16 t with fbase's bits 4-6 holding c % 8
+  const int fbase = (lane & 31) * 256 + (((g ^ ((lane >> 3) & 1)) << 7) | ((lane & 7) << 4));
+  char* wdst = lds + tid * 16;
+
+  // the staging pieces of sub-stage s (stage s / 4, block s % 4)
+  auto aload = [&](u32x4 (&v)[RD_APT], int s) {
+    const int unit = min(4 * (s >> 2) + su, Uk - 1);
+    const int off = unit * 16 + 4 * (s & 3) + sm;
+#pragma unroll
+    for (int j = 0; j < RD_APT; ++j) v[j] = arow[j][off];
+  };
+  auto astore = [&](const u32x4 (&v)[RD_APT], int buf) {
+#pragma unroll
+    for (int j = 0; j < RD_APT; ++j)
+      *reinterpret_cast<u32x4*>(wdst + buf * RD_SUB + j * (RD_THREADS * 16)) = v[j];
+  };
+  // chunk j / scale half h of this lane's two units in stage U, every row tile
+  auto rload_chunk = [&](int j, int U) {
+    if constexpr (ACT) {
+#pragma unroll
+      for (int v = 0; v < 2; ++v) {
+        const int uc = min(4 * U + 2 * g + v, Uk - 1);
+#pragma unroll
+        for (int r = 0; r < RD_RT; ++r) raw[r][v].c[j] = __builtin_nontemporal_load(rc[r] + (size_t)j * Uk + uc);
+      }
+    }
+  };
+  // (a unit past the row, in a partial last stage, reads its scales from a
+  // zeroed word, so its weights decode to zeros; the choice is made on the
+  // address, so no instruction waits for the loaded value)
+  auto rload_scale = [&](int h, int U) {
+    if constexpr (ACT) {
+#pragma unroll
+      for (int v = 0; v < 2; ++v) {
+        const int unit = 4 * U + 2 * g + v, uc = min(unit, Uk - 1);
+#pragma unroll
+        for (int r = 0; r < RD_RT; ++r) {
+          const MOEQ_GLOBAL uint32_t* src =
+              unit < Uk ? reinterpret_cast<const MOEQ_GLOBAL uint32_t*>(rs[r] + uc) + h : zero;
+          if (h == 0) raw[r][v].s.x = *src;
+          else raw[r][v].s.y = *src;
+        }
+      }
+    }
+  };
+
+  // prologue: stage 0's codes (for 4 bits, chunks 0 and 1: each later chunk
+  // is requested two sub-stages before its use); sub-stages 0 and 1 stored
+  if constexpr (ACT) {
+#pragma unroll
+    for (int j = 0; j < (B == 4 ? 2 : B); ++j) rload_chunk(j, 0);
+    rload_scale(0, 0);
+    rload_scale(1, 0);
+  }
+  u32x4 xv[RD_APT];
+  aload(xv, 0);
+  astore(xv, 0);
+  aload(xv, 1);
+  astore(xv, 1);
+  __syncthreads();
+
+  // k step TS of sub-stage Q: operands into FA / FB (fragment reads from LDS
+  // and the weight decode), then the matrix products of a step whose operands
+  // are ready.  The steps of a sub-stage are software-pipelined: the operands
+  // of step t + 1 are prepared among the products of step t, and a
+  // scheduling barrier keeps the compiler from hoisting later steps' decodes
+  // (which costs registers and spills).
+  half8 fa0[RD_RT], fb0[NT], fa1[RD_RT], fb1[NT];
+#define RD_OPERANDS(Q, TS, FA, FB)                                                                      \
+  do {                                                                                                  \
+    if constexpr (ACT) {                                                                                \
+      _Pragma("unroll") for (int T = 0; T < NT; ++T) FB[T] =                                            \
+          *reinterpret_cast<const half8*>(lds + (Q) * RD_SUB + T * (32 * 256) + (fbase ^ (16 * (TS))));  \
+      _Pragma("unroll") for (int r = 0; r < RD_RT; ++r) FA[r] =                                         \
+          rd_piece<B, Q, (TS) & 3>(raw[r][(TS) >> 2], kc);                                              \
+    }                                                                                                   \
+  } while (0)
+#define RD_PRODUCTS(FA, FB)                                                                             \
+  do {                                                                                                  \
+    if constexpr (ACT) {                                                                                \
+      _Pragma("unroll") for (int T = 0; T < NT; ++T)                                                    \
+      _Pragma("unroll") for (int r = 0; r < RD_RT; ++r) acc[r][T] =                                     \
+          __builtin_amdgcn_mfma_f32_32x32x16_f16(FA[r], FB[T], acc[r][T], 0, 0, 0);                     \
+    }                                                                                                   \
+  } while (0)
+#define RD_KSTEPS(Q)                                                                                    \
+  do {                                                                                                  \
+    RD_OPERANDS(Q, 0, fa0, fb0);                                                                        \
+    RD_OPERANDS(Q, 1, fa1, fb1);                                                                        \
+    RD_PRODUCTS(fa0, fb0);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 2, fa0, fb0);                                                                        \
+    RD_PRODUCTS(fa1, fb1);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 3, fa1, fb1);                                                                        \
+    RD_PRODUCTS(fa0, fb0);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 4, fa0, fb0);                                                                        \
+    RD_PRODUCTS(fa1, fb1);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 5, fa1, fb1);                                                                        \
+    RD_PRODUCTS(fa0, fb0);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 6, fa0, fb0);                                                                        \
+    RD_PRODUCTS(fa1, fb1);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_OPERANDS(Q, 7, fa1, fb1);                                                                        \
+    RD_PRODUCTS(fa0, fb0);                                                                              \
+    __builtin_amdgcn_sched_barrier(0);                                                                  \
+    RD_PRODUCTS(fa1, fb1);                                                                              \
+  } while (0)
+
+  // sub-stage s = 4U + Q in buffer Q: request sub-stage s + 2 into the
+  // staging registers, multiply sub-stage s while they arrive, store them
+  // into buffer (Q + 2) % 4 (free: its sub-stage s - 2 was read before the
+  // last barrier), and request the codes of stage U + 1 whose registers this
+  // sub-stage freed.  No branches: past the last sub-stage or stage the loads
+  // repeat the last one (clamped) and the stores go to buffers nobody reads
+  // again, so the compiler counts the outstanding loads exactly.
+#define RD_SUBSTAGE(Q)                                                                                  \
+  do {                                                                                                  \
+    aload(xv, min(4 * U + (Q) + 2, NSUB - 1));                                                          \
+    RD_KSTEPS(Q);                                                                                       \
+    astore(xv, ((Q) + 2) & 3);                                                                          \
+    const int Un_ = min(U + 1, NS - 1);                                                                 \
+    if constexpr (B == 4) rload_chunk(((Q) + 2) & 3, (Q) < 2 ? U : Un_);                               \
+    if constexpr (B == 2 && ((Q) & 1)) rload_chunk((Q) >> 1, Un_);                                     \
+    if constexpr (B == 3 && (Q) >= 1) rload_chunk((Q) - 1, Un_);                                        \
+    if constexpr ((Q) == 1) rload_scale(0, Un_);                                                        \
+    if constexpr ((Q) == 3) rload_scale(1, Un_);                                                        \
+    __syncthreads();                                                                                    \
+  } while (0)
+
+  for (int U = 0; U < NS; ++U) {
+    RD_SUBSTAGE(0);
+    RD_SUBSTAGE(1);
+    RD_SUBSTAGE(2);
+    RD_SUBSTAGE(3);
+  }
+#undef RD_SUBSTAGE
+#undef RD_KSTEPS
+#undef RD_PRODUCTS
+#undef RD_OPERANDS
+}
+
+// Width dispatch of one wave's K loop (B is uniform per wave: one tensor).
+template <int NT>
+__device__ __forceinline__ void rd_kloop_any(int bits, bool act, const MOEQ_GLOBAL u32x4* const (&rc)[RD_RT],
+                                             const MOEQ_GLOBAL u32x2* const (&rs)[RD_RT], int Uk,
+                                             const MOEQ_GLOBAL u32x4* const (&arow)[RD_APT], int su, int sm,
+                                             const MOEQ_GLOBAL uint32_t* zero, char* lds, int tid, int lane,
+                                             f32x16 (&acc)[RD_RT][NT]) {
+  if (!act)
+    rd_kloop<2, NT, false>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+  else if (bits == 2)
+    rd_kloop<2, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+  else if (bits == 3)
+    rd_kloop<3, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+  else
+    rd_kloop<4, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+}
+
+// Accumulator element v (0..15) of lane l in a 32 x 32 tile: row (weight row)
+// 8 (v / 4) + 4 (l / 32) + v % 4, column (token) l % 32.
+__device__ __forceinline__ int rd_acc_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
+
+// Gate/up tile: features [f0, f0 + 128) of one slot, tokens [m0, m0 + 64)
+// of its bucket (Mt of them real).  NT token tiles of 32 are multiplied.
+template <int NT>
+__device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int Mt, int f0, const TensorDev& tg,
+                               const TensorDev& tu, char* lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = a.H, I = a.I, Uk = H / kUnit;
+  constexpr int HW = RD_WAVES / 2;   // waves per projection
+  const TensorDev& t = wave < HW ? tg : tu;
+  const int bits = __builtin_amdgcn_readfirstlane(t.bits);
+  const int row0 = f0 + (wave % HW) * RD_WROWS;
+  const MOEQ_GLOBAL u32x4* rc[RD_RT];
+  const MOEQ_GLOBAL u32x2* rs[RD_RT];
+#pragma unroll
+  for (int r = 0; r < RD_RT; ++r) {
+    const int row = row0 + 32 * r + (lane & 31);
+    rc[r] = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)row * bits * Uk * 4));
+    rs[r] = gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (H / kBlock)));
+  }
+  // staging slots of this thread: rows j * 16 + tid / 16, piece (tid % 16) ^ (row % 16)
+  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
+  const MOEQ_GLOBAL u32x4* arow[RD_APT];
+#pragma unroll
+  for (int j = 0; j < RD_APT; ++j) {
+    int ar = j * (RD_THREADS / 16) + (tid >> 4);
+    ar = ar < Mt ? ar : 0;
+    const int tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
+    arow[j] = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H));
+  }
+  const int lp = (tid & 15) ^ ((tid >> 4) & 15);
+  f32x16 acc[RD_RT][NT];
+#pragma unroll
+  for (int r = 0; r < RD_RT; ++r)
+#pragma unroll
+    for (int T = 0; T < NT; ++T)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[r][T][v] = 0.f;
+  rd_kloop_any<NT>(bits, true, rc, rs, Uk, arow, lp >> 2, lp & 3, gptr(a.zeros), lds, tid, lane, acc);
+
+  // SwiGLU: the up waves hand their accumulators to the gate waves of the
+  // same features (the buffers are free after the loop's last barrier)
+  f32x16* xch = reinterpret_cast<f32x16*>(lds);
+  if (wave >= HW) {
+#pragma unroll
+    for (int r = 0; r < RD_RT; ++r)
+#pragma unroll
+      for (int T = 0; T < NT; ++T) xch[(((wave - HW) * RD_RT + r) * 2 + T) * 64 + lane] = acc[r][T];
+  }
+  __syncthreads();
+  if (wave >= HW) return;
+  const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
+#pragma unroll
+  for (int T = 0; T < NT; ++T) {
+    const int rr = T * 32 + (lane & 31);
+    const bool ok = rr < Mt;
+    float sc = 1.0f;
+    if (ok) {
+      const int tk = sl.shared >= 0 ? m0 + rr : perm[sl.base + m0 + rr] / a.k;
+      sc = __builtin_amdgcn_ldexpf(1.0f, xexp[tk]);
+    }
+    MOEQ_GLOBAL float* hout = (MOEQ_GLOBAL float*)(a.h + (size_t)(sl.base + m0 + rr) * I + row0);
+    float rmax = 0.0f;
+#pragma unroll
+    for (int r = 0; r < RD_RT; ++r) {
+      const f32x16 u = xch[((wave * RD_RT + r) * 2 + T) * 64 + lane];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f32x4 hv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int v = 4 * q + i;
+          hv[i] = silu(acc[r][T][v] * sc) * (u[v] * sc);
+          rmax = fmaxf(rmax, fabsf(hv[i]));
+        }
+        if (ok) *reinterpret_cast<MOEQ_GLOBAL f32x4*>(hout + 32 * r + rd_acc_row(4 * q, lane)) = hv;
+      }
+    }
+    rmax = fmaxf(rmax, __shfl_xor(rmax, 32, 64));
+    if (ok && lane < 32) atomicMax(a.rowmax + sl.base + m0 + rr, __float_as_uint(rmax));
+  }
+}
+
+// Down tile: output features [n0, n0 + 256) (rows of the down tensor) of one
+// slot, tokens [m0, m0 + 64); results times the routing weight are the
+// slot's partial rows.
+template <int NT>
+__device__ void rd_down_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int Mt, int n0, const TensorDev& td,
+                             char* lds) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int H = a.H, I = a.I, Uk = I / kUnit;
+  const int bits = __builtin_amdgcn_readfirstlane(td.bits);
+  const int row0 = n0 + wave * RD_WROWS;
+  const bool act = row0 < H;   // H is a multiple of 128 and of 64: a wave's rows are all in or all out
+  const MOEQ_GLOBAL u32x4* rc[RD_RT];
+  const MOEQ_GLOBAL u32x2* rs[RD_RT];
+#pragma unroll
+  for (int r = 0; r < RD_RT; ++r) {
+    const int row = act ? row0 + 32 * r + (lane & 31) : 0;
+    rc[r] = gptr(reinterpret_cast<const u32x4*>(td.codes + (size_t)row * bits * Uk * 4));
+    rs[r] = gptr(reinterpret_cast<const u32x2*>(td.scales + (size_t)row * (I / kBlock)));
+  }
+  const MOEQ_GLOBAL u32x4* arow[RD_APT];
+#pragma unroll
+  for (int j = 0; j < RD_APT; ++j) {
+    int ar = j * (RD_THREADS / 16) + (tid >> 4);
+    ar = ar < Mt ? ar : 0;
+    arow[j] = gptr(reinterpret_cast<const u32x4*>(a.h16 + (size_t)(sl.base + m0 + ar) * I));
+  }
+  const int lp = (tid & 15) ^ ((tid >> 4) & 15);
+  f32x16 acc[RD_RT][NT];
+#pragma unroll
+  for (int r = 0; r < RD_RT; ++r)
+#pragma unroll
+    for (int T = 0; T < NT; ++T)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[r][T][v] = 0.f;
+  rd_kloop_any<NT>(bits, act, rc, rs, Uk, arow, lp >> 2, lp & 3, gptr(a.zeros), lds, tid, lane, acc);
+  if (!act) return;
+
+  const MOEQ_GLOBAL uint32_t* rowmax = gptr((const uint32_t*)a.rowmax);
+  const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
+#pragma unroll
+  for (int T = 0; T < NT; ++T) {
+    const int rr = T * 32 + (lane & 31);
+    if (rr >= Mt) continue;
+    const int e = max((int)((rowmax[sl.base + m0 + rr] >> 23) & 0xFFu) - 127 - 14, -100);
+    int prow;
+    float wv;
+    if (sl.shared >= 0) {
+      prow = a.n * a.k + sl.shared * a.n + m0 + rr;
+      wv = 1.0f;
+    } else {
+      prow = perm[sl.base + m0 + rr];
+      wv = gptr(a.w)[prow];
+    }
+    const float sc = __builtin_amdgcn_ldexpf(wv, e);
+    MOEQ_GLOBAL float* pout = (MOEQ_GLOBAL float*)(a.partial + (size_t)prow * H + row0);
+#pragma unroll
+    for (int r = 0; r < RD_RT; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[r][T][4 * q + i] * sc;
+        *reinterpret_cast<MOEQ_GLOBAL f32x4*>(pout + 32 * r + rd_acc_row(4 * q, lane)) = v;
+      }
+  }
+}
+
+// grid: tile_grid(max m-tiles, n-tiles); tiles of slots whose gate and up
+// (down) tensors are both 2-4 bits wide
+__global__ __launch_bounds__(RD_THREADS, 2) void gateup_rd_kernel(DecodeArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds_c[];
+  const int nN = a.I / (RD_ROWS / 2);
   int mt, nt;
-  if (!tile_of_wg(blockIdx.x, tl[0], nN, &mt, &nt)) return;
-  const SlotInfo sl = slot_of(a, tl[1 + 2 * mt]);
-  const int m0 = tl[2 + 2 * mt];
+  if (!tile_of_wg(blockIdx.x, a.tiles_rd[0], nN, &mt, &nt)) return;
+  const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
+  const int m0 = a.tiles_rd[2 + 2 * mt];
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
-  if (!tg.codes || !tu.codes) return;
-  if (tg.bits > 4 || tu.bits > 4) return;
-  gateup_rs_body<BMT>(gemm_args(a), sl, m0, nt * 64, tg, tu, lds_h);
+  if (!tg.codes || !tu.codes || tg.bits > 4 || tu.bits > 4) return;
+  const int Mt = min(RD_T, sl.M - m0);
+  const GemmArgs g = gemm_args(a);
+  if (Mt <= 32)
+    rd_gateup_tile<1>(g, sl, m0, Mt, nt * (RD_ROWS / 2), tg, tu, lds_c);
+  else
+    rd_gateup_tile<2>(g, sl, m0, Mt, nt * (RD_ROWS / 2), tg, tu, lds_c);
+}
+
+__global__ __launch_bounds__(RD_THREADS, 2) void down_rd_kernel(DecodeArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds_c[];
+  const int nN = (a.H + RD_ROWS - 1) / RD_ROWS;
+  int mt, nt;
+  if (!tile_of_wg(blockIdx.x, a.tiles_rd[0], nN, &mt, &nt)) return;
+  const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
+  const int m0 = a.tiles_rd[2 + 2 * mt];
+  const TensorDev td = a.desc[sl.desc * 3 + 2];
+  if (!td.codes || td.bits > 4) return;
+  const int Mt = min(RD_T, sl.M - m0);
+  const GemmArgs g = gemm_args(a);
+  if (Mt <= 32)
+    rd_down_tile<1>(g, sl, m0, Mt, nt * RD_ROWS, td, lds_c);
+  else
+    rd_down_tile<2>(g, sl, m0, Mt, nt * RD_ROWS, td, lds_c);
+}
+
+// Diagnostic: one tensor through the grouped GEMMs' decoders, one thread per
+// (row, unit): binary16 d * (c - z) bit patterns in natural weight order
+// (rd_piece for 2-4 bits, decode_blk for 5/6/8).
+template <int B>
+__global__ __launch_bounds__(256) void dequant_gemm_kernel(TensorDev t, uint16_t* out) {
+  const int U = t.K / kUnit;
+  const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (long long)t.rows * U) return;
+  const int r = (int)(gid / U), u = (int)(gid % U);
+  const MOEQ_GLOBAL u32x4* rc = row_chunks(t, B, r);
+  const MOEQ_GLOBAL uint16_t* rs = gptr(t.scales + (size_t)r * (t.K / kBlock));
+  u32x4* o = reinterpret_cast<u32x4*>(out + (size_t)r * t.K + kUnit * u);
+  if constexpr (B <= 4) {
+    RdUnit<B> un;
+#pragma unroll
+    for (int j = 0; j < B; ++j) un.c[j] = rc[(size_t)j * U + u];
+    un.s = *reinterpret_cast<const MOEQ_GLOBAL u32x2*>(rs + 4 * u);
+    const RdConsts kc = rd_consts<B>();
+#define DQG(Q, M) o[4 * (Q) + (M)] = __builtin_bit_cast(u32x4, rd_piece<B, Q, M>(un, kc))
+    DQG(0, 0); DQG(0, 1); DQG(0, 2); DQG(0, 3);
+    DQG(1, 0); DQG(1, 1); DQG(1, 2); DQG(1, 3);
+    DQG(2, 0); DQG(2, 1); DQG(2, 2); DQG(2, 3);
+    DQG(3, 0); DQG(3, 1); DQG(3, 2); DQG(3, 3);
+#undef DQG
+  } else {
+    __attribute__((aligned(16))) _Float16 blk[32];
+#define DQW(Q)                                                                    \
+  do {                                                                            \
+    const RawBlk rb = load_blk<B, Q>(rc, rs, U, u);                               \
+    decode_blk<B>(rb, ((Q) * B) & 3, ((Q) & 1) != 0, blk);                        \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i) o[4 * (Q) + i] = reinterpret_cast<const u32x4*>(blk)[i]; \
+  } while (0)
+    DQW(0); DQW(1); DQW(2); DQW(3);
+#undef DQW
+  }
 }
 
 }  // namespace
 
-int prefill_max_mtiles(int n, int k, int S, int n_kept) {
+int prefill_max_tiles(int n, int k, int S, int n_kept, int rows) {
   const long long nk = (long long)n * k;
-  const long long routed = (nk + BM - 1) / BM + (nk < n_kept ? nk : n_kept);
-  return (int)(routed + (long long)S * ((n + BM - 1) / BM));
+  const long long routed = (nk + rows - 1) / rows + (nk < n_kept ? nk : n_kept);
+  return (int)(routed + (long long)S * ((n + rows - 1) / rows));
 }
 
-int prefill_max_small(int n, int k, int S, int n_kept) {
-  const long long nk = (long long)n * k;
-  return (int)((nk < n_kept ? nk : n_kept) + S);
-}
+int prefill_max_mtiles(int n, int k, int S, int n_kept) { return prefill_max_tiles(n, k, S, n_kept, BM); }
+int prefill_max_rtiles(int n, int k, int S, int n_kept) { return prefill_max_tiles(n, k, S, n_kept, kRdTile); }
 
 namespace {
 
-// sets the LDS limit of a GEMM kernel once per process, then launches it
+// Raises a GEMM kernel's dynamic LDS limit (once per device and kernel), then
+// launches it.
+constexpr int kMaxDevices = 64;
 template <typename K>
-hipError_t launch_gemm(K kernel, bool& attr, int grid, size_t lds, hipStream_t s, const DecodeArgs& a) {
-  if (!attr) {
-    const hipError_t e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+hipError_t launch_gemm(K kernel, std::atomic<uint64_t>& done, int block, int grid, size_t lds, hipStream_t s,
+                       const DecodeArgs& a) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < kMaxDevices ? 1ull << dev : 0ull;
+  if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    attr = true;
+    done.fetch_or(bit, std::memory_order_release);
   }
-  kernel<<<grid, 512, lds, s>>>(a);
+  kernel<<<grid, block, lds, s>>>(a);
   return hipGetLastError();
 }
 
+std::atomic<uint64_t> g_attr_gu_rd{0}, g_attr_dn_rd{0}, g_attr_gu_w{0}, g_attr_dn_w{0};
+
 }  // namespace
+
+hipError_t launch_dequant_gemm(const TensorDev& t, uint16_t* out, hipStream_t s) {
+  const long long n = (long long)t.rows * (t.K / kUnit);
+  const int grid = (int)((n + 255) / 256);
+  switch (t.bits) {
+    case 2: dequant_gemm_kernel<2><<<grid, 256, 0, s>>>(t, out); break;
+    case 3: dequant_gemm_kernel<3><<<grid, 256, 0, s>>>(t, out); break;
+    case 4: dequant_gemm_kernel<4><<<grid, 256, 0, s>>>(t, out); break;
+    case 5: dequant_gemm_kernel<5><<<grid, 256, 0, s>>>(t, out); break;
+    case 6: dequant_gemm_kernel<6><<<grid, 256, 0, s>>>(t, out); break;
+    case 8: dequant_gemm_kernel<8><<<grid, 256, 0, s>>>(t, out); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s) {
   prefill_tiles_kernel<<<1, 1024, 0, s>>>(a);
   return hipGetLastError();
 }
 
-hipError_t launch_gateup_prefill_big(const DecodeArgs& a, hipStream_t s) {
-  const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
-  const int grid = tile_grid(a.max_mtiles, a.I / BN);
-  static bool attr_n = false, attr_w = false;
-  hipError_t e = launch_gemm(gateup_rs_kernel<BM>, attr_n, tile_grid(a.max_mtiles, a.I / 64), rs_lds(BM), s, a);
-  if (e == hipSuccess && a.wide_gateup) e = launch_gemm(gateup_gemm8_kernel<true>, attr_w, grid, lds, s, a);
-  return e;
-}
-
-hipError_t launch_gateup_prefill_small(const DecodeArgs& a, hipStream_t s2) {
-  static bool attr_s = false;
-  return launch_gemm(gateup_rs_kernel<BM / 2>, attr_s, tile_grid(a.max_small, a.I / 64), rs_lds(BM / 2), s2, a);
-}
-
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
-  hipError_t e = launch_prefill_tiles(a, s);
-  if (e == hipSuccess) e = launch_gateup_prefill_big(a, s);
-  if (e == hipSuccess) e = launch_gateup_prefill_small(a, s);
+  hipError_t e = launch_gemm(gateup_rd_kernel, g_attr_gu_rd, RD_THREADS, tile_grid(a.max_rtiles, a.I / (RD_ROWS / 2)),
+                             RD_LDS, s, a);
+  if (e == hipSuccess && a.wide_gateup) {
+    const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
+    e = launch_gemm(gateup_gemm8_kernel, g_attr_gu_w, 512, tile_grid(a.max_mtiles, a.I / BN), lds, s, a);
+  }
   return e;
 }
 
@@ -1027,11 +1275,12 @@ hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) {
   h16_kernel<<<(rows + 3) / 4, 256, 0, s>>>(a.h, a.rowmax, rows, a.I, a.h16);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
-  const int grid = tile_grid(a.max_mtiles, a.H / BN);
-  static bool attr_n = false, attr_w = false;
-  e = launch_gemm(down_gemm8_kernel<false>, attr_n, grid, lds, s, a);
-  if (e == hipSuccess && a.wide_down) e = launch_gemm(down_gemm8_kernel<true>, attr_w, grid, lds, s, a);
+  e = launch_gemm(down_rd_kernel, g_attr_dn_rd, RD_THREADS, tile_grid(a.max_rtiles, (a.H + RD_ROWS - 1) / RD_ROWS),
+                  RD_LDS, s, a);
+  if (e == hipSuccess && a.wide_down) {
+    const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
+    e = launch_gemm(down_gemm8_kernel, g_attr_dn_w, 512, tile_grid(a.max_mtiles, a.H / BN), lds, s, a);
+  }
   return e;
 }
 

@@ -23,6 +23,17 @@ __global__ __launch_bounds__(256) void fill_u8_kernel(uint8_t* p, int n, uint8_t
   if (i < n) p[i] = v;
 }
 
+// Host values handed to the device through the kernel arguments, which the
+// launch copies: the caller's buffer may change as soon as the launch returns.
+constexpr int kArgFloats = 256;
+struct HostFloats {
+  float v[kArgFloats];
+};
+__global__ __launch_bounds__(kArgFloats) void store_floats_kernel(float* dst, int n, HostFloats src) {
+  const int i = threadIdx.x;
+  if (i < n) dst[i] = src.v[i];
+}
+
 __global__ __launch_bounds__(256) void expert_stats_kernel(const int32_t* offsets, const int32_t* perm,
                                                            const float* w, int E, int n, double alpha,
                                                            double* importance, int32_t* counts) {
@@ -57,6 +68,18 @@ __global__ __launch_bounds__(1024) void select_kernel(const double* importance, 
 hipError_t launch_fill_u8(uint8_t* p, int n, uint8_t v, hipStream_t s) {
   fill_u8_kernel<<<(n + 255) / 256, 256, 0, s>>>(p, n, v);
   return hipGetLastError();
+}
+
+hipError_t launch_store_host_floats(float* dst, const float* src, int n, hipStream_t s) {
+  for (int i = 0; i < n; i += kArgFloats) {
+    HostFloats h{};
+    const int m = n - i < kArgFloats ? n - i : kArgFloats;
+    for (int j = 0; j < m; ++j) h.v[j] = src ? src[i + j] : 0.0f;
+    store_floats_kernel<<<1, kArgFloats, 0, s>>>(dst + i, m, h);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm, const float* w, int E, int n,

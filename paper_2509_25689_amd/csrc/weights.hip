@@ -1,6 +1,6 @@
 // Weight-format kernels: canonical packing -> device layout (repack), device
-// layout -> float32 (dequantize, a diagnostic that runs the same unpacking as
-// the matrix-vector kernels), and float32 -> canonical packing (quantize).
+// layout -> float32 through each decoder the products use (diagnostics), and
+// float32 -> canonical packing (quantize).
 //
 // The format is the symmetric block format standing in for the paper's
 // per-tensor low-bit formats (Section 3.3): weight = d * (c - 2^(b-1)), one
@@ -82,7 +82,8 @@ __global__ __launch_bounds__(256) void repack_kernel(const uint8_t* canon, int r
     for (int e = 0; e < 4; ++e) row[((size_t)j * U + u) * 4 + e] = w[4 * j + e];
 }
 
-// one thread per (row, unit): the matrix-vector kernels' unpacking, then
+// one thread per (row, unit): the bfloat16-form unpacking of block_pairs
+// (the 2-64-token gate/up and the 5/6/8-bit matrix-vector kernels), then
 // d * (c - 2^(b-1)) exactly
 template <int B>
 __global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {
@@ -116,6 +117,35 @@ __global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {
         o[32 * q + 2 * P] = d * (c0 - z);
         o[32 * q + 2 * P + 1] = d * (c1 - z);
       }
+    }
+  }
+}
+
+// one thread per (row, unit): the binary16-subnormal code pairs of
+// block_pairs_sub (the one-token gate/up and the 2-4-bit down matrix-vector
+// kernels).  Pair P's two halves are c * 2^(k-24) with k = sub_shift<B>(P);
+// c is rebuilt exactly as that value times 2^(24-k), then d * (c - 2^(b-1)).
+template <int B>
+__global__ __launch_bounds__(256) void dequant_sub_kernel(TensorDev t, float* out) {
+  const int U = t.K / kUnit;
+  const long long gid = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (long long)t.rows * U) return;
+  const int r = (int)(gid / U), u = (int)(gid % U);
+  uint32_t w[4 * B];
+  load_unit<B>(t.codes + (size_t)r * B * U * 4, U, u, w);
+  const uint16_t* sc = t.scales + (size_t)r * (t.K / kBlock) + 4 * u;
+  const float z = (float)(1 << (B - 1));
+  float* o = out + (size_t)r * t.K + kUnit * u;
+  for (int q = 0; q < 4; ++q) {
+    const float d = half_to_float(sc[q]);
+    uint32_t p[16];
+    block_pairs_sub<B>(w + q * B, p);
+#pragma unroll
+    for (int P = 0; P < 16; ++P) {
+      const float up = __builtin_amdgcn_ldexpf(1.0f, 24 - sub_shift<B>(P));
+      const float c0 = half_to_float(p[P] & 0xFFFFu) * up, c1 = half_to_float(p[P] >> 16) * up;
+      o[32 * q + 2 * P] = d * (c0 - z);
+      o[32 * q + 2 * P + 1] = d * (c1 - z);
     }
   }
 }
@@ -178,6 +208,18 @@ hipError_t launch_repack(const uint8_t* canon, int rows, int K, int bits, uint32
     case 5: repack_kernel<5><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
     case 6: repack_kernel<6><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
     case 8: repack_kernel<8><<<grid, 256, 0, s>>>(canon, rows, K, dev); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant_sub(const TensorDev& t, float* out, hipStream_t s) {
+  const long long n = (long long)t.rows * (t.K / kUnit);
+  const int grid = (int)((n + 255) / 256);
+  switch (t.bits) {
+    case 2: dequant_sub_kernel<2><<<grid, 256, 0, s>>>(t, out); break;
+    case 3: dequant_sub_kernel<3><<<grid, 256, 0, s>>>(t, out); break;
+    case 4: dequant_sub_kernel<4><<<grid, 256, 0, s>>>(t, out); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -30,6 +30,7 @@ STATUS_NAMES = {0: "OK", -1: "INVALID_ARG", -2: "UNSUPPORTED", -3: "OUT_OF_MEMOR
 MOEQ_PROJ_GATE, MOEQ_PROJ_UP, MOEQ_PROJ_DOWN = 0, 1, 2
 MOEQ_WEIGHTS_HOST, MOEQ_WEIGHTS_DEVICE = 0, 1
 MOEQ_PATH_AUTO, MOEQ_PATH_DECODE, MOEQ_PATH_PREFILL = 0, 1, 2
+MOEQ_DECODER_EXACT, MOEQ_DECODER_GEMV_SUBNORMAL, MOEQ_DECODER_GEMM_F16 = 0, 1, 2
 
 
 class MoeqError(RuntimeError):
@@ -94,6 +95,7 @@ def _load():
         "moeq_route": [P, P, I32, P, P, P],
         "moeq_bucket": [P, P, I32, P, P, P],
         "moeq_dequant": [P, I32, I32, P, P],
+        "moeq_dequant_as": [P, I32, I32, I32, P, P],
         "moeq_quantize": [P, I32, I32, I32, P, P, P],
         "moeq_layer_bytes": [P, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)],
         "moeq_set_stage_events": [P, ctypes.POINTER(P), I32],
@@ -222,6 +224,10 @@ def moeq_dequant(layer, expert, proj, out, stream=0):
     _check(lib.moeq_dequant(layer, expert, proj, out, stream or None))
 
 
+def moeq_dequant_as(layer, expert, proj, decoder, out, stream=0):
+    _check(lib.moeq_dequant_as(layer, expert, proj, decoder, out, stream or None))
+
+
 def moeq_quantize(w, rows, K, bits, codes, scales, stream=0):
     _check(lib.moeq_quantize(w, rows, K, bits, codes, scales, stream or None))
 
@@ -309,6 +315,13 @@ class Layer:
             for p, t in enumerate(triple):
                 s[3 * i + p] = moeq_qtensor(int(t["bits"]), _addr(t["codes"]), _addr(t["scales"]))
         loc = MOEQ_WEIGHTS_DEVICE if device_weights else MOEQ_WEIGHTS_HOST
+        self.device = None
+        try:
+            import torch
+            if torch.cuda.is_available():
+                self.device = torch.cuda.current_device()
+        except ImportError:
+            pass
         self.handle = moeq_layer_create(self.cfg, self._mask.ctypes.data,
                                         0 if self._bias is None else self._bias.ctypes.data,
                                         r, s if S else None, loc)
@@ -324,6 +337,22 @@ class Layer:
         except Exception:
             pass
 
+    def _check_tensor(self, name, t, dtype, shape):
+        """Shape, dtype, layout and device of a tensor handed to the library:
+        the kernels trust these, and a wrong one would make them read or
+        write outside the buffer."""
+        import torch
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name} must be a torch tensor")
+        if t.dtype != dtype:
+            raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device.type != "cuda" or (self.device is not None and t.device.index != self.device):
+            raise ValueError(f"{name} must be on cuda:{self.device}, got {t.device}")
+
     @staticmethod
     def _stream(stream):
         if stream is not None:
@@ -335,9 +364,13 @@ class Layer:
         """x: bf16 CUDA tensor [n, H]; logits: float32 CUDA tensor [n, E], or None
         to let the layer compute them with its router weight -> y float32 [n, H]."""
         import torch
-        n = x.shape[0]
+        n = x.shape[0] if x.dim() == 2 else -1
+        self._check_tensor("x", x, torch.bfloat16, (n, self.shape.hidden))
+        if logits is not None:
+            self._check_tensor("logits", logits, torch.float32, (n, self.shape.n_experts))
         if y is None:
             y = torch.empty((n, self.shape.hidden), dtype=torch.float32, device=x.device)
+        self._check_tensor("y", y, torch.float32, (n, self.shape.hidden))
         moeq_forward(self.handle, x.data_ptr(), 0 if logits is None else logits.data_ptr(), n,
                      y.data_ptr(), self._stream(stream))
         return y
@@ -359,14 +392,16 @@ class Layer:
     def router_logits(self, x, stream=None):
         """x: bf16 CUDA tensor [n, H] -> float32 logits [n, E] from the set router weight."""
         import torch
-        n = x.shape[0]
+        n = x.shape[0] if x.dim() == 2 else -1
+        self._check_tensor("x", x, torch.bfloat16, (n, self.shape.hidden))
         out = torch.empty((n, self.shape.n_experts), dtype=torch.float32, device=x.device)
         moeq_router_logits(self.handle, x.data_ptr(), n, out.data_ptr(), self._stream(stream))
         return out
 
     def route(self, logits, stream=None):
         import torch
-        n = logits.shape[0]
+        n = logits.shape[0] if logits.dim() == 2 else -1
+        self._check_tensor("logits", logits, torch.float32, (n, self.shape.n_experts))
         idx = torch.empty((n, self.shape.top_k), dtype=torch.int32, device=logits.device)
         w = torch.empty((n, self.shape.top_k), dtype=torch.float32, device=logits.device)
         moeq_route(self.handle, logits.data_ptr(), n, idx.data_ptr(), w.data_ptr(),
@@ -375,7 +410,8 @@ class Layer:
 
     def bucket(self, idx, stream=None):
         import torch
-        n = idx.shape[0]
+        n = idx.shape[0] if idx.dim() == 2 else -1
+        self._check_tensor("idx", idx, torch.int32, (n, self.shape.top_k))
         offsets = torch.empty(self.shape.n_experts + 1, dtype=torch.int32, device=idx.device)
         perm = torch.empty(n * self.shape.top_k, dtype=torch.int32, device=idx.device)
         moeq_bucket(self.handle, idx.data_ptr(), n, offsets.data_ptr(), perm.data_ptr(),
@@ -387,6 +423,17 @@ class Layer:
         rows, K = self.shape.rows_cols(proj)
         out = torch.empty((rows, K), dtype=torch.float32, device="cuda")
         moeq_dequant(self.handle, expert, proj, out.data_ptr(), self._stream(stream))
+        return out
+
+    def dequant_as(self, expert, proj, decoder, stream=None):
+        """One tensor through one of the library's decoders: float32 [rows, K]
+        (MOEQ_DECODER_EXACT, MOEQ_DECODER_GEMV_SUBNORMAL) or binary16 bit
+        patterns as int16 [rows, K] (MOEQ_DECODER_GEMM_F16)."""
+        import torch
+        rows, K = self.shape.rows_cols(proj)
+        dt = torch.int16 if decoder == MOEQ_DECODER_GEMM_F16 else torch.float32
+        out = torch.empty((rows, K), dtype=dt, device="cuda")
+        moeq_dequant_as(self.handle, expert, proj, decoder, out.data_ptr(), self._stream(stream))
         return out
 
     def set_path(self, path):

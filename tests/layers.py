@@ -55,16 +55,43 @@ def random_packed_layer(shape, plan, key, mask=None):
     return LayerData(shape, mask, bits_r, bits_s, make)
 
 
-def oracle_forward(data, x_bits, idx, w):
-    """The oracle's layer output for the given routing."""
-    cache = {}
+class DeviceLayerData(LayerData):
+    """Random packed tensors drawn on the GPU per tensor key
+    (synth.device_random_packed): the layer is built from the device tensors,
+    and the oracle regenerates any tensor it needs and copies it to the host."""
 
-    def routed(e):
-        if e not in cache:
-            cache[e] = data.dequant("r", e)
-        return cache[e]
+    def __init__(self, shape, plan, key, mask=None):
+        import torch
+        self._torch = torch
+        if mask is None:
+            mask = synth.expert_mask(shape, key)
+        bits_r, bits_s = synth.bit_plan(shape, plan, key)
+        self.key = key
+
+        def make(kind, e, p, bits):
+            dev = self.device_tensor(kind, e, p)
+            return dict(bits=bits, codes=dev["codes"].cpu().numpy(),
+                        scales=dev["scales"].cpu().numpy().view(np.uint16))
+        super().__init__(shape, mask, bits_r, bits_s, make)
+
+    def device_tensor(self, kind, e, p):
+        bits = int(self.bits_r[e, p] if kind == "r" else self.bits_s[e, p])
+        rows, K = self.shape.rows_cols(p)
+        codes, scales = synth.device_random_packed(self._torch, rows, K, bits, self.key, kind, e, p)
+        return dict(bits=bits, codes=codes, scales=scales)
+
+    def make_layer(self, moeq, max_tokens, **kw):
+        routed = {int(e): tuple(self.device_tensor("r", e, p) for p in range(3)) for e in np.nonzero(self.mask)[0]}
+        shared = [tuple(self.device_tensor("s", s, p) for p in range(3)) for s in range(self.shape.n_shared)]
+        self._torch.cuda.synchronize()
+        return moeq.Layer(self.shape, self.mask, routed, shared, max_tokens=max_tokens, device_weights=True, **kw)
+
+
+def oracle_forward(data, x_bits, idx, w):
+    """The oracle's layer output for the given routing.  Every expert is
+    dequantized once, when the oracle asks for it, and not kept."""
     shared = [data.dequant("s", s) for s in range(data.shape.n_shared)]
-    return moe.moe_forward(x_bits, idx, w, routed, shared)
+    return moe.moe_forward(x_bits, idx, w, lambda e: data.dequant("r", e), shared)
 
 
 def scaled_bits(bits, s):

@@ -44,6 +44,23 @@ def _create(cfg, mask=None, bias=None, bits=4, codes=1, scales=1, loc=0, out=Tru
     return st, handle
 
 
+def test_peaks_library_exports_every_header_function():
+    """The benchmark's roofline probes: a library of their own, every function
+    of include/moeq_peaks.h exported."""
+    from paper_2509_25689_amd import peaks
+    lib = peaks.load()
+    names = peaks.header_functions()
+    assert set(names) == {"moeq_peaks_stream_read", "moeq_peaks_read_workgroups", "moeq_peaks_mfma",
+                          "moeq_peaks_mfma_flops"}
+    for name in names:
+        assert hasattr(lib, name), name
+    # host-only figures and argument checks (no GPU call is made)
+    assert lib.moeq_peaks_read_workgroups(1 << 30) == (1 << 30) // (256 * 8 * 16)
+    assert lib.moeq_peaks_mfma_flops(2, 3) == 2 * 4 * 3 * 8 * 2 * 16 * 16 * 32
+    assert lib.moeq_peaks_stream_read(None, 16, None, None) != 0
+    assert lib.moeq_peaks_mfma(0, 1, None, None) != 0
+
+
 @pytest.mark.parametrize("field,value,status", [
     ("hidden", 0, moeq.MOEQ_ERR_INVALID_ARG),
     ("hidden", 500, moeq.MOEQ_ERR_INVALID_ARG),          # not a multiple of 32
@@ -155,6 +172,7 @@ def test_entry_points_reject_null_layer():
     assert L.moeq_route(None, 1, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_bucket(None, 1, 1, 1, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_dequant(None, 0, 0, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert L.moeq_dequant_as(None, 0, 0, moeq.MOEQ_DECODER_GEMM_F16, 1, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_set_path(None, 0) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_layer_bytes(None, None, None) == moeq.MOEQ_ERR_INVALID_ARG
     assert L.moeq_set_router_weight(None, 1, moeq.MOEQ_WEIGHTS_HOST) == moeq.MOEQ_ERR_INVALID_ARG

@@ -46,7 +46,7 @@ def test_forward_at_size_limits(gpu_lib, big, n, path):
     y = L.forward(_dev(x_bits.view(np.int16), torch.bfloat16), _dev(logits))
     torch.cuda.synchronize()
     L.set_path(gpu_lib.MOEQ_PATH_AUTO)
-    rows = np.arange(n) if n <= 16 else np.array([0, n // 2, n - 1])
+    rows = np.arange(n)
     idx, w = router.route(logits[rows], data.mask, n_group=shape.n_group, topk_group=shape.topk_group,
                           top_k=shape.top_k, group_topn=shape.group_topn, norm_topk=shape.norm_topk,
                           routed_scale=shape.routed_scale)

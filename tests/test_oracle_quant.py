@@ -153,3 +153,32 @@ def test_tensor_bytes_v3():
     # gate/up [2048 x 7168] at 3 bits, down [7168 x 2048] at 4 bits
     assert quant.tensor_bytes(2048, 7168, 3) == 6_422_528
     assert quant.tensor_bytes(7168, 2048, 4) == 8_257_536
+
+
+def test_dequantize_half_exact_when_representable():
+    """d a power of two: every d * (c - z) has at most 8 significant bits, so
+    its binary16 rounding is the value itself (closed form)."""
+    for bits in BITS:
+        z = quant.zero_point(bits)
+        codes = np.arange(1 << bits, dtype=np.uint8)
+        codes = np.resize(codes, 64).reshape(2, 32)
+        scales = np.array([[0x2000], [0x3C00]], np.uint16)     # 2^-7 and 1.0
+        got = quant.dequantize_half(codes, scales, bits).view(np.float16).astype(np.float64)
+        want = (codes.astype(np.float64) - z) * np.array([[2.0 ** -7], [1.0]])
+        assert np.array_equal(got, want), bits
+
+
+def test_dequantize_half_rounds_worked_example():
+    """d = 1 + 2^-10 (0x3C01): 7 d = 7 + 7 * 2^-10 needs 13 bits; binary16 keeps
+    11 (spacing 2^-8 in [4, 8)), and 7 * 2^-10 = 1.75 * 2^-8 rounds up to
+    2^-7, so 7d -> 7 + 2^-7 (0x4702).  -3 d = -(3 + 3 * 2^-10): spacing 2^-9 in
+    [2, 4), 3 * 2^-10 = 1.5 * 2^-9 is a tie between 2^-9 and 2^-8 -> even
+    mantissa 2^-8: -(3 + 2^-8) = 0xC202.  d (c - z) with c = z: +0 or -0."""
+    codes = np.full((1, 32), 8, np.uint8)
+    codes[0, 0] = 15          # c - z = 7
+    codes[0, 1] = 5           # c - z = -3
+    scales = np.array([[0x3C01]], np.uint16)
+    got = quant.dequantize_half(codes, scales, 4)
+    assert got[0, 0] == 0x4702
+    assert got[0, 1] == 0xC202
+    assert np.all(got[0, 2:].view(np.float16) == 0)
