@@ -302,6 +302,26 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
                                    int32_t n_tokens, double alpha, double retain, double* importance,
                                    uint8_t* mask, int32_t* counts, void* stream);
 
+/* moeq_expert_importance without any allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops, hosts
+ * that forbid hipMalloc): identical arguments, results and errors, but the
+ * scratch lives in a 16 MiB array compiled into the library, one per device,
+ * held until the process ends.  The scratch of a call is
+ *   the sum, each part rounded up to a multiple of 256, of
+ *                       16 * n_tokens * top_k  (ids, weights, ranks, permutation)
+ *                     + 4 * ceil(n_tokens / 64) * n_experts  (per-chunk counts)
+ *                     + 13 * n_experts + 8  (offsets, active list, mask, bias)
+ * bytes; a call that needs more than 16 MiB returns CAPACITY (e.g. about
+ * 100k tokens at top_k 8 over 256 experts fit).  The array keeps the last
+ * call's contents and no part of it needs to start cleared.  Calls on one
+ * device share the array, so calls that overlap in time on one device (two
+ * streams, or two host threads) race: order them on one stream.  The first
+ * call on a device looks up the array's device address (no allocation).
+ * Errors: INVALID_ARG, CAPACITY, DEVICE. */
+moeq_status moeq_expert_importance_noalloc(const moeq_config* cfg, const float* score_bias, const float* logits,
+                                           int32_t n_tokens, double alpha, double retain, double* importance,
+                                           uint8_t* mask, int32_t* counts, void* stream);
+
 /* ---- Mixed-precision bit allocation (Section 3.3), host only ----------------
  * These entry points run on the host, make no HIP call and need no device.
  *

@@ -602,12 +602,46 @@ moeq_status moeq_router_logits(moeq_layer* L, const void* x, int32_t n, float* l
   return e == hipSuccess ? ok() : hip_fail(e, "router gate launch");
 }
 
-moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,
-                                   int32_t n_tokens, double alpha, double retain, double* importance,
-                                   uint8_t* mask, int32_t* counts, void* stream) {
+// Scratch of moeq_expert_importance_noalloc (16 MiB; see below).
+static __device__ __align__(256) uint8_t scratch[(size_t)16 << 20];
+
+namespace {
+
+// Scratch of the router-statistics pass over n tokens (layout shared by both
+// entry points): idx, w, per-chunk counts, ranks, offsets, permutation,
+// active list, the all-kept mask and the bias, each 256-byte aligned.
+struct ImportanceScratch {
+  size_t o_idx, o_w, o_cc, o_rank, o_off, o_perm, o_act, o_mask, o_bias, total;
+};
+
+ImportanceScratch importance_scratch(size_t n_tokens, int k, int E) {
+  const size_t nk = n_tokens * k, chunks = (n_tokens + kChunk - 1) / kChunk;
+  ImportanceScratch l{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  l.o_idx = take(nk * 4);
+  l.o_w = take(nk * 4);
+  l.o_cc = take(chunks * E * 4);
+  l.o_rank = take(nk * 4);
+  l.o_off = take((size_t)(E + 1) * 4);
+  l.o_perm = take(nk * 4);
+  l.o_act = take((size_t)(E + 1) * 4);
+  l.o_mask = take(E);
+  l.o_bias = take((size_t)E * 4);
+  l.total = off;
+  return l;
+}
+
+// Argument checks shared by both entry points (host only, before any HIP call).
+moeq_status importance_check(const moeq_config* cfg, const float* score_bias, const float* logits, int32_t n_tokens,
+                             double alpha, double retain, const double* importance, const uint8_t* mask) {
   moeq_status st = check_config(cfg);
   if (st != MOEQ_OK) return st;
-  const int E = cfg->n_experts, k = cfg->top_k;
+  const int E = cfg->n_experts;
   if (n_tokens < 1 || n_tokens > (1 << 24))
     return fail(MOEQ_ERR_INVALID_ARG, "n_tokens %d outside 1..2^24", n_tokens);
   if (!logits || !importance || !mask)
@@ -618,39 +652,30 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
     for (int e = 0; e < E; ++e)
       if (!isfinite(score_bias[e]) || fabsf(score_bias[e]) > 1e30f)
         return fail(MOEQ_ERR_INVALID_ARG, "score_bias[%d] is not a finite value of magnitude <= 1e30", e);
-  {
-    std::vector<uint8_t> all(E, 1);
-    int kept = 0;
-    if ((st = check_routing(cfg, all.data(), &kept)) != MOEQ_OK) return st;
-  }
+  std::vector<uint8_t> all(E, 1);
+  int kept = 0;
+  return check_routing(cfg, all.data(), &kept);
+}
+
+// The pass itself on caller-provided scratch `buf` (layout importance_scratch):
+// route with every expert kept, bucket, per-expert statistics, mask.
+hipError_t importance_run(const moeq_config* cfg, const float* score_bias, const float* logits, int32_t n_tokens,
+                          double alpha, double retain, double* importance, uint8_t* mask, int32_t* counts,
+                          hipStream_t s, uint8_t* buf, const ImportanceScratch& l) {
+  const int E = cfg->n_experts, k = cfg->top_k;
   int keep = (int)std::ceil(retain * (double)E - 1e-9);
   keep = keep < 1 ? 1 : keep > E ? E : keep;
-
-  hipStream_t s = (hipStream_t)stream;
-  const size_t nk = (size_t)n_tokens * k, chunks = ((size_t)n_tokens + kChunk - 1) / kChunk;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t at = off;
-    off = align_up(off + bytes, 256);
-    return at;
-  };
-  const size_t o_idx = take(nk * 4), o_w = take(nk * 4), o_cc = take(chunks * E * 4), o_rank = take(nk * 4),
-               o_off = take((size_t)(E + 1) * 4), o_perm = take(nk * 4), o_act = take((size_t)(E + 1) * 4),
-               o_mask = take(E), o_bias = take((size_t)E * 4);
-  uint8_t* buf = nullptr;
-  hipError_t e = hipMallocAsync((void**)&buf, off, s);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync (importance scratch)");
   Workspace ws{};
-  ws.idx = (int32_t*)(buf + o_idx);
-  ws.w = (float*)(buf + o_w);
-  ws.chunk_cnt = (int32_t*)(buf + o_cc);
-  ws.rank = (int32_t*)(buf + o_rank);
-  ws.offsets = (int32_t*)(buf + o_off);
-  ws.perm = (int32_t*)(buf + o_perm);
-  ws.active = (int32_t*)(buf + o_act);
-  uint8_t* all_kept = buf + o_mask;
-  float* bias = (float*)(buf + o_bias);
-  e = launch_fill_u8(all_kept, E, 1, s);
+  ws.idx = (int32_t*)(buf + l.o_idx);
+  ws.w = (float*)(buf + l.o_w);
+  ws.chunk_cnt = (int32_t*)(buf + l.o_cc);
+  ws.rank = (int32_t*)(buf + l.o_rank);
+  ws.offsets = (int32_t*)(buf + l.o_off);
+  ws.perm = (int32_t*)(buf + l.o_perm);
+  ws.active = (int32_t*)(buf + l.o_act);
+  uint8_t* all_kept = buf + l.o_mask;
+  float* bias = (float*)(buf + l.o_bias);
+  hipError_t e = launch_fill_u8(all_kept, E, 1, s);
   // the bias travels in kernel arguments, so score_bias is free on return
   if (e == hipSuccess) e = launch_store_host_floats(bias, score_bias, E, s);
   RouterParams rp{};
@@ -671,10 +696,68 @@ moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bi
   if (e == hipSuccess) e = launch_bucket_chunked(ws.idx, n_tokens, k, E, ws, s);
   if (e == hipSuccess)
     e = launch_expert_importance(ws.offsets, ws.perm, ws.w, E, n_tokens, alpha, keep, importance, mask, counts, s);
+  return e;
+}
+
+// ---- scratch of moeq_expert_importance_noalloc: the file-scope device array ----
+// Each device the library runs on holds its own copy for the life of the
+// process.  In host code `scratch` is only a stand-in for the symbol: its
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current, and only that address is ever handed to kernels.
+constexpr size_t kStaticScratchBytes = sizeof(scratch);
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t static_scratch(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = (uint8_t*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
+moeq_status moeq_expert_importance(const moeq_config* cfg, const float* score_bias, const float* logits,
+                                   int32_t n_tokens, double alpha, double retain, double* importance,
+                                   uint8_t* mask, int32_t* counts, void* stream) {
+  moeq_status st = importance_check(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask);
+  if (st != MOEQ_OK) return st;
+  const ImportanceScratch l = importance_scratch((size_t)n_tokens, cfg->top_k, cfg->n_experts);
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* buf = nullptr;
+  hipError_t e = hipMallocAsync((void**)&buf, l.total, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync (importance scratch)");
+  e = importance_run(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask, counts, s, buf, l);
   const hipError_t ef = hipFreeAsync(buf, s);
   if (e != hipSuccess) return hip_fail(e, "expert importance");
   if (ef != hipSuccess) return hip_fail(ef, "hipFreeAsync (importance scratch)");
   return ok();
+}
+
+moeq_status moeq_expert_importance_noalloc(const moeq_config* cfg, const float* score_bias, const float* logits,
+                                           int32_t n_tokens, double alpha, double retain, double* importance,
+                                           uint8_t* mask, int32_t* counts, void* stream) {
+  moeq_status st = importance_check(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask);
+  if (st != MOEQ_OK) return st;
+  const ImportanceScratch l = importance_scratch((size_t)n_tokens, cfg->top_k, cfg->n_experts);
+  if (l.total > kStaticScratchBytes)
+    return fail(MOEQ_ERR_CAPACITY,
+                "%d tokens at top_k %d over %d experts need %zu bytes of scratch; the static scratch holds %zu",
+                n_tokens, cfg->top_k, cfg->n_experts, l.total, kStaticScratchBytes);
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  uint8_t* buf = nullptr;
+  if ((e = static_scratch(dev, &buf)) != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static scratch)");
+  e = importance_run(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask, counts,
+                     (hipStream_t)stream, buf, l);
+  return e == hipSuccess ? ok() : hip_fail(e, "expert importance");
 }
 
 moeq_status moeq_set_stage_events(moeq_layer* L, void* const* events, int32_t count) {

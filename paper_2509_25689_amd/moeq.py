@@ -107,6 +107,8 @@ def _load():
         "moeq_router_logits": [P, P, I32, P, P],
         "moeq_expert_importance": [ctypes.POINTER(moeq_config), P, P, I32, ctypes.c_double, ctypes.c_double,
                                    P, P, P, P],
+        "moeq_expert_importance_noalloc": [ctypes.POINTER(moeq_config), P, P, I32, ctypes.c_double,
+                                           ctypes.c_double, P, P, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -249,6 +251,13 @@ def moeq_expert_importance(cfg, score_bias, logits, n_tokens, alpha, retain, imp
     """cfg: moeq_config; score_bias: host address or 0; the rest device addresses (counts may be 0)."""
     _check(lib.moeq_expert_importance(ctypes.byref(cfg), score_bias or None, logits, n_tokens, alpha, retain,
                                       importance, mask, counts or None, stream or None))
+
+
+def moeq_expert_importance_noalloc(cfg, score_bias, logits, n_tokens, alpha, retain, importance, mask, counts=0,
+                                   stream=0):
+    """As moeq_expert_importance, with the library's static scratch (no allocation)."""
+    _check(lib.moeq_expert_importance_noalloc(ctypes.byref(cfg), score_bias or None, logits, n_tokens, alpha,
+                                              retain, importance, mask, counts or None, stream or None))
 
 
 def expert_importance(shape, logits, *, alpha, retain, bias=None, stream=None):

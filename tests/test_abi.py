@@ -227,6 +227,28 @@ def test_expert_importance_validation():
     assert call(c=c2) == moeq.MOEQ_ERR_INVALID_ARG
 
 
+def test_expert_importance_noalloc_validation():
+    """The entry point without allocation checks what the allocating one checks,
+    and the size of its static scratch, all before any HIP call."""
+    lib = moeq.lib
+    cfg = _cfg()
+    fake = ctypes.c_void_p(16)
+
+    def call(c=cfg, logits=fake, n=8, alpha=0.5, retain=0.75, imp=fake, mask=fake):
+        return lib.moeq_expert_importance_noalloc(ctypes.byref(c) if c is not None else None, None, logits, n,
+                                                  alpha, retain, imp, mask, None, None)
+
+    assert call(c=None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(n=0) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(logits=None) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(alpha=2.0) == moeq.MOEQ_ERR_INVALID_ARG
+    assert call(retain=0.0) == moeq.MOEQ_ERR_INVALID_ARG
+    # 16 bytes per (token, slot) of ids, weights, ranks and permutation alone:
+    # 2^20 tokens at top_k 2 need 32 MiB, more than the 16 MiB static scratch
+    assert call(n=1 << 20) == moeq.MOEQ_ERR_CAPACITY
+    assert "static scratch" in moeq.moeq_last_error()
+
+
 def test_regroup_validation():
     """regroup must be 0 or 1 and needs a kept count divisible by n_group."""
     assert _create(_cfg(regroup=2))[0] == moeq.MOEQ_ERR_INVALID_ARG
