@@ -675,8 +675,8 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
 // tokens: one token tile, else two), so a small bucket does not spend
 // matrix instructions on an empty tile, and the loop has no branches.
 constexpr int RD_T = kRdTile;         // tokens per workgroup tile
-constexpr int RD_ROWS = 256;          // weight rows per workgroup
-constexpr int RD_WAVES = 4;
+constexpr int RD_ROWS = 512;          // weight rows per workgroup
+constexpr int RD_WAVES = 8;
 constexpr int RD_THREADS = 64 * RD_WAVES;
 constexpr int RD_RT = 2;              // row tiles of 32 per wave
 constexpr int RD_WROWS = 32 * RD_RT;  // weight rows per wave
@@ -686,7 +686,7 @@ constexpr int RD_APT = RD_SUB / 16 / RD_THREADS;  // 16-byte staging pieces per 
 constexpr size_t RD_LDS = (size_t)RD_NBUF * RD_SUB;
 static_assert(RD_WAVES * RD_WROWS == RD_ROWS, "the waves cover the workgroup's rows");
 static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * 2 * 64 * 64, "the SwiGLU hand-over must fit the activation buffers");
-static_assert(2 * RD_LDS <= 160 * 1024, "two workgroups share a compute unit's LDS");
+static_assert(RD_LDS <= 160 * 1024, "the activation buffers fit a compute unit's LDS");
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
@@ -861,18 +861,18 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
   };
 
   // prologue: stage 0's codes (for 4 bits, chunks 0 and 1: each later chunk
-  // is requested two sub-stages before its use); sub-stages 0 and 1 stored
+  // is requested two sub-stages before its use); sub-stage 0 stored, 1 in
+  // flight in the second staging set
   if constexpr (ACT) {
 #pragma unroll
     for (int j = 0; j < (B == 4 ? 2 : B); ++j) rload_chunk(j, 0);
     rload_scale(0, 0);
     rload_scale(1, 0);
   }
-  u32x4 xv[RD_APT];
-  aload(xv, 0);
-  astore(xv, 0);
-  aload(xv, 1);
-  astore(xv, 1);
+  u32x4 xa[RD_APT], xb[RD_APT];
+  aload(xa, 0);
+  astore(xa, 0);
+  aload(xb, 1);
   __syncthreads();
 
   // k step TS of sub-stage Q: operands into FA / FB (fragment reads from LDS
@@ -926,18 +926,20 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
     RD_PRODUCTS(fa1, fb1);                                                                              \
   } while (0)
 
-  // sub-stage s = 4U + Q in buffer Q: request sub-stage s + 2 into the
-  // staging registers, multiply sub-stage s while they arrive, store them
-  // into buffer (Q + 2) % 4 (free: its sub-stage s - 2 was read before the
-  // last barrier), and request the codes of stage U + 1 whose registers this
-  // sub-stage freed.  No branches: past the last sub-stage or stage the loads
-  // repeat the last one (clamped) and the stores go to buffers nobody reads
-  // again, so the compiler counts the outstanding loads exactly.
-#define RD_SUBSTAGE(Q)                                                                                  \
+  // sub-stage s = 4U + Q in buffer Q: request sub-stage s + 2 into staging
+  // set X (free: its data went to LDS at the end of s - 1), multiply
+  // sub-stage s, store sub-stage s + 1 from the other set Y (requested when
+  // s - 1 began) into buffer (Q + 1) % 4 (free: its sub-stage s - 3 was read
+  // before earlier barriers), and request the codes of a later stage whose
+  // registers this sub-stage freed.  Each activation load thus has two
+  // sub-stages to arrive.  No branches: past the last sub-stage or stage the
+  // loads repeat the last one (clamped) and the stores go to buffers nobody
+  // reads again, so the compiler counts the outstanding loads exactly.
+#define RD_SUBSTAGE(Q, X, Y)                                                                            \
   do {                                                                                                  \
-    aload(xv, min(4 * U + (Q) + 2, NSUB - 1));                                                          \
+    aload(X, min(4 * U + (Q) + 2, NSUB - 1));                                                           \
     RD_KSTEPS(Q);                                                                                       \
-    astore(xv, ((Q) + 2) & 3);                                                                          \
+    astore(Y, ((Q) + 1) & 3);                                                                           \
     const int Un_ = min(U + 1, NS - 1);                                                                 \
     if constexpr (B == 4) rload_chunk(((Q) + 2) & 3, (Q) < 2 ? U : Un_);                               \
     if constexpr (B == 2 && ((Q) & 1)) rload_chunk((Q) >> 1, Un_);                                     \
@@ -948,10 +950,10 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
   } while (0)
 
   for (int U = 0; U < NS; ++U) {
-    RD_SUBSTAGE(0);
-    RD_SUBSTAGE(1);
-    RD_SUBSTAGE(2);
-    RD_SUBSTAGE(3);
+    RD_SUBSTAGE(0, xa, xb);
+    RD_SUBSTAGE(1, xb, xa);
+    RD_SUBSTAGE(2, xa, xb);
+    RD_SUBSTAGE(3, xb, xa);
   }
 #undef RD_SUBSTAGE
 #undef RD_KSTEPS
@@ -980,7 +982,7 @@ __device__ __forceinline__ void rd_kloop_any(int bits, bool act, const MOEQ_GLOB
 // 8 (v / 4) + 4 (l / 32) + v % 4, column (token) l % 32.
 __device__ __forceinline__ int rd_acc_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
 
-// Gate/up tile: features [f0, f0 + 128) of one slot, tokens [m0, m0 + 64)
+// Gate/up tile: features [f0, f0 + 256) of one slot, tokens [m0, m0 + 64)
 // of its bucket (Mt of them real).  NT token tiles of 32 are multiplied.
 template <int NT>
 __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int Mt, int f0, const TensorDev& tg,
@@ -992,11 +994,12 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
   const TensorDev& t = wave < HW ? tg : tu;
   const int bits = __builtin_amdgcn_readfirstlane(t.bits);
   const int row0 = f0 + (wave % HW) * RD_WROWS;
+  const bool act = row0 < I;   // I is a multiple of 128: a wave's features are all in or all out
   const MOEQ_GLOBAL u32x4* rc[RD_RT];
   const MOEQ_GLOBAL u32x2* rs[RD_RT];
 #pragma unroll
   for (int r = 0; r < RD_RT; ++r) {
-    const int row = row0 + 32 * r + (lane & 31);
+    const int row = act ? row0 + 32 * r + (lane & 31) : 0;
     rc[r] = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)row * bits * Uk * 4));
     rs[r] = gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (H / kBlock)));
   }
@@ -1018,19 +1021,19 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
     for (int T = 0; T < NT; ++T)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[r][T][v] = 0.f;
-  rd_kloop_any<NT>(bits, true, rc, rs, Uk, arow, lp >> 2, lp & 3, gptr(a.zeros), lds, tid, lane, acc);
+  rd_kloop_any<NT>(bits, act, rc, rs, Uk, arow, lp >> 2, lp & 3, gptr(a.zeros), lds, tid, lane, acc);
 
   // SwiGLU: the up waves hand their accumulators to the gate waves of the
   // same features (the buffers are free after the loop's last barrier)
   f32x16* xch = reinterpret_cast<f32x16*>(lds);
-  if (wave >= HW) {
+  if (wave >= HW && act) {
 #pragma unroll
     for (int r = 0; r < RD_RT; ++r)
 #pragma unroll
       for (int T = 0; T < NT; ++T) xch[(((wave - HW) * RD_RT + r) * 2 + T) * 64 + lane] = acc[r][T];
   }
   __syncthreads();
-  if (wave >= HW) return;
+  if (wave >= HW || !act) return;
   const MOEQ_GLOBAL int32_t* xexp = gptr(a.xexp);
 #pragma unroll
   for (int T = 0; T < NT; ++T) {
@@ -1063,7 +1066,7 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
   }
 }
 
-// Down tile: output features [n0, n0 + 256) (rows of the down tensor) of one
+// Down tile: output features [n0, n0 + 512) (rows of the down tensor) of one
 // slot, tokens [m0, m0 + 64); results times the routing weight are the
 // slot's partial rows.
 template <int NT>
@@ -1133,9 +1136,9 @@ __device__ void rd_down_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int 
 
 // grid: tile_grid(max m-tiles, n-tiles); tiles of slots whose gate and up
 // (down) tensors are both 2-4 bits wide
-__global__ __launch_bounds__(RD_THREADS, 2) void gateup_rd_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(RD_THREADS, 1) void gateup_rd_kernel(DecodeArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds_c[];
-  const int nN = a.I / (RD_ROWS / 2);
+  const int nN = (a.I + RD_ROWS / 2 - 1) / (RD_ROWS / 2);
   int mt, nt;
   if (!tile_of_wg(blockIdx.x, a.tiles_rd[0], nN, &mt, &nt)) return;
   const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
@@ -1150,7 +1153,7 @@ __global__ __launch_bounds__(RD_THREADS, 2) void gateup_rd_kernel(DecodeArgs a) 
     rd_gateup_tile<2>(g, sl, m0, Mt, nt * (RD_ROWS / 2), tg, tu, lds_c);
 }
 
-__global__ __launch_bounds__(RD_THREADS, 2) void down_rd_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds_c[];
   const int nN = (a.H + RD_ROWS - 1) / RD_ROWS;
   int mt, nt;
@@ -1261,7 +1264,7 @@ hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
-  hipError_t e = launch_gemm(gateup_rd_kernel, g_attr_gu_rd, RD_THREADS, tile_grid(a.max_rtiles, a.I / (RD_ROWS / 2)),
+  hipError_t e = launch_gemm(gateup_rd_kernel, g_attr_gu_rd, RD_THREADS, tile_grid(a.max_rtiles, (a.I + RD_ROWS / 2 - 1) / (RD_ROWS / 2)),
                              RD_LDS, s, a);
   if (e == hipSuccess && a.wide_gateup) {
     const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
