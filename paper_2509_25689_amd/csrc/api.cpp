@@ -91,6 +91,7 @@ struct moeq_layer {
   uint8_t* mask = nullptr;
   float* bias = nullptr;
   int wide_gateup = 0, wide_down = 0;  // 0: no 5/6/8-bit tensor, 1: shared experts only, 2: routed too
+  int down_bits = 0;                   // width of every kept and shared down tensor when they agree
   int32_t* kept_ids = nullptr;  // kept experts ascending, when the router regroups them
   float* router_w = nullptr;    // float32 [n_experts x hidden] gate weight, when set
   float* gate_logits = nullptr; // float32 [max_tokens x n_experts], logits the forward computes
@@ -337,11 +338,16 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     if (wide(shared[s * 3 + 0]) || wide(shared[s * 3 + 1])) L->wide_gateup = 1;
     if (wide(shared[s * 3 + 2])) L->wide_down = 1;
   }
+  int db = -1;
+  auto agree = [&db](int b) { db = db == -1 || db == b ? b : 0; };
+  for (int s = 0; s < S; ++s) agree(shared[s * 3 + 2].bits);
   for (int e = 0; e < E; ++e)
     if (expert_mask[e]) {
       if (wide(routed[e * 3 + 0]) || wide(routed[e * 3 + 1])) L->wide_gateup = 2;
       if (wide(routed[e * 3 + 2])) L->wide_down = 2;
+      agree(routed[e * 3 + 2].bits);
     }
+  L->down_bits = db > 0 ? db : 0;
   hipError_t he = hipGetDevice(&L->device);
   if (he != hipSuccess) {
     release(L);
@@ -513,6 +519,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.zeros = L->ws.zeros;
   a.wide_gateup = L->wide_gateup;
   a.wide_down = L->wide_down;
+  a.idx = L->ws.idx;
+  a.down_bits = L->down_bits;
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
   hipError_t e = hipSuccess;
@@ -546,7 +554,7 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   mark(2);
   if (e == hipSuccess) e = prefill ? launch_down_prefill(a, s) : launch_down_decode(a, s);
   mark(3);
-  if (e == hipSuccess) e = launch_combine(a, s);
+  if (e == hipSuccess && (prefill || !down_combines(a))) e = launch_combine(a, s);
   mark(4);
   if (e != hipSuccess) return hip_fail(e, prefill ? "forward (prefill path)" : "forward (decode path)");
   return ok();

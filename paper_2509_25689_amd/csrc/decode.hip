@@ -504,6 +504,127 @@ __global__ __launch_bounds__(256, TM == 1 ? kDownMinBlocks : 2) void down_kernel
 }
 
 // ---------------------------------------------------------------------------
+// One token: down x routing weight and the combine in one pass, for layers
+// whose down tensors all have one width BD and at most 16 units per row.  A
+// workgroup of NT threads owns NT / 16 rows of y across every slot (the
+// token's k choices in choice order, then the shared experts): a group of 16
+// lanes owns one row, lane u unit u of that row in every slot, with D slots'
+// codes in flight.  The lane accumulates w_j * (its partial dot of slot j) in
+// slot order and the group sums its lanes with DPP in a fixed order: no
+// partial rows, no combine launch.  All h rows are staged once per workgroup
+// (binary16 with per-block prescales, as in the down kernel), their loads
+// issued in batches so a batch costs one memory round trip.
+struct DownSlot {
+  const uint32_t* codes;
+  const uint16_t* scales;
+  float w;
+  int hrow;
+};
+
+constexpr int kDown1Batch = 6;  // staged 32-byte pieces per thread per round trip
+
+template <int BD, int NT, int D>
+__global__ __launch_bounds__(NT) void down1_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  __shared__ DownSlot slots[kMaxTopK + kMaxShared];
+  const int H = a.H, I = a.I, U = I / kUnit, k = a.k, NS = a.k + a.S;
+  const int xts = U * kXStride, sts = U * 4;
+  uint32_t* xl = smem;
+  float2* xs = reinterpret_cast<float2*>(smem + NS * xts);
+  if ((int)threadIdx.x < NS) {
+    const int j = threadIdx.x;
+    DownSlot v;
+    if (j < k) {
+      // choice j of the token: its bucket of one holds h row offsets[e]
+      const int e = a.idx[j];
+      const TensorDev t = a.desc[e * 3 + 2];
+      v.codes = t.codes;
+      v.scales = t.scales;
+      v.w = a.w[j];
+      v.hrow = a.offsets[e];
+    } else {
+      const TensorDev t = a.desc[(a.E + (j - k)) * 3 + 2];
+      v.codes = t.codes;
+      v.scales = t.scales;
+      v.w = 1.0f;
+      v.hrow = k + (j - k);
+    }
+    slots[j] = v;
+  }
+  __syncthreads();
+
+  const int u = threadIdx.x & 15;
+  const int row = blockIdx.x * (NT / 16) + (threadIdx.x >> 4);
+  const int rowc = min(row, H - 1), uc = min(u, U - 1);
+  auto load_slot = [&](DownRows<BD>& b, int j) {
+    const DownSlot& sl = slots[min(j, NS - 1)];
+    load_unit<BD>(sl.codes + (size_t)rowc * BD * U * 4, U, uc, b.w);
+    b.s = *gptr(reinterpret_cast<const u32x2*>(sl.scales + (size_t)rowc * (I / kBlock) + 4 * uc));
+  };
+  DownRows<BD> buf[D];
+#pragma unroll
+  for (int i = 0; i < D - 1; ++i) load_slot(buf[i], i);
+
+  // stage every slot's h row: piece p (8 values) of slot p / (I / 8); a
+  // batch's loads all go out before its first piece is converted
+  const int PPS = I / 8, NP = NS * PPS;
+  for (int p0 = 0; p0 < NP; p0 += NT * kDown1Batch) {
+    f32x4 v[kDown1Batch][2];
+#pragma unroll
+    for (int i = 0; i < kDown1Batch; ++i) {
+      if (p0 + i * NT < NP) {
+        // pieces past the end repeat the last block's (same values, same place)
+        int p = p0 + i * NT + (int)threadIdx.x;
+        p = p < NP ? p : NP - 4 + (p & 3);
+        const MOEQ_GLOBAL f32x4* src =
+            gptr(reinterpret_cast<const f32x4*>(a.h + (size_t)slots[p / PPS].hrow * I)) + 2 * (p % PPS);
+        v[i][0] = src[0];
+        v[i][1] = src[1];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kDown1Batch; ++i) {
+      if (p0 + i * NT < NP) {
+        int p = p0 + i * NT + (int)threadIdx.x;
+        p = p < NP ? p : NP - 4 + (p & 3);
+        const int m = p / PPS, c = p % PPS;
+        const float f[8] = {v[i][0].x, v[i][0].y, v[i][0].z, v[i][0].w,
+                            v[i][1].x, v[i][1].y, v[i][1].z, v[i][1].w};
+        const int uu = c >> 4, cq = c & 15;
+        stage_piece(f, xl + m * xts + uu * kXStride + cq * 4, xs + m * sts + uu * 4 + (cq >> 2), (cq & 3) == 0);
+      }
+    }
+  }
+  __syncthreads();
+
+  const uint32_t* xu = xl + uc * kXStride;
+  const float2* su4 = xs + uc * 4;
+  float acc = 0.0f;
+#pragma unroll 1
+  for (int j0 = 0; j0 < NS; j0 += D) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int b = 0; b < D; ++b) {
+      const int j = j0 + b;
+      if (j < NS) {
+        // slot j + D - 1 goes out before slot j is reduced
+        load_slot(buf[(b + D - 1) % D], j + D - 1);
+        float o = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint32_t pr[16];
+          block_pairs_sub<BD>(buf[b].w + q * BD, pr);
+          o = block_dot_sub<BD>(pr, xu + j * xts + 16 * q, block_scale_sub(buf[b].s, q), su4[j * sts + q], o);
+        }
+        acc = fmaf(slots[j].w, u < U ? o : 0.0f, acc);
+      }
+    }
+  }
+  const float ys = group_sum<16>(acc);
+  if (u == 15 && row < H) a.y[row] = ys;
+}
+
+// ---------------------------------------------------------------------------
 // y_t = sum_j partial(t*k + j) + sum_s partial(n*k + s*n + t), fixed order;
 // the loads of eight partial rows are issued together.
 __global__ __launch_bounds__(256) void combine_kernel(DecodeArgs a) {
@@ -1038,7 +1159,41 @@ hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
   return e;
 }
 
+namespace {
+// threads per workgroup (NT / 16 rows) and slots in flight per lane (D) of
+// the one-token down + combine kernel
+#ifndef MOEQ_DOWN1_THREADS
+#define MOEQ_DOWN1_THREADS 512
+#endif
+#ifndef MOEQ_DOWN1_DEPTH
+#define MOEQ_DOWN1_DEPTH 3
+#endif
+size_t down1_lds(const DecodeArgs& a) {
+  const size_t U = a.I / kUnit, NS = a.k + a.S;
+  return NS * (U * kXStride * 4 + U * 4 * sizeof(float2));
+}
+
+template <int BD>
+hipError_t launch_down1_b(const DecodeArgs& a, hipStream_t s) {
+  constexpr int NT = MOEQ_DOWN1_THREADS, R = NT / 16;
+  down1_kernel<BD, NT, MOEQ_DOWN1_DEPTH><<<(a.H + R - 1) / R, NT, down1_lds(a), s>>>(a);
+  return hipGetLastError();
+}
+}  // namespace
+
+bool down_combines(const DecodeArgs& a) {
+  return a.n == 1 && a.wide_down == 0 && a.down_bits >= 2 && a.down_bits <= 4 && a.I / kUnit <= 16 &&
+         down1_lds(a) <= 65536;
+}
+
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {
+  if (down_combines(a)) {
+    switch (a.down_bits) {
+      case 2: return launch_down1_b<2>(a, s);
+      case 3: return launch_down1_b<3>(a, s);
+      default: return launch_down1_b<4>(a, s);
+    }
+  }
   const hipError_t e = a.n == 1 ? launch_down_tm<1>(a, s) : launch_down_tm<4>(a, s);
   return e == hipSuccess ? launch_wide_down(a, s) : e;
 }

@@ -120,6 +120,9 @@ struct DecodeArgs {
   const uint16_t* x16;
   uint16_t* h16;
   const uint32_t* zeros;  // 256 zero bytes
+  const int32_t* idx;     // [n*k] chosen experts, token-major
+  // width shared by every kept routed and shared down tensor (2-4), else 0
+  int32_t down_bits;
   // slots with a 5/6/8-bit gate or up (down) tensor: 0 none, 1 shared
   // experts only, 2 routed experts too
   int32_t wide_gateup, wide_down;
@@ -130,7 +133,10 @@ hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 // s2 after the routing and joins it back into s)
 hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2);
+// down x routing weight; for one token with one down width (down_combines)
+// it also sums the slots into y, and the combine is not launched
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
+bool down_combines(const DecodeArgs& a);
 hipError_t launch_combine(const DecodeArgs& a, hipStream_t s);
 // gate.hip: logits = x W_r^T (bf16 x [n x H], float32 W_r [E x H]); up to
 // kGateFewTokens tokens take the streaming kernel, more the tiled one
@@ -147,7 +153,10 @@ hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm,
                                     hipStream_t s);
 // prefill.hip
 constexpr int kGemmBM = 128;  // tokens per m-tile of the LDS-decoded (5/6/8-bit) GEMMs
-constexpr int kRdTile = 64;   // tokens per tile of the register-decoded (2-4-bit) GEMMs
+#ifndef MOEQ_RD_TILE
+#define MOEQ_RD_TILE 64
+#endif
+constexpr int kRdTile = MOEQ_RD_TILE;  // tokens per tile of the register-decoded (2-4-bit) GEMMs
 int prefill_max_mtiles(int n, int k, int S, int n_kept);
 int prefill_max_rtiles(int n, int k, int S, int n_kept);
 // the tile list (and cleared h row maxima), then the gate/up GEMMs, then

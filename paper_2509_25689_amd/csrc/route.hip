@@ -69,6 +69,11 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
 // Maximum of an unsigned key over the wavefront, returned to every lane
 // (0 is the identity, so each step folds into one v_max_u32 with DPP).
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
@@ -92,12 +97,21 @@ __device__ __forceinline__ int wave_incl_sum(int v) {
   return v;
 }
 
+// Which of the lane's experts the selection chose: bit i of `bits` for
+// expert lane*EPL + i, chosen as the token's j-th expert with j = order[i].
+template <int EPL>
+struct LaneChoice {
+  uint32_t bits;
+  int order[EPL];
+};
+
 // Route token t with the calling wavefront.  Lane l owns experts
 // [l*EPL, l*EPL + EPL).  gs_l: this wave's LDS row of >= G floats.  Writes
 // idx/w for the token to idx_g/w_g and, if idx_s is not null, the ids to idx_s.
+// Returns the lane's share of the choice (router expert indices).
 template <int EPL>
-__device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
-                                 float* w_g, int32_t* idx_s) {
+__device__ LaneChoice<EPL> route_token_wave(const RouterParams& rp, int t, float* gs_l, int32_t* idx_g,
+                                            float* w_g, int32_t* idx_s) {
   const int lane = threadIdx.x & 63;
   if (rp.x) {
     // binary exponent prescale for half precision: e puts the row's largest
@@ -135,18 +149,29 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
   const float* lg = rp.logits + (size_t)t * rp.E_row;
   float s[EPL], b[EPL];
-  // every load is issued before the first is used (one memory round trip;
-  // lanes past E read expert 0 and discard it)
+  // every load is issued before the first is used, unconditionally (a
+  // conditional load makes the compiler wait for all outstanding ones), so
+  // the inputs take one memory round trip (two with kept_ids); lanes past E
+  // read the last expert and discard it
   float lv[EPL], bv[EPL];
   bool kv[EPL];
+  int eo[EPL];  // original expert ids
+  if (rp.kept_ids) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) eo[i] = rp.kept_ids[min(lane * EPL + i, E - 1)];
+  } else {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) eo[i] = min(lane * EPL + i, E - 1);
+  }
+  uint8_t mk[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
-    const int e = lane * EPL + i;
-    const int eo = e < E ? (rp.kept_ids ? rp.kept_ids[e] : e) : 0;  // original expert id
-    lv[i] = lg[eo];
-    bv[i] = rp.bias[eo];
-    kv[i] = rp.kept_ids || rp.mask[eo];
+    lv[i] = lg[eo[i]];
+    bv[i] = rp.bias[eo[i]];
+    mk[i] = rp.mask[eo[i]];
   }
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) kv[i] = (rp.kept_ids != nullptr) | (mk[i] != 0);
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
@@ -175,12 +200,19 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
         c = b[i];
       }
     }
-    for (int off = 1; off < lpg; off <<= 1) {
-      const float oa = __shfl_xor(a, off, 64), oc = __shfl_xor(c, off, 64);
+    // partners: quad butterflies, then the mirror lane of the half row and
+    // of the row (each step pairs lanes whose partial groups are disjoint
+    // halves of the next larger group), then shuffles beyond 16 lanes
+    auto merge = [&](float oa, float oc) {
       const float lo = fminf(a, oa);
       a = fmaxf(a, oa);
       c = fmaxf(lo, fmaxf(c, oc));
-    }
+    };
+    if (lpg > 1) merge(dpp_f32<0xB1>(a), dpp_f32<0xB1>(c));    // quad_perm [1,0,3,2]
+    if (lpg > 2) merge(dpp_f32<0x4E>(a), dpp_f32<0x4E>(c));    // quad_perm [2,3,0,1]
+    if (lpg > 4) merge(dpp_f32<0x141>(a), dpp_f32<0x141>(c));  // row_half_mirror
+    if (lpg > 8) merge(dpp_f32<0x140>(a), dpp_f32<0x140>(c));  // row_mirror
+    for (int off = 16; off < lpg; off <<= 1) merge(__shfl_xor(a, off, 64), __shfl_xor(c, off, 64));
     float gsc = a;
     if (rp.topn == 2 && c != -INFINITY) gsc = a + c;  // 0 + a + c in float32, best first
     if (lane % lpg == 0 && lane / lpg < G) gs_l[lane / lpg] = gsc;
@@ -226,15 +258,24 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
 
   // ---- expert selection ----
   // Each lane sorts its own candidates (biased score descending, lower id
-  // first); then k rounds of: wave-wide float max of every lane's current
-  // head, the lowest lane holding it wins (lane l owns ids [l*EPL, l*EPL+EPL),
-  // so that is the lowest id among equal scores), the winner drops its head.
+  // first); then k rounds of: wave-wide max of every lane's current head
+  // key, the lowest lane holding it wins (lane l owns ids [l*EPL, l*EPL+EPL),
+  // so that is the lowest id among equal scores), the winner advances.
+  int gi[EPL];  // group of each of the lane's experts
+  if (per % EPL == 0) {
+    const int g0 = lane * EPL / per;
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) gi[i] = g0;
+  } else {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) gi[i] = (lane * EPL + i) / per;
+  }
   float cv[EPL], cs[EPL];
   int ci[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = lane * EPL + i;
-    const bool ok = e < E && b[i] != -INFINITY && ((gsel >> (e / per)) & 1);
+    const bool ok = e < E && b[i] != -INFINITY && ((gsel >> gi[i]) & 1);
     cv[i] = ok ? b[i] : -INFINITY;
     cs[i] = s[i];
     ci[i] = i;
@@ -254,27 +295,42 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
       cs[j - 1] = sw ? ts : cs[j - 1];
       ci[j - 1] = sw ? ti : ci[j - 1];
     }
-  // keys: order-preserving map of the head score, 0 = no candidate left
-  auto head_key = [](float v) { return v == -INFINITY ? 0u : ord_f32(v); };
-  uint32_t hk = head_key(cv[0]);
+  // keys: order-preserving map of the score, 0 = no candidate left
+  uint32_t key[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) key[i] = cv[i] == -INFINITY ? 0u : ord_f32(cv[i]);
+  LaneChoice<EPL> ch;
+  ch.bits = 0;
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) ch.order[i] = 0;
+  // the lane's head: its pos-th sorted candidate (pos = EPL: none left)
+  int pos = 0;
+  uint32_t hk = key[0];
+  float hs = cs[0];
+  int hi = ci[0];
   float sum = 0.0f, my_s = 0.0f;
   int my_i = 0, last = 0;
   for (int r = 0; r < rp.k; ++r) {
     const uint32_t m = wave_max_u32(hk);
-    const uint64_t hold = __ballot(hk == m) & (m ? ~0ull : 0ull);
+    const uint64_t hold = m ? __ballot(hk == m) : 0ull;
     // creation checks guarantee k candidates; never leave the index range
-    const int wl = hold ? __builtin_ctzll(hold) : 0;
-    const int e = hold ? wl * EPL + __builtin_amdgcn_readlane(ci[0], wl) : last;
-    const float sv = hold ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, cs[0]), wl)) : 0.0f;
-    const bool win = hold && lane == wl;
+    const int wl = hold ? (int)__builtin_ctzll(hold) : 0;
+    const int li = __builtin_amdgcn_readlane(hi, wl);
+    const float sv = hold ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hs), wl)) : 0.0f;
+    const int e = hold ? wl * EPL + li : last;
+    if (hold && lane == wl) {
+      ch.bits |= 1u << hi;
 #pragma unroll
-    for (int i = 0; i + 1 < EPL; ++i) {
-      cv[i] = win ? cv[i + 1] : cv[i];
-      cs[i] = win ? cs[i + 1] : cs[i];
-      ci[i] = win ? ci[i + 1] : ci[i];
+      for (int i = 0; i < EPL; ++i) ch.order[i] = i == hi ? r : ch.order[i];
+      ++pos;
+      hk = 0u;
+#pragma unroll
+      for (int i = 1; i < EPL; ++i) {
+        hk = pos == i ? key[i] : hk;
+        hs = pos == i ? cs[i] : hs;
+        hi = pos == i ? ci[i] : hi;
+      }
     }
-    cv[EPL - 1] = win ? -INFINITY : cv[EPL - 1];
-    hk = win ? head_key(cv[0]) : hk;
     sum = sum + sv;
     if (lane == r) {
       my_i = e;
@@ -294,6 +350,7 @@ __device__ void route_token_wave(const RouterParams& rp, int t, float* gs_l, int
     if (idx_s) idx_s[t * rp.k + lane] = id;
   }
   wave_sync();  // gs_l is reused by this wave's next token
+  return ch;
 }
 
 // Experts per lane for E experts (the kernels are instantiated per value).
@@ -380,14 +437,34 @@ __global__ __launch_bounds__(small_threads<EPL>()) void route_bucket_small_kerne
 // Every chosen expert holds one assignment: offsets[e] is the number of
 // chosen ids below e, the active list is the chosen ids in ascending order,
 // and perm at an id's ascending rank is its slot.  The result equals the
-// counting sort's.
+// counting sort's.  Without kept_ids the lanes own the original ids, and the
+// ranks come from each lane's choice bits and a prefix sum over the lanes.
 template <int EPL>
 __global__ __launch_bounds__(64) void route_bucket_one_kernel(RouterParams rp, Workspace ws) {
   __shared__ float gs_l[64];
   __shared__ int32_t ids[kMaxTopK];
-  route_token_wave<EPL>(rp, 0, gs_l, ws.idx, ws.w, ids);
-  wave_sync();
+  const LaneChoice<EPL> ch = route_token_wave<EPL>(rp, 0, gs_l, ws.idx, ws.w, ids);
   const int lane = threadIdx.x, k = rp.k, E = rp.E_row;
+  if (!rp.kept_ids) {
+    const int cnt = __popc(ch.bits);
+    const int below = wave_incl_sum(cnt) - cnt;  // chosen ids of the lanes below
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = lane * EPL + i;
+      const int r = below + __popc(ch.bits & ((1u << i) - 1u));
+      if (e < E) ws.offsets[e] = r;
+      if ((ch.bits >> i) & 1u) {
+        ws.active[1 + r] = e;
+        ws.perm[r] = ch.order[i];
+      }
+    }
+    if (lane == 0) {
+      ws.offsets[E] = k;
+      ws.active[0] = k;
+    }
+    return;
+  }
+  wave_sync();
   if (lane < k) {
     const int mine = ids[lane];
     int r = 0;
