@@ -154,7 +154,7 @@ hipError_t launch_expert_importance(const int32_t* offsets, const int32_t* perm,
 // prefill.hip
 constexpr int kGemmBM = 128;  // tokens per m-tile of the LDS-decoded (5/6/8-bit) GEMMs
 #ifndef MOEQ_RD_TILE
-#define MOEQ_RD_TILE 64
+#define MOEQ_RD_TILE 128
 #endif
 constexpr int kRdTile = MOEQ_RD_TILE;  // tokens per tile of the register-decoded (2-4-bit) GEMMs
 int prefill_max_mtiles(int n, int k, int S, int n_kept);

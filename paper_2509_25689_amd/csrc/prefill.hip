@@ -675,17 +675,19 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
 // tokens: one token tile, else two), so a small bucket does not spend
 // matrix instructions on an empty tile, and the loop has no branches.
 constexpr int RD_T = kRdTile;         // tokens per workgroup tile
-constexpr int RD_ROWS = 512;          // weight rows per workgroup
 constexpr int RD_WAVES = 8;
 constexpr int RD_THREADS = 64 * RD_WAVES;
-constexpr int RD_RT = 2;              // row tiles of 32 per wave
+constexpr int RD_NTMAX = RD_T / 32;   // token tiles of 32 per workgroup tile
+constexpr int RD_RT = RD_T >= 128 ? 1 : 2;  // row tiles of 32 per wave
 constexpr int RD_WROWS = 32 * RD_RT;  // weight rows per wave
+constexpr int RD_ROWS = RD_WAVES * RD_WROWS;  // weight rows per workgroup
 constexpr int RD_SUB = RD_T * 256;    // bytes of one activation sub-stage
 constexpr int RD_NBUF = 4;            // activation sub-stages resident in LDS
 constexpr int RD_APT = RD_SUB / 16 / RD_THREADS;  // 16-byte staging pieces per thread and sub-stage
 constexpr size_t RD_LDS = (size_t)RD_NBUF * RD_SUB;
 static_assert(RD_WAVES * RD_WROWS == RD_ROWS, "the waves cover the workgroup's rows");
-static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * 2 * 64 * 64, "the SwiGLU hand-over must fit the activation buffers");
+static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * RD_NTMAX * 64 * 64,
+              "the SwiGLU hand-over must fit the activation buffers");
 static_assert(RD_LDS <= 160 * 1024, "the activation buffers fit a compute unit's LDS");
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -1030,7 +1032,7 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
 #pragma unroll
     for (int r = 0; r < RD_RT; ++r)
 #pragma unroll
-      for (int T = 0; T < NT; ++T) xch[(((wave - HW) * RD_RT + r) * 2 + T) * 64 + lane] = acc[r][T];
+      for (int T = 0; T < NT; ++T) xch[(((wave - HW) * RD_RT + r) * RD_NTMAX + T) * 64 + lane] = acc[r][T];
   }
   __syncthreads();
   if (wave >= HW || !act) return;
@@ -1048,7 +1050,7 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
     float rmax = 0.0f;
 #pragma unroll
     for (int r = 0; r < RD_RT; ++r) {
-      const f32x16 u = xch[((wave * RD_RT + r) * 2 + T) * 64 + lane];
+      const f32x16 u = xch[((wave * RD_RT + r) * RD_NTMAX + T) * 64 + lane];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         f32x4 hv;
@@ -1147,10 +1149,17 @@ __global__ __launch_bounds__(RD_THREADS, 1) void gateup_rd_kernel(DecodeArgs a) 
   if (!tg.codes || !tu.codes || tg.bits > 4 || tu.bits > 4) return;
   const int Mt = min(RD_T, sl.M - m0);
   const GemmArgs g = gemm_args(a);
+  const int f0 = nt * (RD_ROWS / 2);
   if (Mt <= 32)
-    rd_gateup_tile<1>(g, sl, m0, Mt, nt * (RD_ROWS / 2), tg, tu, lds_c);
-  else
-    rd_gateup_tile<2>(g, sl, m0, Mt, nt * (RD_ROWS / 2), tg, tu, lds_c);
+    rd_gateup_tile<1>(g, sl, m0, Mt, f0, tg, tu, lds_c);
+  else if (RD_NTMAX == 2 || Mt <= 64)
+    rd_gateup_tile<2>(g, sl, m0, Mt, f0, tg, tu, lds_c);
+  else if constexpr (RD_NTMAX == 4) {
+    if (Mt <= 96)
+      rd_gateup_tile<3>(g, sl, m0, Mt, f0, tg, tu, lds_c);
+    else
+      rd_gateup_tile<4>(g, sl, m0, Mt, f0, tg, tu, lds_c);
+  }
 }
 
 __global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
@@ -1164,10 +1173,17 @@ __global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
   if (!td.codes || td.bits > 4) return;
   const int Mt = min(RD_T, sl.M - m0);
   const GemmArgs g = gemm_args(a);
+  const int n0 = nt * RD_ROWS;
   if (Mt <= 32)
-    rd_down_tile<1>(g, sl, m0, Mt, nt * RD_ROWS, td, lds_c);
-  else
-    rd_down_tile<2>(g, sl, m0, Mt, nt * RD_ROWS, td, lds_c);
+    rd_down_tile<1>(g, sl, m0, Mt, n0, td, lds_c);
+  else if (RD_NTMAX == 2 || Mt <= 64)
+    rd_down_tile<2>(g, sl, m0, Mt, n0, td, lds_c);
+  else if constexpr (RD_NTMAX == 4) {
+    if (Mt <= 96)
+      rd_down_tile<3>(g, sl, m0, Mt, n0, td, lds_c);
+    else
+      rd_down_tile<4>(g, sl, m0, Mt, n0, td, lds_c);
+  }
 }
 
 // Diagnostic: one tensor through the grouped GEMMs' decoders, one thread per
