@@ -6,9 +6,9 @@
  *   - a plain streaming read of device memory with 16-byte coalesced loads:
  *     the practical ceiling of an HBM-bound kernel that only reads (the
  *     decode matrix-vector products stream their packed weights this way);
- *   - a loop of dense v_mfma_f32_16x16x32_f16 instructions on register
+ *   - a loop of dense v_mfma_f32_32x32x16_f16 instructions on register
  *     operands with no memory traffic: the practical ceiling of the binary16
- *     matrix cores the prefill grouped GEMMs run on.
+ *     matrix cores for the instruction the prefill grouped GEMMs issue.
  * The rates are computed by the caller from its own event timing of a launch:
  * bytes read per launch = n_bytes; flops per launch = moeq_peaks_mfma_flops().
  *
@@ -33,13 +33,13 @@ extern "C" {
 int moeq_peaks_stream_read(const void* src, size_t n_bytes, uint32_t* sink, void* stream);
 int moeq_peaks_read_workgroups(size_t n_bytes);
 
-/* Runs `iters` rounds of 8 independent binary16 MFMA chains on every wave of
+/* Runs `iters` rounds of 4 independent binary16 MFMA chains on every wave of
  * `workgroups` workgroups of 256 threads, then writes one float per thread
  * (sum of its accumulators) to sink so the work is not removed.
  *   sink   DEVICE float [workgroups * 256] */
 int moeq_peaks_mfma(int workgroups, int iters, float* sink, void* stream);
 /* Dense flops of one moeq_peaks_mfma launch: workgroups * 4 waves * iters *
- * 8 MFMAs * 2 * 16 * 16 * 32. */
+ * 4 MFMAs * 2 * 32 * 32 * 16. */
 double moeq_peaks_mfma_flops(int workgroups, int iters);
 
 #ifdef __cplusplus

@@ -9,7 +9,7 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kReadThreads = 256;
 constexpr int kReadUnroll = 8;  // 16-byte loads in flight per thread
@@ -37,9 +37,10 @@ __global__ __launch_bounds__(kReadThreads) void stream_read_kernel(const u32x4* 
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
 }
 
-// 8 independent accumulator chains per wave, so that the issue of one MFMA
-// never waits on the result of the previous one.
-constexpr int kChains = 8;
+// 4 independent accumulator chains per wave of v_mfma_f32_32x32x16_f16 (the
+// shape the grouped GEMMs issue), so that the issue of one MFMA never waits
+// on the result of the previous one.
+constexpr int kChains = 4;
 __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) {
   const int lane = threadIdx.x & 63;
   half8 a, b;
@@ -48,16 +49,20 @@ __global__ __launch_bounds__(256) void mfma_loop_kernel(int iters, float* sink) 
     a[i] = (_Float16)(0.001f * (float)((lane + i) & 7));
     b[i] = (_Float16)(0.001f * (float)((lane * 3 + i) & 7));
   }
-  f32x4 acc[kChains];
+  f32x16 acc[kChains];
 #pragma unroll
-  for (int c = 0; c < kChains; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[c][v] = 0.f;
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
-    for (int c = 0; c < kChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[c], 0, 0, 0);
+    for (int c = 0; c < kChains; ++c) acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[c], 0, 0, 0);
   }
   float s = 0.f;
 #pragma unroll
-  for (int c = 0; c < kChains; ++c) s += acc[c][0] + acc[c][1] + acc[c][2] + acc[c][3];
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += acc[c][v];
   sink[(size_t)blockIdx.x * 256 + threadIdx.x] = s;
 }
 
@@ -82,7 +87,7 @@ int moeq_peaks_mfma(int workgroups, int iters, float* sink, void* stream) {
 }
 
 double moeq_peaks_mfma_flops(int workgroups, int iters) {
-  return (double)workgroups * 4.0 * iters * kChains * 2.0 * 16 * 16 * 32;
+  return (double)workgroups * 4.0 * iters * kChains * 2.0 * 32 * 32 * 16;
 }
 
 }  // extern "C"
