@@ -91,6 +91,7 @@ struct moeq_layer {
   uint8_t* mask = nullptr;
   float* bias = nullptr;
   int wide_gateup = 0, wide_down = 0;  // 0: no 5/6/8-bit tensor, 1: shared experts only, 2: routed too
+  int lds_gateup = 0, lds_down = 0;    // some gate/up (down) tensor takes the LDS-decoded GEMM
   int down_bits = 0;                   // width of every kept and shared down tensor when they agree
   int32_t* kept_ids = nullptr;  // kept experts ascending, when the router regroups them
   float* router_w = nullptr;    // float32 [n_experts x hidden] gate weight, when set
@@ -354,9 +355,11 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     return hip_fail(he, "hipGetDevice");
   }
   uint8_t* staging = nullptr;
+  uint32_t* scale_keys = nullptr;  // per descriptor: the largest scale key (launch_scale_key_max)
   auto bail = [&](hipError_t e, const char* what) {
     hipStreamSynchronize(nullptr);
     hipFree(staging);
+    hipFree(scale_keys);
     release(L);
     return hip_fail(e, what);
   };
@@ -377,6 +380,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   if (weights_location == MOEQ_WEIGHTS_HOST && max_codes &&
       (he = hipMalloc((void**)&staging, max_codes)) != hipSuccess)
     return bail(he, "hipMalloc(staging)");
+  if ((he = hipMalloc((void**)&scale_keys, sizeof(uint32_t) * plan.size())) != hipSuccess ||
+      (he = hipMemset(scale_keys, 0, sizeof(uint32_t) * plan.size())) != hipSuccess)
+    return bail(he, "scale keys");
 
   uint8_t* base = (uint8_t*)L->store;
   L->desc_host.assign(plan.size(), TensorDev{nullptr, nullptr, 0, 0, 0, 0});
@@ -396,6 +402,9 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
                        weights_location == MOEQ_WEIGHTS_HOST ? hipMemcpyHostToDevice
                                                              : hipMemcpyDeviceToDevice)) != hipSuccess)
       return e;
+    if ((e = launch_scale_key_max((const uint16_t*)(base + tp.scales_off), sb / 2,
+                                  scale_keys + (size_t)slot * 3 + p, 0)) != hipSuccess)
+      return e;
     TensorDev& d = L->desc_host[(size_t)slot * 3 + p];
     d.codes = (const uint32_t*)(base + tp.codes_off);
     d.scales = (const uint16_t*)(base + tp.scales_off);
@@ -412,6 +421,25 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     for (int p = 0; p < 3; ++p)
       if ((he = upload(E + s, p, shared[s * 3 + p])) != hipSuccess) return bail(he, "weight upload");
 
+  // tensors the grouped GEMMs' register decoder cannot take (wider than 4
+  // bits, or a scale outside (0, rd_scale_limit(bits)])
+  {
+    std::vector<uint32_t> keys(plan.size());
+    if ((he = hipMemcpy(keys.data(), scale_keys, sizeof(uint32_t) * plan.size(), hipMemcpyDeviceToHost)) !=
+        hipSuccess)
+      return bail(he, "scale keys");
+    for (size_t i = 0; i < plan.size(); ++i) {
+      TensorDev& d = L->desc_host[i];
+      if (!d.codes) continue;
+      if (d.bits <= 4 && keys[i] > rd_scale_limit(d.bits)) d.flags |= kTensorOffRegisterDecoder;
+      if (d.bits > 4 || (d.flags & kTensorOffRegisterDecoder)) {
+        if (i % 3 == 2)
+          L->lds_down = 1;
+        else
+          L->lds_gateup = 1;
+      }
+    }
+  }
   std::vector<float> bias_h(E, 0.0f);
   if (score_bias) memcpy(bias_h.data(), score_bias, sizeof(float) * E);
   if ((he = hipMemcpy(L->desc, L->desc_host.data(), sizeof(TensorDev) * plan.size(),
@@ -423,6 +451,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
   if ((he = hipStreamSynchronize(nullptr)) != hipSuccess) return bail(he, "create");
   hipFree(staging);
   staging = nullptr;
+  hipFree(scale_keys);
+  scale_keys = nullptr;
 
   uint8_t* w = (uint8_t*)L->ws_mem;
   L->ws.idx = (int32_t*)(w + o_idx);
@@ -519,6 +549,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.zeros = L->ws.zeros;
   a.wide_gateup = L->wide_gateup;
   a.wide_down = L->wide_down;
+  a.lds_gateup = L->lds_gateup;
+  a.lds_down = L->lds_down;
   a.idx = L->ws.idx;
   a.down_bits = L->down_bits;
   const bool prefill =

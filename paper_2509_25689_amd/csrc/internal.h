@@ -38,8 +38,16 @@ struct TensorDev {
   int32_t bits;
   int32_t rows;
   int32_t K;
-  int32_t pad;
+  int32_t flags;  // kTensor* bits
 };
+
+// TensorDev.flags: some block scale of the tensor is not a positive finite
+// binary16 at most rd_scale_limit(bits), so the grouped GEMMs' register
+// decoder (which forms d * (c - z) from d * 2^(14 + b)) cannot take it; its
+// tiles go to the LDS-decoded kernels instead.
+constexpr int32_t kTensorOffRegisterDecoder = 1;
+// Largest binary16 bit pattern of a scale d with d * 2^(14 + b) finite.
+constexpr uint32_t rd_scale_limit(int b) { return 0x7BFFu - ((uint32_t)(14 + b) << 10); }
 
 struct RouterParams {
   const float* logits;    // [n x E_row]
@@ -95,6 +103,10 @@ hipError_t launch_repack(const uint8_t* canon_codes, int rows, int K, int bits,
 hipError_t launch_dequant(const TensorDev& t, float* out, hipStream_t s);
 // widths 2-4: the binary16-subnormal pair decoder rebuilt to float32
 hipError_t launch_dequant_sub(const TensorDev& t, float* out, hipStream_t s);
+// *out = max over the n binary16 scales of key(s): the magnitude bits of a
+// positive finite scale, 0xFFFF for a zero, negative or non-finite one
+// (atomic maximum: *out must start at 0)
+hipError_t launch_scale_key_max(const uint16_t* scales, size_t n, uint32_t* out, hipStream_t s);
 hipError_t launch_quantize(const float* w, int rows, int K, int bits, uint8_t* codes,
                            uint16_t* scales, hipStream_t s);
 // decode.hip
@@ -126,6 +138,9 @@ struct DecodeArgs {
   // slots with a 5/6/8-bit gate or up (down) tensor: 0 none, 1 shared
   // experts only, 2 routed experts too
   int32_t wide_gateup, wide_down;
+  // many-token path: some kept or shared gate/up (down) tensor is wider than
+  // 4 bits or off the register decoder, so the LDS-decoded GEMM runs too
+  int32_t lds_gateup, lds_down;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 // the same work split over two streams: the one-token buckets (and the wide

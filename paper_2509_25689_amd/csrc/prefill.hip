@@ -135,6 +135,13 @@ __device__ __forceinline__ bool tile_of_wg(int hw, int T, int nN, int* mt, int* 
 }
 inline int tile_grid(int max_tiles, int nN) { return (max_tiles + kXcds - 1) / kXcds * kXcds * nN; }
 
+// The register-decoded GEMMs take a tensor of 2-4 bits whose scales the
+// create-time scan found positive, finite and small enough (flags); the
+// LDS-decoded GEMMs take every other tensor.
+__device__ __forceinline__ bool rd_ok(const TensorDev& t) {
+  return t.bits <= 4 && !(t.flags & kTensorOffRegisterDecoder);
+}
+
 // Row-base pointer of a tensor row in the device layout.
 __device__ __forceinline__ const MOEQ_GLOBAL u32x4* row_chunks(const TensorDev& t, int bits, int row) {
   const int U = t.K / kUnit;
@@ -532,8 +539,9 @@ __device__ void gateup_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, i
   }
 }
 
-// The tiles with a 5, 6 or 8-bit gate or up tensor (the other of the two may
-// be narrower); 2-4-bit tiles take gateup_rd_kernel.
+// The tiles whose gate or up tensor the register decoder cannot take (5, 6
+// or 8 bits wide, or scales outside its range; the other of the two may be
+// any width); the other tiles take gateup_rd_kernel.
 __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   extern __shared__ _Float16 lds_h[];
   const int nN = a.I / BN;
@@ -544,7 +552,7 @@ __global__ __launch_bounds__(512, 1) void gateup_gemm8_kernel(DecodeArgs a) {
   const SlotInfo sl = slot_of(a, slot);
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
-  if (tg.bits <= 4 && tu.bits <= 4) return;
+  if (rd_ok(tg) && rd_ok(tu)) return;
   gateup_gemm_body8(gemm_args(a), sl, m0, nt * BN, tg, tu, lds_h);
 }
 
@@ -583,7 +591,13 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
   if (!wrole) {
     gemm_loop8<1, 4, 0, false, 4>(rc, rs, U, arow, wdst, adst, As, Ws, lane, wm, wn, nk, acc);
   } else {
-    if (bits == 5) {
+    if (bits == 2) {
+      if (blk) DN8(2, 1); else DN8(2, 0);
+    } else if (bits == 3) {
+      if (blk) DN8(3, 1); else DN8(3, 0);
+    } else if (bits == 4) {
+      if (blk) DN8(4, 1); else DN8(4, 0);
+    } else if (bits == 5) {
       if (blk) DN8(5, 1); else DN8(5, 0);
     } else if (bits == 6) {
       if (blk) DN8(6, 1); else DN8(6, 0);
@@ -621,7 +635,8 @@ __device__ void down_gemm_body8(const GemmArgs a, const SlotInfo sl, int m0, int
   }
 }
 
-// The tiles whose down tensor is 5, 6 or 8 bits wide (2-4-bit tiles take
+// The tiles whose down tensor the register decoder cannot take (5, 6 or 8
+// bits wide, or scales outside its range; the other tiles take
 // down_rd_kernel).  Four waves per SIMD (128 registers): two workgroups share
 // a compute unit (2 x 80 KB of LDS) and overlap their K-step chains.
 __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
@@ -634,7 +649,7 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
   const SlotInfo sl = slot_of(a, slot);
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
-  if (td.bits <= 4) return;
+  if (rd_ok(td)) return;
   down_gemm_body8(gemm_args(a), sl, m0, nt * BN, td, lds_h);
 }
 
@@ -718,79 +733,90 @@ __device__ __forceinline__ void rd_load(RdUnit<B>& u, const MOEQ_GLOBAL u32x4* r
   u.s = unit < Uk ? s : u32x2{0u, 0u};
 }
 
+// Register decode of the code pairs (weights 2i and 2i + 1 sit in the low
+// and high halves of a dword).  The pair is shifted and masked to bit
+// P = 10 - b of each half with the exponent field zero: two binary16
+// subnormals c * 2^(P - 24), exact.  One packed fused multiply-add with
+// D = d * 2^(24 - P) and C = -2^(b-1) d then forms c d - z d = d (c - z) and
+// rounds it once: the binary16 value of d * (c - z).  D and C are exact for a
+// positive finite d <= rd_scale_limit(b), which the create-time scan
+// guarantees for every tensor these kernels take.
+template <int B>
+constexpr int rd_at() { return 10 - B; }
+
 struct RdConsts {
-  uint32_t base;  // binary16 1024 in both halves
-  uint32_t mask;  // the width's code mask in both halves
-  half2_t zb;     // -(1024 + 2^(b-1)) in both halves
+  uint32_t mask;  // the width's code mask at bit P of both halves
 };
 
 template <int B>
 __device__ __forceinline__ RdConsts rd_consts() {
+  constexpr uint32_t m = ((1u << B) - 1u) << rd_at<B>();
   RdConsts k;
-  asm("v_mov_b32 %0, 0x64006400" : "=v"(k.base));
-  if constexpr (B == 4) asm("v_mov_b32 %0, 0x000F000F" : "=v"(k.mask));
-  if constexpr (B == 3) asm("v_mov_b32 %0, 0x00070007" : "=v"(k.mask));
-  if constexpr (B == 2) asm("v_mov_b32 %0, 0x00030003" : "=v"(k.mask));
-  const _Float16 zf = (_Float16)(-(1024.0f + (float)(1 << (B - 1))));
-  k.zb = half2_t{zf, zf};
+  k.mask = m | (m << 16);
   return k;
 }
 
+struct RdScale {
+  half2_t D, C;  // d * 2^(24 - P) and -2^(b-1) d in both halves
+};
+
+template <int B, int Q>
+__device__ __forceinline__ RdScale rd_scale(const RdUnit<B>& u) {
+  const uint32_t sp = Q < 2 ? u.s.x : u.s.y;
+  const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)((Q & 1) ? sp >> 16 : sp));
+  const _Float16 D = __builtin_amdgcn_ldexph(d, 24 - rd_at<B>());
+  const _Float16 C = d * (_Float16)(-(float)(1 << (B - 1)));
+  return RdScale{half2_t{D, D}, half2_t{C, C}};
+}
+
 // code pair at bit offset S of each half of w -> binary16 d * (c - z) pair
-template <int S>
-__device__ __forceinline__ uint32_t rd_pair(uint32_t w, const RdConsts& k, half2_t d2) {
-  const uint32_t v = and_or(w >> S, k.mask, k.base);
-  const half2_t c = __builtin_bit_cast(half2_t, v) + k.zb;
-  return __builtin_bit_cast(uint32_t, c * d2);
+template <int B, int S>
+__device__ __forceinline__ uint32_t rd_pair(uint32_t w, const RdConsts& k, const RdScale& sc) {
+  constexpr int P = rd_at<B>();
+  const uint32_t v = (S >= P ? w >> (S - P) : w << (P - S)) & k.mask;
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(half2_t, v), sc.D, sc.C));
 }
 
 // Operand piece M (weights 8M .. 8M + 7) of block Q of this lane's unit.
 template <int B, int Q, int M>
 __device__ __forceinline__ half8 rd_piece(const RdUnit<B>& u, const RdConsts& k) {
-  const uint32_t sp = Q < 2 ? u.s.x : u.s.y;
-  const _Float16 d = __builtin_bit_cast(_Float16, (uint16_t)((Q & 1) ? sp >> 16 : sp));
-  const half2_t d2 = {d, d};
+  const RdScale sc = rd_scale<B, Q>(u);
   uint32_t p[4];
   if constexpr (B == 4) {
     const uint32_t w = rd_dword(u, 4 * Q + M);
-    p[0] = rd_pair<0>(w, k, d2);
-    p[1] = rd_pair<4>(w, k, d2);
-    p[2] = rd_pair<8>(w, k, d2);
-    p[3] = rd_pair<12>(w, k, d2);
+    p[0] = rd_pair<B, 0>(w, k, sc);
+    p[1] = rd_pair<B, 4>(w, k, sc);
+    p[2] = rd_pair<B, 8>(w, k, sc);
+    p[3] = rd_pair<B, 12>(w, k, sc);
   } else if constexpr (B == 2) {
     const uint32_t w = rd_dword(u, 2 * Q + M / 2);
     constexpr int o = 8 * (M & 1);
-    p[0] = rd_pair<o + 0>(w, k, d2);
-    p[1] = rd_pair<o + 2>(w, k, d2);
-    p[2] = rd_pair<o + 4>(w, k, d2);
-    p[3] = rd_pair<o + 6>(w, k, d2);
+    p[0] = rd_pair<B, o + 0>(w, k, sc);
+    p[1] = rd_pair<B, o + 2>(w, k, sc);
+    p[2] = rd_pair<B, o + 4>(w, k, sc);
+    p[3] = rd_pair<B, o + 6>(w, k, sc);
   } else {
     // pairs 4M .. 4M + 3 of the block; pair P < 15 sits in dword P / 5 at
     // offset 3 (P % 5), pair 15 is bit q of each code in bit 15 / 31 of dword q
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      constexpr int dummy = 0;
-      (void)dummy;
       const int P = 4 * M + i;
       if (P < 15) {
         const uint32_t w = rd_dword(u, 3 * Q + P / 5);
         switch (P % 5) {
-          case 0: p[i] = rd_pair<0>(w, k, d2); break;
-          case 1: p[i] = rd_pair<3>(w, k, d2); break;
-          case 2: p[i] = rd_pair<6>(w, k, d2); break;
-          case 3: p[i] = rd_pair<9>(w, k, d2); break;
-          default: p[i] = rd_pair<12>(w, k, d2); break;
+          case 0: p[i] = rd_pair<B, 0>(w, k, sc); break;
+          case 1: p[i] = rd_pair<B, 3>(w, k, sc); break;
+          case 2: p[i] = rd_pair<B, 6>(w, k, sc); break;
+          case 3: p[i] = rd_pair<B, 9>(w, k, sc); break;
+          default: p[i] = rd_pair<B, 12>(w, k, sc); break;
         }
       } else {
-        uint32_t m1, m2, m4;
-        asm("v_mov_b32 %0, 0x00010001" : "=v"(m1));
-        asm("v_mov_b32 %0, 0x00020002" : "=v"(m2));
-        asm("v_mov_b32 %0, 0x00040004" : "=v"(m4));
-        uint32_t t = and_or(rd_dword(u, 3 * Q) >> 15, m1, k.base);
-        t = and_or(rd_dword(u, 3 * Q + 1) >> 14, m2, t);
-        t = and_or(rd_dword(u, 3 * Q + 2) >> 13, m4, t);
-        const half2_t c = __builtin_bit_cast(half2_t, t) + k.zb;
-        p[i] = __builtin_bit_cast(uint32_t, c * d2);
+        constexpr int A = rd_at<B>();
+        constexpr uint32_t b0 = (1u << A) | (1u << (A + 16));
+        uint32_t t = (rd_dword(u, 3 * Q) >> (15 - A)) & b0;
+        t = and_or(rd_dword(u, 3 * Q + 1) >> (14 - A), b0 << 1, t);
+        t = and_or(rd_dword(u, 3 * Q + 2) >> (13 - A), b0 << 2, t);
+        p[i] = __builtin_bit_cast(uint32_t, __builtin_elementwise_fma(__builtin_bit_cast(half2_t, t), sc.D, sc.C));
       }
     }
   }
@@ -1146,7 +1172,7 @@ __global__ __launch_bounds__(RD_THREADS, 1) void gateup_rd_kernel(DecodeArgs a) 
   const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
   const int m0 = a.tiles_rd[2 + 2 * mt];
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
-  if (!tg.codes || !tu.codes || tg.bits > 4 || tu.bits > 4) return;
+  if (!tg.codes || !tu.codes || !rd_ok(tg) || !rd_ok(tu)) return;
   const int Mt = min(RD_T, sl.M - m0);
   const GemmArgs g = gemm_args(a);
   const int f0 = nt * (RD_ROWS / 2);
@@ -1170,7 +1196,7 @@ __global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
   const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
   const int m0 = a.tiles_rd[2 + 2 * mt];
   const TensorDev td = a.desc[sl.desc * 3 + 2];
-  if (!td.codes || td.bits > 4) return;
+  if (!td.codes || !rd_ok(td)) return;
   const int Mt = min(RD_T, sl.M - m0);
   const GemmArgs g = gemm_args(a);
   const int n0 = nt * RD_ROWS;
@@ -1188,7 +1214,8 @@ __global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
 
 // Diagnostic: one tensor through the grouped GEMMs' decoders, one thread per
 // (row, unit): binary16 d * (c - z) bit patterns in natural weight order
-// (rd_piece for 2-4 bits, decode_blk for 5/6/8).
+// (rd_piece for the tensors the register-decoded GEMMs take, decode_blk for
+// the others, as the LDS-decoded GEMMs do).
 template <int B>
 __global__ __launch_bounds__(256) void dequant_gemm_kernel(TensorDev t, uint16_t* out) {
   const int U = t.K / kUnit;
@@ -1198,7 +1225,8 @@ __global__ __launch_bounds__(256) void dequant_gemm_kernel(TensorDev t, uint16_t
   const MOEQ_GLOBAL u32x4* rc = row_chunks(t, B, r);
   const MOEQ_GLOBAL uint16_t* rs = gptr(t.scales + (size_t)r * (t.K / kBlock));
   u32x4* o = reinterpret_cast<u32x4*>(out + (size_t)r * t.K + kUnit * u);
-  if constexpr (B <= 4) {
+  if (rd_ok(t)) {
+    if constexpr (B <= 4) {
     RdUnit<B> un;
 #pragma unroll
     for (int j = 0; j < B; ++j) un.c[j] = rc[(size_t)j * U + u];
@@ -1210,6 +1238,7 @@ __global__ __launch_bounds__(256) void dequant_gemm_kernel(TensorDev t, uint16_t
     DQG(2, 0); DQG(2, 1); DQG(2, 2); DQG(2, 3);
     DQG(3, 0); DQG(3, 1); DQG(3, 2); DQG(3, 3);
 #undef DQG
+    }
   } else {
     __attribute__((aligned(16))) _Float16 blk[32];
 #define DQW(Q)                                                                    \
@@ -1282,7 +1311,7 @@ hipError_t launch_prefill_tiles(const DecodeArgs& a, hipStream_t s) {
 hipError_t launch_gateup_prefill(const DecodeArgs& a, hipStream_t s) {
   hipError_t e = launch_gemm(gateup_rd_kernel, g_attr_gu_rd, RD_THREADS, tile_grid(a.max_rtiles, (a.I + RD_ROWS / 2 - 1) / (RD_ROWS / 2)),
                              RD_LDS, s, a);
-  if (e == hipSuccess && a.wide_gateup) {
+  if (e == hipSuccess && a.lds_gateup) {
     const size_t lds = (size_t)2 * (BM + 2 * BN) * LDS_STRIDE * sizeof(_Float16);
     e = launch_gemm(gateup_gemm8_kernel, g_attr_gu_w, 512, tile_grid(a.max_mtiles, a.I / BN), lds, s, a);
   }
@@ -1296,7 +1325,7 @@ hipError_t launch_down_prefill(const DecodeArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   e = launch_gemm(down_rd_kernel, g_attr_dn_rd, RD_THREADS, tile_grid(a.max_rtiles, (a.H + RD_ROWS - 1) / RD_ROWS),
                   RD_LDS, s, a);
-  if (e == hipSuccess && a.wide_down) {
+  if (e == hipSuccess && a.lds_down) {
     const size_t lds = (size_t)2 * (BM + BN) * LDS_STRIDE * sizeof(_Float16);
     e = launch_gemm(down_gemm8_kernel, g_attr_dn_w, 512, tile_grid(a.max_mtiles, a.H / BN), lds, s, a);
   }

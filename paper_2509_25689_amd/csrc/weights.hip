@@ -213,6 +213,26 @@ hipError_t launch_repack(const uint8_t* canon, int rows, int K, int bits, uint32
   return hipGetLastError();
 }
 
+namespace {
+__global__ __launch_bounds__(256) void scale_key_max_kernel(const uint16_t* sc, size_t n, uint32_t* out) {
+  uint32_t m = 0;
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+    const uint32_t v = sc[i], mag = v & 0x7FFFu;
+    m = max(m, (v & 0x8000u) || mag == 0 || mag >= 0x7C00u ? 0xFFFFu : mag);
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+  if ((threadIdx.x & 63) == 0 && m) atomicMax(out, m);
+}
+}  // namespace
+
+hipError_t launch_scale_key_max(const uint16_t* scales, size_t n, uint32_t* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const size_t want = (n + 255) / 256;
+  const int grid = (int)(want < 1024 ? want : 1024);
+  scale_key_max_kernel<<<grid, 256, 0, s>>>(scales, n, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_dequant_sub(const TensorDev& t, float* out, hipStream_t s) {
   const long long n = (long long)t.rows * (t.K / kUnit);
   const int grid = (int)((n + 255) / 256);
