@@ -10,17 +10,19 @@
 // Arithmetic: activations (bf16, exact in binary16 after a per-token
 // power-of-two prescale), dequantized weights fp16(d * (c - z)) (one rounding)
 // and the SwiGLU activations h (binary16 after a per-row power-of-two
-// prescale) enter v_mfma_f32_16x16x32_f16 with float32 accumulation.
+// prescale) enter binary16 matrix instructions with float32 accumulation.
 //
-// 2-4-bit tensors (every tensor of the workloads measured here) take the
-// register-decoded GEMMs below: the packed weights are decoded in registers
-// straight into the matrix operand, tokens are the 16-wide side of the
-// matrix tiles.  Tiles with a 5, 6 or 8-bit tensor take the LDS-decoded
-// GEMMs (gateup_gemm8_kernel, down_gemm8_kernel): 128 tokens x 128 weight
-// rows per workgroup, the weight tile of each K step decoded once into LDS.
-// Workgroups are mapped to tiles from the tile count on the device: each XCD
-// takes an equal run of consecutive m-tiles (one expert's tiles share its
-// L2), whatever the worst-case size of the grid.
+// 2-4-bit tensors whose block scales are positive, finite and within the
+// register decoder's bound (every tensor of the workloads measured here) take
+// the register-decoded GEMMs below (v_mfma_f32_32x32x16_f16, tiles of up to
+// 128 tokens): the packed weights are decoded in registers straight into the
+// matrix operand.  Every other tensor (5, 6 or 8 bits, or scales outside the
+// bound) takes the LDS-decoded GEMMs (gateup_gemm8_kernel, down_gemm8_kernel,
+// v_mfma_f32_16x16x32_f16): 128 tokens x 128 weight rows per workgroup, the
+// weight tile of each K step decoded once into LDS.  Workgroups are mapped to
+// tiles from the tile count on the device: each XCD takes an equal run of
+// consecutive tiles (one expert's tiles share its L2), whatever the
+// worst-case size of the grid.
 #include <atomic>
 
 #include "internal.h"
@@ -660,35 +662,33 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
 // Weights are the MFMA's first operand (32 weight rows x 16 k) and tokens
 // its second (16 k x 32 tokens) of v_mfma_f32_32x32x16_f16 (on gfx950 it
 // runs at twice the rate of the 16 x 16 x 32 shape), so a bucket of M tokens
-// costs ceil(M / 32) token tiles per 32 weight rows.  A workgroup of four
-// waves owns 256 weight rows and up to 64 tokens of one expert bucket; each
-// wave owns 64 weight rows (two row tiles) and all the tokens (two token
-// tiles), 2 x 2 accumulator tiles of 32 x 32.  Two workgroups share a
-// compute unit, so the two waves on a SIMD come from independent workgroups
-// and one's waits (loads, barriers) are covered by the other's work.
+// costs ceil(M / 32) token tiles per 32 weight rows.  A workgroup of eight
+// waves owns up to 128 tokens of one expert bucket and 256 weight rows; each
+// wave owns one row tile of 32 and all the tokens (1-4 token tiles), so one
+// decoded weight fragment feeds up to four matrix instructions.  One
+// workgroup per compute unit (two waves per SIMD).
 //
-// Weights never pass through LDS.  Lane l of a wave (row r = l % 32 of each
+// Weights never pass through LDS.  Lane l of a wave (row r = l % 32 of its
 // row tile, k-half g = l / 32) loads, for each K stage of 512 weights (4
-// units of 128), units 4U + 2g and 4U + 2g + 1 of its rows: the two lanes of
+// units of 128), units 4U + 2g and 4U + 2g + 1 of its row: the two lanes of
 // a row read 64 contiguous bytes per chunk plane.  It decodes them in
 // registers straight into the operand layout, binary16 d * (c - 2^(b-1))
 // with one rounding: at k step t (0..7) of sub-stage q (block q of each
 // unit), the 8 operand values of lane (r, g) are weights 32 q + 8 (t % 4) ..
 // + 7 of unit 4U + 2g + t / 4.  The activation operand of lane (c, g) must
 // hold the same k values, which the LDS tile provides: activations go through
-// LDS in sub-stages of 128 k values (block q of the stage's four units), 64
+// LDS in sub-stages of 128 k values (block q of the stage's four units), 128
 // token rows of 16 pieces of 16 bytes, piece p = 4 u + m (unit u of the
 // stage, piece m of its block) stored at position p ^ (row % 16) of its row
 // (no bank conflicts for the 16-byte fragment reads).  Four LDS buffers:
 // sub-stage s + 2 is requested when s begins and stored when it ends.
 //
-// gate/up: waves 0 and 1 own 64 gate rows each, waves 2 and 3 the same
-// features' up rows (each wave works on one tensor, so on one width); the
-// up waves hand their accumulators to the gate waves through LDS for the
-// SwiGLU epilogue.  down: four waves of 64 output features of one tensor.
-// The K loop is instantiated per width and per token count (up to 32
-// tokens: one token tile, else two), so a small bucket does not spend
-// matrix instructions on an empty tile, and the loop has no branches.
+// gate/up: waves 0-3 own 32 gate rows each, waves 4-7 the same features' up
+// rows (each wave works on one tensor, so on one width); the up waves hand
+// their accumulators to the gate waves through LDS for the SwiGLU epilogue.
+// down: eight waves of 32 output features of one tensor.  The K loop is
+// instantiated per width and per token-tile count, so a small bucket does
+// not spend matrix instructions on empty tiles, and the loop has no branches.
 constexpr int RD_T = kRdTile;         // tokens per workgroup tile
 constexpr int RD_WAVES = 8;
 constexpr int RD_THREADS = 64 * RD_WAVES;
