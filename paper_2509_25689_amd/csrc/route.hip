@@ -310,34 +310,47 @@ __device__ LaneChoice<EPL> route_token_wave(const RouterParams& rp, int t, float
   int hi = ci[0];
   float sum = 0.0f, my_s = 0.0f;
   int my_i = 0, last = 0;
-  for (int r = 0; r < rp.k; ++r) {
+  // branch-free rounds (selects, not exec masks), unrolled by 8: each round
+  // is a short dependency chain, and taken branches would dominate it
+  auto round = [&](int r) {
     const uint32_t m = wave_max_u32(hk);
-    const uint64_t hold = m ? __ballot(hk == m) : 0ull;
+    const uint64_t hold = __ballot((hk == m) & (m != 0u));
     // creation checks guarantee k candidates; never leave the index range
+    // (the lane reads are unconditional; the selects follow them)
     const int wl = hold ? (int)__builtin_ctzll(hold) : 0;
     const int li = __builtin_amdgcn_readlane(hi, wl);
-    const float sv = hold ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hs), wl)) : 0.0f;
+    const float sr = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, hs), wl));
+    const float sv = hold ? sr : 0.0f;
     const int e = hold ? wl * EPL + li : last;
-    if (hold && lane == wl) {
-      ch.bits |= 1u << hi;
+    const bool win = hold && lane == wl;
+    ch.bits |= win ? 1u << hi : 0u;
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) ch.order[i] = i == hi ? r : ch.order[i];
-      ++pos;
-      hk = 0u;
+    for (int i = 0; i < EPL; ++i) ch.order[i] = win && i == hi ? r : ch.order[i];
+    const int np = pos + 1;
+    uint32_t nk = 0u;
+    float ns = hs;
+    int ni = hi;
 #pragma unroll
-      for (int i = 1; i < EPL; ++i) {
-        hk = pos == i ? key[i] : hk;
-        hs = pos == i ? cs[i] : hs;
-        hi = pos == i ? ci[i] : hi;
-      }
+    for (int i = 1; i < EPL; ++i) {
+      nk = np == i ? key[i] : nk;
+      ns = np == i ? cs[i] : ns;
+      ni = np == i ? ci[i] : ni;
     }
+    pos = win ? np : pos;
+    hk = win ? nk : hk;
+    hs = win ? ns : hs;
+    hi = win ? ni : hi;
     sum = sum + sv;
-    if (lane == r) {
-      my_i = e;
-      my_s = sv;
-    }
+    my_i = lane == r ? e : my_i;
+    my_s = lane == r ? sv : my_s;
     last = e;
+  };
+  int r = 0;
+  for (; r + 8 <= rp.k; r += 8) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) round(r + q);
   }
+  for (; r < rp.k; ++r) round(r);
   if (lane < rp.k) {
     float wv;
     if (rp.norm)

@@ -214,21 +214,41 @@ hipError_t launch_repack(const uint8_t* canon, int rows, int K, int bits, uint32
 }
 
 namespace {
+__device__ __forceinline__ uint32_t scale_key(uint32_t v) {
+  const uint32_t mag = v & 0x7FFFu;
+  return (v & 0x8000u) || mag == 0 || mag >= 0x7C00u ? 0xFFFFu : mag;
+}
+
+// 8 scales per thread and load, a workgroup maximum in LDS, one atomic per
+// workgroup
 __global__ __launch_bounds__(256) void scale_key_max_kernel(const uint16_t* sc, size_t n, uint32_t* out) {
+  __shared__ uint32_t wmax[4];
   uint32_t m = 0;
-  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
-    const uint32_t v = sc[i], mag = v & 0x7FFFu;
-    m = max(m, (v & 0x8000u) || mag == 0 || mag >= 0x7C00u ? 0xFFFFu : mag);
+  const size_t n8 = n / 8;
+  const u32x4* s8 = reinterpret_cast<const u32x4*>(sc);
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (size_t)gridDim.x * 256) {
+    const u32x4 v = s8[i];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) m = max(m, max(scale_key(w[j] & 0xFFFFu), scale_key(w[j] >> 16)));
   }
+  for (size_t i = n8 * 8 + (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+    m = max(m, scale_key(sc[i]));
   for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
-  if ((threadIdx.x & 63) == 0 && m) atomicMax(out, m);
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    m = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+    if (m) atomicMax(out, m);
+  }
 }
 }  // namespace
 
 hipError_t launch_scale_key_max(const uint16_t* scales, size_t n, uint32_t* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
-  const size_t want = (n + 255) / 256;
-  const int grid = (int)(want < 1024 ? want : 1024);
+  // the scales are 256-byte aligned in the layer's store (16-byte loads)
+  const size_t want = (n / 8 + 255) / 256 + 1;
+  const int grid = (int)(want < 256 ? want : 256);
   scale_key_max_kernel<<<grid, 256, 0, s>>>(scales, n, out);
   return hipGetLastError();
 }
