@@ -40,17 +40,31 @@ constexpr int BM = kGemmBM, BN = 128, BK = 64;
 // halves per LDS row: 16 halves of padding (measured best of 8, 16, 24, 40)
 constexpr int LDS_STRIDE = BK + 16;
 
+constexpr int kXcds = 8;  // the hardware deals workgroup ids to them round-robin
+#ifndef MOEQ_RD_DEAL
+#define MOEQ_RD_DEAL 1
+#endif
+constexpr int kRdDeal = MOEQ_RD_DEAL;  // register-decoded tiles dealt to an XCD at a time
+
 // ---- tile lists: slot order = shared experts, then active experts; every
-// bucket of M rows becomes ceil(M / 128) tiles of up to 128 rows (tiles_all,
-// for the LDS-decoded GEMMs) and ceil(M / 64) tiles of up to 64 rows
-// (tiles_rd, for the register-decoded GEMMs), large and small buckets
-// interleaved in slot order, so every XCD's share mixes both.  Also clears
-// the running maxima of the h rows.
+// bucket of M rows becomes ceil(M / 128) tiles of up to 128 rows.  tiles_all
+// (the LDS-decoded GEMMs) keeps slot order, large and small buckets
+// interleaved, so every XCD's share mixes both.  tiles_rd (the
+// register-decoded GEMMs) holds a run of tiles_rd[0] positions per XCD (empty
+// ones -1): the tiles sorted by work (full tiles in slot order, then the
+// remainders by decreasing row count) and dealt to the XCDs in turn in groups
+// of kRdDeal, so every XCD gets nearly the same work and runs its largest
+// tiles first (kRdDeal = 0: slot order).  Also clears the running maxima of
+// the h rows.
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
+  constexpr int kCls = kRdTile / 32;  // remainder classes by 32-row steps
   __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];
   __shared__ int32_t off[kMaxShared + kMaxExperts + 2];
-  __shared__ int32_t cnt2[kMaxShared + kMaxExperts + 1];
-  __shared__ int32_t off2[kMaxShared + kMaxExperts + 2];
+  __shared__ int32_t full[kMaxShared + kMaxExperts + 1];  // full register-decoded tiles of the slot
+  __shared__ int32_t foff[kMaxShared + kMaxExperts + 1];  // sorted index of the first one
+  __shared__ int32_t rpos[kMaxShared + kMaxExperts + 1];  // remainder rows, then its sorted index or -1
+  __shared__ int32_t soff[kMaxShared + kMaxExperts + 1];  // the slot's first tile in slot order
+  __shared__ int32_t run_len;
   const int tid = threadIdx.x;
   const int nslots = a.S + a.active[0];
   for (int s = tid; s < nslots; s += 1024) {
@@ -62,24 +76,41 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
       M = a.offsets[e + 1] - a.offsets[e];
     }
     cnt[s] = (M + BM - 1) / BM;
-    cnt2[s] = (M + kRdTile - 1) / kRdTile;
+    full[s] = M / kRdTile;
+    rpos[s] = M % kRdTile;
   }
+  for (int t = tid; t < a.max_rtiles; t += 1024) a.tiles_rd[1 + 2 * t] = -1;
   // rows of h whose running maxima the gate/up epilogue accumulates
   const int rows = a.n * (a.k + a.S);
   for (int r = tid; r < rows; r += 1024) a.rowmax[r] = 0u;
   __syncthreads();
   if (tid == 0) {
-    int run = 0, run2 = 0;
+    int run = 0, F = 0, so = 0;
+    int ncls[kCls + 1] = {};
     for (int s = 0; s < nslots; ++s) {
       off[s] = run;
-      off2[s] = run2;
       run += cnt[s];
-      run2 += cnt2[s];
+      foff[s] = F;
+      F += full[s];
+      soff[s] = so;
+      so += full[s] + (rpos[s] ? 1 : 0);
+      if (rpos[s]) ++ncls[(rpos[s] + 31) / 32];
     }
     a.tiles_all[0] = min(run, a.max_mtiles);
-    a.tiles_rd[0] = min(run2, a.max_rtiles);
+    int base[kCls + 1];
+    int T = F;
+    for (int c = kCls; c >= 1; --c) {
+      base[c] = T;
+      T += ncls[c];
+    }
+    for (int s = 0; s < nslots; ++s) rpos[s] = rpos[s] ? base[(rpos[s] + 31) / 32]++ : -1;
+    int B = kRdDeal ? kRdDeal * ((T + kRdDeal * kXcds - 1) / (kRdDeal * kXcds)) : (T + kXcds - 1) / kXcds;
+    B = min(B, a.max_rtiles / kXcds);
+    run_len = B;
+    a.tiles_rd[0] = B;
   }
   __syncthreads();
+  const int B = run_len;
   for (int s = tid; s < nslots; s += 1024) {
     for (int i = 0; i < cnt[s]; ++i) {
       const int t = off[s] + i;
@@ -88,9 +119,22 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
         a.tiles_all[2 + 2 * t] = i * BM;
       }
     }
-    for (int i = 0; i < cnt2[s]; ++i) {
-      const int t = off2[s] + i;
-      if (t < a.max_rtiles) {
+    for (int i = 0; i <= full[s]; ++i) {
+      int si;  // sorted index
+      if (i < full[s])
+        si = foff[s] + i;
+      else if (rpos[s] >= 0)
+        si = rpos[s];
+      else
+        break;
+      int t;
+      if (kRdDeal) {
+        const int q = si / kRdDeal, x = q % kXcds;
+        t = x * B + kRdDeal * (q / kXcds) + si % kRdDeal;
+      } else {
+        t = soff[s] + i;
+      }
+      if (t < kXcds * B) {
         a.tiles_rd[1 + 2 * t] = s;
         a.tiles_rd[2 + 2 * t] = i * kRdTile;
       }
@@ -125,7 +169,6 @@ __device__ __forceinline__ SlotInfo slot_of(const DecodeArgs& a, int s) {
 // so one m-tile's activations stay in one L2 and every XCD gets the same
 // share of the T tiles present, however large the grid (which covers
 // 8 ceil(Tmax / 8) m-tiles).  False for a workgroup without a tile.
-constexpr int kXcds = 8;
 __device__ __forceinline__ bool tile_of_wg(int hw, int T, int nN, int* mt, int* nt) {
   const int x = hw % kXcds, j = hw / kXcds;
   const int B = (T + kXcds - 1) / kXcds;
@@ -136,6 +179,19 @@ __device__ __forceinline__ bool tile_of_wg(int hw, int T, int nN, int* mt, int* 
   return *mt < T;
 }
 inline int tile_grid(int max_tiles, int nN) { return (max_tiles + kXcds - 1) / kXcds * kXcds * nN; }
+
+// Workgroup -> (list position, n-tile) in the register-decoded tile list:
+// XCD x takes the B = tiles_rd[0] positions [x B, x B + B), all n-tiles of a
+// position in a row.  False for a workgroup past the run or at an empty
+// position.
+__device__ __forceinline__ bool rd_tile_of_wg(const int32_t* tiles, int hw, int nN, int* mt, int* nt) {
+  const int x = hw % kXcds, j = hw / kXcds;
+  const int lm = j / nN;
+  if (lm >= tiles[0]) return false;
+  *mt = x * tiles[0] + lm;
+  *nt = j % nN;
+  return tiles[1 + 2 * *mt] >= 0;
+}
 
 // The register-decoded GEMMs take a tensor of 2-4 bits whose scales the
 // create-time scan found positive, finite and small enough (flags); the
@@ -1168,7 +1224,7 @@ __global__ __launch_bounds__(RD_THREADS, 1) void gateup_rd_kernel(DecodeArgs a) 
   extern __shared__ __attribute__((aligned(16))) char lds_c[];
   const int nN = (a.I + RD_ROWS / 2 - 1) / (RD_ROWS / 2);
   int mt, nt;
-  if (!tile_of_wg(blockIdx.x, a.tiles_rd[0], nN, &mt, &nt)) return;
+  if (!rd_tile_of_wg(a.tiles_rd, blockIdx.x, nN, &mt, &nt)) return;
   const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
   const int m0 = a.tiles_rd[2 + 2 * mt];
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
@@ -1192,7 +1248,7 @@ __global__ __launch_bounds__(RD_THREADS, 1) void down_rd_kernel(DecodeArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds_c[];
   const int nN = (a.H + RD_ROWS - 1) / RD_ROWS;
   int mt, nt;
-  if (!tile_of_wg(blockIdx.x, a.tiles_rd[0], nN, &mt, &nt)) return;
+  if (!rd_tile_of_wg(a.tiles_rd, blockIdx.x, nN, &mt, &nt)) return;
   const SlotInfo sl = slot_of(a, a.tiles_rd[1 + 2 * mt]);
   const int m0 = a.tiles_rd[2 + 2 * mt];
   const TensorDev td = a.desc[sl.desc * 3 + 2];
@@ -1261,7 +1317,13 @@ int prefill_max_tiles(int n, int k, int S, int n_kept, int rows) {
 }
 
 int prefill_max_mtiles(int n, int k, int S, int n_kept) { return prefill_max_tiles(n, k, S, n_kept, BM); }
-int prefill_max_rtiles(int n, int k, int S, int n_kept) { return prefill_max_tiles(n, k, S, n_kept, kRdTile); }
+// capacity of the register-decoded list: 8 runs of the longest run any count
+// of tiles up to the largest needs
+int prefill_max_rtiles(int n, int k, int S, int n_kept) {
+  const int T = prefill_max_tiles(n, k, S, n_kept, kRdTile);
+  const int g = kRdDeal ? kRdDeal * kXcds : kXcds;
+  return (T + g - 1) / g * g;
+}
 
 namespace {
 
