@@ -755,6 +755,7 @@ constexpr int RD_ROWS = RD_WAVES * RD_WROWS;  // weight rows per workgroup
 constexpr int RD_SUB = RD_T * 256;    // bytes of one activation sub-stage
 constexpr int RD_NBUF = 4;            // activation sub-stages resident in LDS
 constexpr int RD_APT = RD_SUB / 16 / RD_THREADS;  // 16-byte staging pieces per thread and sub-stage
+static_assert(RD_THREADS / 16 == 32, "staging piece j of a thread lies in token tile j");
 constexpr size_t RD_LDS = (size_t)RD_NBUF * RD_SUB;
 static_assert(RD_WAVES * RD_WROWS == RD_ROWS, "the waves cover the workgroup's rows");
 static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * RD_NTMAX * 64 * 64,
@@ -903,15 +904,16 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
   char* wdst = lds + tid * 16;
 
   // the staging pieces of sub-stage s (stage s / 4, block s % 4)
+  // (only the NT token tiles that are multiplied are staged)
   auto aload = [&](u32x4 (&v)[RD_APT], int s) {
     const int unit = min(4 * (s >> 2) + su, Uk - 1);
     const int off = unit * 16 + 4 * (s & 3) + sm;
 #pragma unroll
-    for (int j = 0; j < RD_APT; ++j) v[j] = arow[j][off];
+    for (int j = 0; j < NT; ++j) v[j] = arow[j][off];
   };
   auto astore = [&](const u32x4 (&v)[RD_APT], int buf) {
 #pragma unroll
-    for (int j = 0; j < RD_APT; ++j)
+    for (int j = 0; j < NT; ++j)
       *reinterpret_cast<u32x4*>(wdst + buf * RD_SUB + j * (RD_THREADS * 16)) = v[j];
   };
   // chunk j / scale half h of this lane's two units in stage U, every row tile
@@ -1087,11 +1089,12 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
     rc[r] = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)row * bits * Uk * 4));
     rs[r] = gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (H / kBlock)));
   }
-  // staging slots of this thread: rows j * 16 + tid / 16, piece (tid % 16) ^ (row % 16)
+  // staging slots of this thread: rows j * 32 + tid / 16 (token tile j < NT),
+  // piece (tid % 16) ^ (row % 16)
   const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
-  const MOEQ_GLOBAL u32x4* arow[RD_APT];
+  const MOEQ_GLOBAL u32x4* arow[RD_APT] = {};
 #pragma unroll
-  for (int j = 0; j < RD_APT; ++j) {
+  for (int j = 0; j < NT; ++j) {
     int ar = j * (RD_THREADS / 16) + (tid >> 4);
     ar = ar < Mt ? ar : 0;
     const int tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
@@ -1170,9 +1173,9 @@ __device__ void rd_down_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int 
     rc[r] = gptr(reinterpret_cast<const u32x4*>(td.codes + (size_t)row * bits * Uk * 4));
     rs[r] = gptr(reinterpret_cast<const u32x2*>(td.scales + (size_t)row * (I / kBlock)));
   }
-  const MOEQ_GLOBAL u32x4* arow[RD_APT];
+  const MOEQ_GLOBAL u32x4* arow[RD_APT] = {};
 #pragma unroll
-  for (int j = 0; j < RD_APT; ++j) {
+  for (int j = 0; j < NT; ++j) {
     int ar = j * (RD_THREADS / 16) + (tid >> 4);
     ar = ar < Mt ? ar : 0;
     arow[j] = gptr(reinterpret_cast<const u32x4*>(a.h16 + (size_t)(sl.base + m0 + ar) * I));
