@@ -422,7 +422,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
       if ((he = upload(E + s, p, shared[s * 3 + p])) != hipSuccess) return bail(he, "weight upload");
 
   // tensors the grouped GEMMs' register decoder cannot take (wider than 4
-  // bits, or a scale outside (0, rd_scale_limit(bits)])
+  // bits, a scale outside (0, rd_scale_limit(bits)], or rows of an odd number
+  // of 128-weight units)
   {
     std::vector<uint32_t> keys(plan.size());
     if ((he = hipMemcpy(keys.data(), scale_keys, sizeof(uint32_t) * plan.size(), hipMemcpyDeviceToHost)) !=
@@ -431,7 +432,8 @@ moeq_status moeq_layer_create(const moeq_config* cfg, const uint8_t* expert_mask
     for (size_t i = 0; i < plan.size(); ++i) {
       TensorDev& d = L->desc_host[i];
       if (!d.codes) continue;
-      if (d.bits <= 4 && keys[i] > rd_scale_limit(d.bits)) d.flags |= kTensorOffRegisterDecoder;
+      if (d.bits <= 4 && (keys[i] > rd_scale_limit(d.bits) || (d.K / kUnit) % 2 != 0))
+        d.flags |= kTensorOffRegisterDecoder;
       if (d.bits > 4 || (d.flags & kTensorOffRegisterDecoder)) {
         if (i % 3 == 2)
           L->lds_down = 1;

@@ -41,10 +41,11 @@ struct TensorDev {
   int32_t flags;  // kTensor* bits
 };
 
-// TensorDev.flags: some block scale of the tensor is not a positive finite
-// binary16 at most rd_scale_limit(bits), so the grouped GEMMs' register
-// decoder (which forms d * (c - z) from d * 2^(14 + b)) cannot take it; its
-// tiles go to the LDS-decoded kernels instead.
+// TensorDev.flags: the grouped GEMMs' register-decoded kernels cannot take
+// the tensor, because some block scale is not a positive finite binary16 at
+// most rd_scale_limit(bits) (they form d * (c - z) from d * 2^(14 + b)) or
+// its rows hold an odd number of 128-weight units (they load the scales of
+// two units at once); its tiles go to the LDS-decoded kernels instead.
 constexpr int32_t kTensorOffRegisterDecoder = 1;
 // Largest binary16 bit pattern of a scale d with d * 2^(14 + b) finite.
 constexpr uint32_t rd_scale_limit(int b) { return 0x7BFFu - ((uint32_t)(14 + b) << 10); }

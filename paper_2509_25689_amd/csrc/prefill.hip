@@ -194,8 +194,9 @@ __device__ __forceinline__ bool rd_tile_of_wg(const int32_t* tiles, int hw, int 
 }
 
 // The register-decoded GEMMs take a tensor of 2-4 bits whose scales the
-// create-time scan found positive, finite and small enough (flags); the
-// LDS-decoded GEMMs take every other tensor.
+// create-time scan found positive, finite and small enough and whose rows
+// hold an even number of units (flags); the LDS-decoded GEMMs take every
+// other tensor.
 __device__ __forceinline__ bool rd_ok(const TensorDev& t) {
   return t.bits <= 4 && !(t.flags & kTensorOffRegisterDecoder);
 }
@@ -883,20 +884,28 @@ __device__ __forceinline__ half8 rd_piece(const RdUnit<B>& u, const RdConsts& k)
 // The K loop of one wave.  ACT: the wave owns weight rows (else it only
 // stages activations, e.g. rows past the end of the tensor).  rc/rs: per row
 // tile, this lane's row chunk base and scale pairs; arow: the activation rows
-// this thread stages (row j * 16 + tid / 16 of the tile), as 16-byte pieces;
-// su/sm: the unit and piece of the thread's staging slot; zero: a zeroed
-// word (the scales of units past the row).
-template <int B, int NT, bool ACT>
+// this thread stages (row j * 32 + tid / 16 of the tile), as 16-byte pieces;
+// su/sm: the unit and piece of the thread's staging slot; zero: 16 zeroed
+// bytes, 16-byte aligned (the scales of units past the row).
+//
+// Prefetch depths: AL register sets of activation pieces (sub-stage s + AL
+// is requested when s begins) and a ring of WL stages of weight registers
+// (each chunk is requested 4 WL - 2 sub-stages before the sub-stage that
+// first uses it, as soon as the ring slot's previous stage has finished with
+// it).
+template <int B, int NT, bool ACT, int AL, int WL>
 __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD_RT],
                                          const MOEQ_GLOBAL u32x2* const (&rs)[RD_RT], int Uk,
                                          const MOEQ_GLOBAL u32x4* const (&arow)[RD_APT], int su, int sm,
                                          const MOEQ_GLOBAL uint32_t* zero, char* lds, int tid, int lane,
                                          f32x16 (&acc)[RD_RT][NT]) {
-  const int NS = (Uk + 3) / 4;      // K stages of 4 units
-  const int NSUB = 4 * NS;          // activation sub-stages
+  static_assert(WL >= 1 && AL >= 2 && (4 * WL) % AL == 0, "staging sets cycle within the unrolled stages");
+  const int NS = (Uk + 3) / 4;                  // K stages of 4 units
+  const int NSp = (NS + WL - 1) / WL * WL;      // stages run (a stage past NS has zero weights)
+  const int NSUB = 4 * NS;                      // activation sub-stages
   const int g = lane >> 5;
   const RdConsts kc = rd_consts<B>();
-  RdUnit<B> raw[RD_RT][2];          // [row tile][unit 2g, 2g + 1 of the stage]
+  RdUnit<B> raw[WL][RD_RT][2];                  // [ring slot][row tile][unit 2g, 2g + 1 of the stage]
   // fragment read offset of k step t (bytes within a sub-stage buffer):
   // row c = lane % 32, piece (8 g + t) ^ (c % 16) = 8 (g ^ (c / 8 % 2)) + (t ^ (c % 8)),
   // i.e. fbase ^ 16 t with fbase's bits 4-6 holding c % 8
@@ -916,65 +925,93 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
     for (int j = 0; j < NT; ++j)
       *reinterpret_cast<u32x4*>(wdst + buf * RD_SUB + j * (RD_THREADS * 16)) = v[j];
   };
-  // chunk j / scale half h of this lane's two units in stage U, every row tile
-  auto rload_chunk = [&](int j, int U) {
+  // chunk j / scale half h of this lane's two units in stage V, every row
+  // tile, into one ring slot.  Plain (not streaming) loads: a stage reads 64
+  // bytes of each row's chunk plane, half of a 128-byte line whose other half
+  // the next stage reads, so the line has to stay in L2 until then
+  // (streaming loads here cost 20%).
+  auto rload_chunk = [&](RdUnit<B> (&dst)[RD_RT][2], int j, int V) {
     if constexpr (ACT) {
 #pragma unroll
       for (int v = 0; v < 2; ++v) {
-        const int uc = min(4 * U + 2 * g + v, Uk - 1);
+        const int uc = min(4 * V + 2 * g + v, Uk - 1);
 #pragma unroll
-        for (int r = 0; r < RD_RT; ++r) raw[r][v].c[j] = __builtin_nontemporal_load(rc[r] + (size_t)j * Uk + uc);
+        for (int r = 0; r < RD_RT; ++r) dst[r][v].c[j] = rc[r][(size_t)j * Uk + uc];
       }
     }
   };
-  // (a unit past the row, in a partial last stage, reads its scales from a
-  // zeroed word, so its weights decode to zeros; the choice is made on the
-  // address, so no instruction waits for the loaded value)
-  auto rload_scale = [&](int h, int U) {
+  // the chunks that sub-stage f of stage V uses first (4 bits: chunk f;
+  // 3 bits: chunk f for f < 3, used again in sub-stage f + 1; 2 bits: chunk
+  // f / 2 for even f, used in f and f + 1)
+  auto rload_first = [&](RdUnit<B> (&dst)[RD_RT][2], int f, int V) {
+    if constexpr (B == 4) rload_chunk(dst, f, V);
+    if constexpr (B == 3) {
+      if (f < 3) rload_chunk(dst, f, V);
+    }
+    if constexpr (B == 2) {
+      if ((f & 1) == 0) rload_chunk(dst, f >> 1, V);
+    }
+  };
+  // the scales of this lane's two units of stage V (units 2g and 2g + 1 of
+  // the stage, four binary16 scales each: 16 contiguous bytes, as rows hold
+  // an even number of units), one load per row tile, requested in sub-stage
+  // 1 of the stage before and moved into the stage's ring slot at its end.
+  // A stage past the row reads 16 zero bytes, so its weights decode to zeros
+  // (the choice is made on the address, so no instruction waits for the
+  // loaded value).
+  u32x4 sn[RD_RT];
+  auto sload = [&](int V) {
+    if constexpr (ACT) {
+      const int unit = 4 * V + 2 * g;
+#pragma unroll
+      for (int r = 0; r < RD_RT; ++r) {
+        const MOEQ_GLOBAL u32x4* src = unit < Uk ? reinterpret_cast<const MOEQ_GLOBAL u32x4*>(rs[r] + unit)
+                                                 : reinterpret_cast<const MOEQ_GLOBAL u32x4*>(zero);
+        sn[r] = *src;
+      }
+    }
+  };
+  auto sput = [&](RdUnit<B> (&dst)[RD_RT][2]) {
     if constexpr (ACT) {
 #pragma unroll
-      for (int v = 0; v < 2; ++v) {
-        const int unit = 4 * U + 2 * g + v, uc = min(unit, Uk - 1);
-#pragma unroll
-        for (int r = 0; r < RD_RT; ++r) {
-          const MOEQ_GLOBAL uint32_t* src =
-              unit < Uk ? reinterpret_cast<const MOEQ_GLOBAL uint32_t*>(rs[r] + uc) + h : zero;
-          if (h == 0) raw[r][v].s.x = *src;
-          else raw[r][v].s.y = *src;
-        }
+      for (int r = 0; r < RD_RT; ++r) {
+        dst[r][0].s = u32x2{sn[r].x, sn[r].y};
+        dst[r][1].s = u32x2{sn[r].z, sn[r].w};
       }
     }
   };
 
-  // prologue: stage 0's codes (for 4 bits, chunks 0 and 1: each later chunk
-  // is requested two sub-stages before its use); sub-stage 0 stored, 1 in
-  // flight in the second staging set
-  if constexpr (ACT) {
+  // prologue: the chunks whose request point (4 V + f - (4 WL - 2) - 1)
+  // lies before the first sub-stage, in that order; sub-stage 0 stored,
+  // sub-stages 1 .. AL - 1 in flight
 #pragma unroll
-    for (int j = 0; j < (B == 4 ? 2 : B); ++j) rload_chunk(j, 0);
-    rload_scale(0, 0);
-    rload_scale(1, 0);
-  }
-  u32x4 xa[RD_APT], xb[RD_APT];
-  aload(xa, 0);
-  astore(xa, 0);
-  aload(xb, 1);
+  for (int V = 0; V < WL; ++V)
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+      if (4 * V + f < 4 * WL - 1) rload_first(raw[V], f, V);
+  sload(0);
+  sput(raw[0]);
+  u32x4 xs[AL][RD_APT];
+  aload(xs[0], 0);
+  astore(xs[0], 0);
+#pragma unroll
+  for (int i = 1; i < AL; ++i) aload(xs[i], min(i, NSUB - 1));
   __syncthreads();
 
-  // k step TS of sub-stage Q: operands into FA / FB (fragment reads from LDS
-  // and the weight decode), then the matrix products of a step whose operands
-  // are ready.  The steps of a sub-stage are software-pipelined: the operands
-  // of step t + 1 are prepared among the products of step t, and a
-  // scheduling barrier keeps the compiler from hoisting later steps' decodes
-  // (which costs registers and spills).
+  // k step TS of sub-stage Q (ring slot W): operands into FA / FB (fragment
+  // reads from LDS and the weight decode), then the matrix products of a
+  // step whose operands are ready.  The steps of a sub-stage are
+  // software-pipelined: the operands of step t + 1 are prepared among the
+  // products of step t, and a scheduling barrier keeps the compiler from
+  // hoisting later steps' decodes (which costs registers and spills).
   half8 fa0[RD_RT], fb0[NT], fa1[RD_RT], fb1[NT];
-#define RD_OPERANDS(Q, TS, FA, FB)                                                                      \
+#define RD_OPERANDS(W, Q, TS, FA, FB)                                                                   \
   do {                                                                                                  \
     if constexpr (ACT) {                                                                                \
       _Pragma("unroll") for (int T = 0; T < NT; ++T) FB[T] =                                            \
           *reinterpret_cast<const half8*>(lds + (Q) * RD_SUB + T * (32 * 256) + (fbase ^ (16 * (TS))));  \
       _Pragma("unroll") for (int r = 0; r < RD_RT; ++r) FA[r] =                                         \
-          rd_piece<B, Q, (TS) & 3>(raw[r][(TS) >> 2], kc);                                              \
+          rd_piece<B, Q, (TS) & 3>(raw[W][r][(TS) >> 2], kc);                                           \
     }                                                                                                   \
   } while (0)
 #define RD_PRODUCTS(FA, FB)                                                                             \
@@ -985,67 +1022,87 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
           __builtin_amdgcn_mfma_f32_32x32x16_f16(FA[r], FB[T], acc[r][T], 0, 0, 0);                     \
     }                                                                                                   \
   } while (0)
-#define RD_KSTEPS(Q)                                                                                    \
+#define RD_KSTEPS(W, Q)                                                                                 \
   do {                                                                                                  \
-    RD_OPERANDS(Q, 0, fa0, fb0);                                                                        \
-    RD_OPERANDS(Q, 1, fa1, fb1);                                                                        \
+    RD_OPERANDS(W, Q, 0, fa0, fb0);                                                                     \
+    RD_OPERANDS(W, Q, 1, fa1, fb1);                                                                     \
     RD_PRODUCTS(fa0, fb0);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 2, fa0, fb0);                                                                        \
+    RD_OPERANDS(W, Q, 2, fa0, fb0);                                                                     \
     RD_PRODUCTS(fa1, fb1);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 3, fa1, fb1);                                                                        \
+    RD_OPERANDS(W, Q, 3, fa1, fb1);                                                                     \
     RD_PRODUCTS(fa0, fb0);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 4, fa0, fb0);                                                                        \
+    RD_OPERANDS(W, Q, 4, fa0, fb0);                                                                     \
     RD_PRODUCTS(fa1, fb1);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 5, fa1, fb1);                                                                        \
+    RD_OPERANDS(W, Q, 5, fa1, fb1);                                                                     \
     RD_PRODUCTS(fa0, fb0);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 6, fa0, fb0);                                                                        \
+    RD_OPERANDS(W, Q, 6, fa0, fb0);                                                                     \
     RD_PRODUCTS(fa1, fb1);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
-    RD_OPERANDS(Q, 7, fa1, fb1);                                                                        \
+    RD_OPERANDS(W, Q, 7, fa1, fb1);                                                                     \
     RD_PRODUCTS(fa0, fb0);                                                                              \
     __builtin_amdgcn_sched_barrier(0);                                                                  \
     RD_PRODUCTS(fa1, fb1);                                                                              \
   } while (0)
 
-  // sub-stage s = 4U + Q in buffer Q: request sub-stage s + 2 into staging
-  // set X (free: its data went to LDS at the end of s - 1), multiply
-  // sub-stage s, store sub-stage s + 1 from the other set Y (requested when
-  // s - 1 began) into buffer (Q + 1) % 4 (free: its sub-stage s - 3 was read
-  // before earlier barriers), and request the codes of a later stage whose
-  // registers this sub-stage freed.  Each activation load thus has two
-  // sub-stages to arrive.  No branches: past the last sub-stage or stage the
-  // loads repeat the last one (clamped) and the stores go to buffers nobody
-  // reads again, so the compiler counts the outstanding loads exactly.
-#define RD_SUBSTAGE(Q, X, Y)                                                                            \
+  // sub-stage s = 4 (U + W) + Q in LDS buffer Q, weights in ring slot W:
+  // request sub-stage s + AL into the staging set that held s (stored at the
+  // end of s - 1), multiply sub-stage s, store sub-stage s + 1 (requested
+  // when s + 1 - AL began) into buffer (Q + 1) % 4 (free: its sub-stage s - 3
+  // was read before earlier barriers), and request the chunks that
+  // sub-stage Q - 1 of a stage uses first for stage U + W + WL (Q = 0: the
+  // chunks of sub-stage 3 for stage U + W + WL - 1), whose ring registers
+  // this sub-stage freed; sub-stage 1 requests the next stage's scales,
+  // sub-stage 3 moves them into its ring slot.  No branches: past the last
+  // sub-stage or stage the loads repeat the last one (clamped) and the stores
+  // go to buffers nobody reads again, so the compiler counts the outstanding
+  // loads exactly.
+#define RD_SUBSTAGE(W, Q)                                                                               \
   do {                                                                                                  \
-    aload(X, min(4 * U + (Q) + 2, NSUB - 1));                                                           \
-    RD_KSTEPS(Q);                                                                                       \
-    astore(Y, ((Q) + 1) & 3);                                                                           \
-    const int Un_ = min(U + 1, NS - 1);                                                                 \
-    if constexpr (B == 4) rload_chunk(((Q) + 2) & 3, (Q) < 2 ? U : Un_);                               \
-    if constexpr (B == 2 && ((Q) & 1)) rload_chunk((Q) >> 1, Un_);                                     \
-    if constexpr (B == 3 && (Q) >= 1) rload_chunk((Q) - 1, Un_);                                        \
-    if constexpr ((Q) == 1) rload_scale(0, Un_);                                                        \
-    if constexpr ((Q) == 3) rload_scale(1, Un_);                                                        \
+    aload(xs[(4 * (W) + (Q)) % AL], min(4 * (U + (W)) + (Q) + AL, NSUB - 1));                           \
+    RD_KSTEPS(W, Q);                                                                                    \
+    astore(xs[(4 * (W) + (Q) + 1) % AL], ((Q) + 1) & 3);                                                \
+    if constexpr ((Q) == 0)                                                                             \
+      rload_first(raw[((W) + WL - 1) % WL], 3, min(U + (W) + WL - 1, NSp));                             \
+    else                                                                                                \
+      rload_first(raw[W], (Q) - 1, min(U + (W) + WL, NSp));                                             \
+    if constexpr ((Q) == 1) sload(min(U + (W) + 1, NSp));                                               \
+    if constexpr ((Q) == 3) sput(raw[((W) + 1) % WL]);                                                  \
     __syncthreads();                                                                                    \
   } while (0)
 
-  for (int U = 0; U < NS; ++U) {
-    RD_SUBSTAGE(0, xa, xb);
-    RD_SUBSTAGE(1, xb, xa);
-    RD_SUBSTAGE(2, xa, xb);
-    RD_SUBSTAGE(3, xb, xa);
+  for (int U = 0; U < NSp; U += WL) {
+    RD_SUBSTAGE(0, 0);
+    RD_SUBSTAGE(0, 1);
+    RD_SUBSTAGE(0, 2);
+    RD_SUBSTAGE(0, 3);
+    if constexpr (WL == 2) {
+      RD_SUBSTAGE(1, 0);
+      RD_SUBSTAGE(1, 1);
+      RD_SUBSTAGE(1, 2);
+      RD_SUBSTAGE(1, 3);
+    }
   }
 #undef RD_SUBSTAGE
 #undef RD_KSTEPS
 #undef RD_PRODUCTS
 #undef RD_OPERANDS
 }
+
+// Prefetch depths of the K loop (deeper settings, with the registers the
+// smaller token-tile counts leave free, measured no faster: the loads are
+// limited by the requests each compute unit can keep in flight, not by
+// their latency).
+#ifndef MOEQ_RD_AL
+#define MOEQ_RD_AL 2
+#endif
+#ifndef MOEQ_RD_WL
+#define MOEQ_RD_WL 1
+#endif
 
 // Width dispatch of one wave's K loop (B is uniform per wave: one tensor).
 template <int NT>
@@ -1054,14 +1111,15 @@ __device__ __forceinline__ void rd_kloop_any(int bits, bool act, const MOEQ_GLOB
                                              const MOEQ_GLOBAL u32x4* const (&arow)[RD_APT], int su, int sm,
                                              const MOEQ_GLOBAL uint32_t* zero, char* lds, int tid, int lane,
                                              f32x16 (&acc)[RD_RT][NT]) {
+  constexpr int AL = MOEQ_RD_AL, WL = MOEQ_RD_WL;
   if (!act)
-    rd_kloop<2, NT, false>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+    rd_kloop<2, NT, false, AL, WL>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
   else if (bits == 2)
-    rd_kloop<2, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+    rd_kloop<2, NT, true, AL, WL>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
   else if (bits == 3)
-    rd_kloop<3, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+    rd_kloop<3, NT, true, AL, WL>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
   else
-    rd_kloop<4, NT, true>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
+    rd_kloop<4, NT, true, AL, WL>(rc, rs, Uk, arow, su, sm, zero, lds, tid, lane, acc);
 }
 
 // Accumulator element v (0..15) of lane l in a 32 x 32 tile: row (weight row)
