@@ -747,16 +747,26 @@ __global__ __launch_bounds__(512, 4) void down_gemm8_kernel(DecodeArgs a) {
 // instantiated per width and per token-tile count, so a small bucket does
 // not spend matrix instructions on empty tiles, and the loop has no branches.
 constexpr int RD_T = kRdTile;         // tokens per workgroup tile
-constexpr int RD_WAVES = 8;
+#ifndef MOEQ_RD_WAVES
+#define MOEQ_RD_WAVES 8
+#endif
+constexpr int RD_WAVES = MOEQ_RD_WAVES;
 constexpr int RD_THREADS = 64 * RD_WAVES;
 constexpr int RD_NTMAX = RD_T / 32;   // token tiles of 32 per workgroup tile
-constexpr int RD_RT = RD_T >= 128 ? 1 : 2;  // row tiles of 32 per wave
+#ifndef MOEQ_RD_RT
+#define MOEQ_RD_RT (RD_T >= 128 && RD_WAVES == 8 ? 1 : 2)
+#endif
+constexpr int RD_RT = MOEQ_RD_RT;  // row tiles of 32 per wave
 constexpr int RD_WROWS = 32 * RD_RT;  // weight rows per wave
 constexpr int RD_ROWS = RD_WAVES * RD_WROWS;  // weight rows per workgroup
 constexpr int RD_SUB = RD_T * 256;    // bytes of one activation sub-stage
 constexpr int RD_NBUF = 4;            // activation sub-stages resident in LDS
 constexpr int RD_APT = RD_SUB / 16 / RD_THREADS;  // 16-byte staging pieces per thread and sub-stage
-static_assert(RD_THREADS / 16 == 32, "staging piece j of a thread lies in token tile j");
+constexpr int RD_RPJ = RD_THREADS / 16;  // token rows per staging piece index
+static_assert(32 % RD_RPJ == 0, "the staging pieces of a token tile are whole");
+// staging pieces per thread for NT token tiles
+template <int NT>
+constexpr int rd_apt() { return NT * 32 / RD_RPJ; }
 constexpr size_t RD_LDS = (size_t)RD_NBUF * RD_SUB;
 static_assert(RD_WAVES * RD_WROWS == RD_ROWS, "the waves cover the workgroup's rows");
 static_assert(RD_LDS >= (size_t)(RD_WAVES / 2) * RD_RT * RD_NTMAX * 64 * 64,
@@ -884,7 +894,7 @@ __device__ __forceinline__ half8 rd_piece(const RdUnit<B>& u, const RdConsts& k)
 // The K loop of one wave.  ACT: the wave owns weight rows (else it only
 // stages activations, e.g. rows past the end of the tensor).  rc/rs: per row
 // tile, this lane's row chunk base and scale pairs; arow: the activation rows
-// this thread stages (row j * 32 + tid / 16 of the tile), as 16-byte pieces;
+// this thread stages (row j * RD_RPJ + tid / 16 of the tile), as 16-byte pieces;
 // su/sm: the unit and piece of the thread's staging slot; zero: 16 zeroed
 // bytes, 16-byte aligned (the scales of units past the row).
 //
@@ -918,11 +928,11 @@ __device__ __forceinline__ void rd_kloop(const MOEQ_GLOBAL u32x4* const (&rc)[RD
     const int unit = min(4 * (s >> 2) + su, Uk - 1);
     const int off = unit * 16 + 4 * (s & 3) + sm;
 #pragma unroll
-    for (int j = 0; j < NT; ++j) v[j] = arow[j][off];
+    for (int j = 0; j < rd_apt<NT>(); ++j) v[j] = arow[j][off];
   };
   auto astore = [&](const u32x4 (&v)[RD_APT], int buf) {
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
+    for (int j = 0; j < rd_apt<NT>(); ++j)
       *reinterpret_cast<u32x4*>(wdst + buf * RD_SUB + j * (RD_THREADS * 16)) = v[j];
   };
   // chunk j / scale half h of this lane's two units in stage V, every row
@@ -1147,13 +1157,13 @@ __device__ void rd_gateup_tile(const GemmArgs& a, const SlotInfo& sl, int m0, in
     rc[r] = gptr(reinterpret_cast<const u32x4*>(t.codes + (size_t)row * bits * Uk * 4));
     rs[r] = gptr(reinterpret_cast<const u32x2*>(t.scales + (size_t)row * (H / kBlock)));
   }
-  // staging slots of this thread: rows j * 32 + tid / 16 (token tile j < NT),
-  // piece (tid % 16) ^ (row % 16)
+  // staging slots of this thread: rows j * RD_RPJ + tid / 16 (the NT token
+  // tiles multiplied), piece (tid % 16) ^ (row % 16)
   const MOEQ_GLOBAL int32_t* perm = gptr(a.perm);
   const MOEQ_GLOBAL u32x4* arow[RD_APT] = {};
 #pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    int ar = j * (RD_THREADS / 16) + (tid >> 4);
+  for (int j = 0; j < rd_apt<NT>(); ++j) {
+    int ar = j * RD_RPJ + (tid >> 4);
     ar = ar < Mt ? ar : 0;
     const int tok = sl.shared >= 0 ? m0 + ar : perm[sl.base + m0 + ar] / a.k;
     arow[j] = gptr(reinterpret_cast<const u32x4*>(a.x16 + (size_t)tok * H));
@@ -1233,8 +1243,8 @@ __device__ void rd_down_tile(const GemmArgs& a, const SlotInfo& sl, int m0, int 
   }
   const MOEQ_GLOBAL u32x4* arow[RD_APT] = {};
 #pragma unroll
-  for (int j = 0; j < NT; ++j) {
-    int ar = j * (RD_THREADS / 16) + (tid >> 4);
+  for (int j = 0; j < rd_apt<NT>(); ++j) {
+    int ar = j * RD_RPJ + (tid >> 4);
     ar = ar < Mt ? ar : 0;
     arow[j] = gptr(reinterpret_cast<const u32x4*>(a.h16 + (size_t)(sl.base + m0 + ar) * I));
   }
