@@ -58,70 +58,120 @@ constexpr int kRdDeal = MOEQ_RD_DEAL;  // register-decoded tiles dealt to an XCD
 // the h rows.
 __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
   constexpr int kCls = kRdTile / 32;  // remainder classes by 32-row steps
-  __shared__ int32_t cnt[kMaxShared + kMaxExperts + 1];
-  __shared__ int32_t off[kMaxShared + kMaxExperts + 2];
-  __shared__ int32_t full[kMaxShared + kMaxExperts + 1];  // full register-decoded tiles of the slot
-  __shared__ int32_t foff[kMaxShared + kMaxExperts + 1];  // sorted index of the first one
-  __shared__ int32_t rpos[kMaxShared + kMaxExperts + 1];  // remainder rows, then its sorted index or -1
-  __shared__ int32_t soff[kMaxShared + kMaxExperts + 1];  // the slot's first tile in slot order
-  __shared__ int32_t run_len;
-  const int tid = threadIdx.x;
+  // per-slot counts scanned over the slots: LDS-decoded tiles, full
+  // register-decoded tiles, register-decoded tiles, remainders of each class
+  constexpr int NF = 3 + kCls;
+  constexpr int kSlots = kMaxShared + kMaxExperts;
+  static_assert(kSlots <= 2 * 1024, "two slots per thread");
+  __shared__ int32_t off[kSlots];   // first LDS-decoded tile of the slot
+  __shared__ int32_t foff[kSlots];  // sorted index of its first full register-decoded tile
+  __shared__ int32_t soff[kSlots];  // its first register-decoded tile in slot order
+  __shared__ int32_t rpos[kSlots];  // sorted index of its remainder tile, or -1
+  __shared__ int32_t nfull[kSlots];
+  __shared__ int32_t ncnt[kSlots];
+  __shared__ int32_t wsum[16][NF];
+  __shared__ int32_t total[NF];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nslots = a.S + a.active[0];
-  for (int s = tid; s < nslots; s += 1024) {
-    int M;
-    if (s < a.S) {
-      M = a.n;
-    } else {
-      const int e = a.active[1 + s - a.S];
-      M = a.offsets[e + 1] - a.offsets[e];
-    }
-    cnt[s] = (M + BM - 1) / BM;
-    full[s] = M / kRdTile;
-    rpos[s] = M % kRdTile;
-  }
   for (int t = tid; t < a.max_rtiles; t += 1024) a.tiles_rd[1 + 2 * t] = -1;
   // rows of h whose running maxima the gate/up epilogue accumulates
   const int rows = a.n * (a.k + a.S);
   for (int r = tid; r < rows; r += 1024) a.rowmax[r] = 0u;
+
+  // thread tid holds slots 2 tid and 2 tid + 1
+  int val[2][NF], cls[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int sl = 2 * tid + h;
+    int M = 0;
+    if (sl < a.S) {
+      M = a.n;
+    } else if (sl < nslots) {
+      const int e = a.active[1 + sl - a.S];
+      M = a.offsets[e + 1] - a.offsets[e];
+    }
+    const int rem = M % kRdTile;
+    cls[h] = (rem + 31) / 32;
+    val[h][0] = (M + BM - 1) / BM;
+    val[h][1] = M / kRdTile;
+    val[h][2] = M / kRdTile + (rem ? 1 : 0);
+#pragma unroll
+    for (int c = 1; c <= kCls; ++c) val[h][2 + c] = cls[h] == c ? 1 : 0;
+  }
+  // exclusive prefix sums over the slots: within the wave by shuffles, then
+  // over the 16 wave totals
+  int ps[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) ps[f] = val[0][f] + val[1][f];
+#pragma unroll
+  for (int d = 1; d < 64; d *= 2)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      const int t = __shfl_up(ps[f], d, 64);
+      if (lane >= d) ps[f] += t;
+    }
+  if (lane == 63)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) wsum[wave][f] = ps[f];
   __syncthreads();
   if (tid == 0) {
-    int run = 0, F = 0, so = 0;
-    int ncls[kCls + 1] = {};
-    for (int s = 0; s < nslots; ++s) {
-      off[s] = run;
-      run += cnt[s];
-      foff[s] = F;
-      F += full[s];
-      soff[s] = so;
-      so += full[s] + (rpos[s] ? 1 : 0);
-      if (rpos[s]) ++ncls[(rpos[s] + 31) / 32];
+    for (int f = 0; f < NF; ++f) {
+      int run = 0;
+      for (int w = 0; w < 16; ++w) {
+        const int v = wsum[w][f];
+        wsum[w][f] = run;
+        run += v;
+      }
+      total[f] = run;
     }
-    a.tiles_all[0] = min(run, a.max_mtiles);
-    int base[kCls + 1];
-    int T = F;
-    for (int c = kCls; c >= 1; --c) {
-      base[c] = T;
-      T += ncls[c];
+  }
+  __syncthreads();
+  int ex[NF];
+#pragma unroll
+  for (int f = 0; f < NF; ++f) ex[f] = ps[f] - val[0][f] - val[1][f] + wsum[wave][f];
+  // sorted order: full tiles in slot order, then the remainders by class,
+  // largest first, in slot order within a class
+  int base[kCls + 1];
+  base[kCls] = total[1];
+#pragma unroll
+  for (int c = kCls; c > 1; --c) base[c - 1] = base[c] + total[2 + c];
+  const int T = base[1] + total[3];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int sl = 2 * tid + h;
+    if (sl < nslots) {
+      off[sl] = ex[0];
+      foff[sl] = ex[1];
+      soff[sl] = ex[2];
+      int r = -1;
+#pragma unroll
+      for (int c = 1; c <= kCls; ++c)
+        if (cls[h] == c) r = base[c] + ex[2 + c];
+      rpos[sl] = r;
+      ncnt[sl] = val[h][0];
+      nfull[sl] = val[h][1];
     }
-    for (int s = 0; s < nslots; ++s) rpos[s] = rpos[s] ? base[(rpos[s] + 31) / 32]++ : -1;
-    int B = kRdDeal ? kRdDeal * ((T + kRdDeal * kXcds - 1) / (kRdDeal * kXcds)) : (T + kXcds - 1) / kXcds;
-    B = min(B, a.max_rtiles / kXcds);
-    run_len = B;
+#pragma unroll
+    for (int f = 0; f < NF; ++f) ex[f] += val[h][f];
+  }
+  int B = kRdDeal ? kRdDeal * ((T + kRdDeal * kXcds - 1) / (kRdDeal * kXcds)) : (T + kXcds - 1) / kXcds;
+  B = min(B, a.max_rtiles / kXcds);
+  if (tid == 0) {
+    a.tiles_all[0] = min(total[0], a.max_mtiles);
     a.tiles_rd[0] = B;
   }
   __syncthreads();
-  const int B = run_len;
   for (int s = tid; s < nslots; s += 1024) {
-    for (int i = 0; i < cnt[s]; ++i) {
+    for (int i = 0; i < ncnt[s]; ++i) {
       const int t = off[s] + i;
       if (t < a.max_mtiles) {
         a.tiles_all[1 + 2 * t] = s;
         a.tiles_all[2 + 2 * t] = i * BM;
       }
     }
-    for (int i = 0; i <= full[s]; ++i) {
+    for (int i = 0; i <= nfull[s]; ++i) {
       int si;  // sorted index
-      if (i < full[s])
+      if (i < nfull[s])
         si = foff[s] + i;
       else if (rpos[s] >= 0)
         si = rpos[s];
