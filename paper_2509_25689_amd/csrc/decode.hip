@@ -505,8 +505,11 @@ __global__ __launch_bounds__(256, TM == 1 ? kDownMinBlocks : 2) void down_kernel
 
 // ---------------------------------------------------------------------------
 // One token: down x routing weight and the combine in one pass, for layers
-// whose down tensors all have one width BD and at most 16 units per row.  A
-// workgroup of NT threads owns NT / 16 rows of y across every slot (the
+// whose down tensors are 2-4 bits wide with at most 16 units per row: one
+// width BD, or (BD = 0) widths that differ between tensors, where every
+// unit is fetched as four chunk loads, those past the slot's width from 16
+// zero bytes that stay in the vector cache, and the slot's width picks the
+// decoder.  A workgroup of NT threads owns NT / 16 rows of y across every slot (the
 // token's k choices in choice order, then the shared experts): a group of 16
 // lanes owns one row, lane u unit u of that row in every slot, with D slots'
 // codes in flight.  The lane accumulates w_j * (its partial dot of slot j) in
@@ -519,7 +522,22 @@ struct DownSlot {
   const uint16_t* scales;
   float w;
   int hrow;
+  int bits;
 };
+
+// w_j-free partial dot of one slot's unit: sum over its 4 blocks
+template <int B>
+__device__ __forceinline__ float down1_unit_dot(const uint32_t* w, u32x2 sc, const uint32_t* xu,
+                                                const float2* su4) {
+  float o = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t pr[16];
+    block_pairs_sub<B>(w + q * B, pr);
+    o = block_dot_sub<B>(pr, xu + 16 * q, block_scale_sub(sc, q), su4[q], o);
+  }
+  return o;
+}
 
 constexpr int kDown1Batch = 6;  // staged 32-byte pieces per thread per round trip
 
@@ -542,12 +560,14 @@ __global__ __launch_bounds__(NT) void down1_kernel(DecodeArgs a) {
       v.scales = t.scales;
       v.w = a.w[j];
       v.hrow = a.offsets[e];
+      v.bits = t.bits;
     } else {
       const TensorDev t = a.desc[(a.E + (j - k)) * 3 + 2];
       v.codes = t.codes;
       v.scales = t.scales;
       v.w = 1.0f;
       v.hrow = k + (j - k);
+      v.bits = t.bits;
     }
     slots[j] = v;
   }
@@ -556,12 +576,28 @@ __global__ __launch_bounds__(NT) void down1_kernel(DecodeArgs a) {
   const int u = threadIdx.x & 15;
   const int row = blockIdx.x * (NT / 16) + (threadIdx.x >> 4);
   const int rowc = min(row, H - 1), uc = min(u, U - 1);
-  auto load_slot = [&](DownRows<BD>& b, int j) {
+  constexpr int BL = BD == 0 ? 4 : BD;  // chunks loaded per unit
+  auto load_slot = [&](DownRows<BL>& b, int j) {
     const DownSlot& sl = slots[min(j, NS - 1)];
-    load_unit<BD>(sl.codes + (size_t)rowc * BD * U * 4, U, uc, b.w);
+    if constexpr (BD == 0) {
+      const int bits = sl.bits;
+      const MOEQ_GLOBAL u32x4* r4 =
+          gptr(reinterpret_cast<const u32x4*>(sl.codes + (size_t)rowc * bits * U * 4)) + uc;
+      const MOEQ_GLOBAL u32x4* z4 = gptr(reinterpret_cast<const u32x4*>(a.zeros));
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const u32x4 v = __builtin_nontemporal_load(c < bits ? r4 + (size_t)c * U : z4);
+        b.w[4 * c + 0] = v.x;
+        b.w[4 * c + 1] = v.y;
+        b.w[4 * c + 2] = v.z;
+        b.w[4 * c + 3] = v.w;
+      }
+    } else {
+      load_unit<BD>(sl.codes + (size_t)rowc * BD * U * 4, U, uc, b.w);
+    }
     b.s = *gptr(reinterpret_cast<const u32x2*>(sl.scales + (size_t)rowc * (I / kBlock) + 4 * uc));
   };
-  DownRows<BD> buf[D];
+  DownRows<BL> buf[D];
 #pragma unroll
   for (int i = 0; i < D - 1; ++i) load_slot(buf[i], i);
 
@@ -609,12 +645,15 @@ __global__ __launch_bounds__(NT) void down1_kernel(DecodeArgs a) {
       if (j < NS) {
         // slot j + D - 1 goes out before slot j is reduced
         load_slot(buf[(b + D - 1) % D], j + D - 1);
-        float o = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint32_t pr[16];
-          block_pairs_sub<BD>(buf[b].w + q * BD, pr);
-          o = block_dot_sub<BD>(pr, xu + j * xts + 16 * q, block_scale_sub(buf[b].s, q), su4[j * sts + q], o);
+        float o;
+        if constexpr (BD == 0) {
+          switch (__builtin_amdgcn_readfirstlane(slots[j].bits)) {
+            case 2: o = down1_unit_dot<2>(buf[b].w, buf[b].s, xu + j * xts, su4 + j * sts); break;
+            case 3: o = down1_unit_dot<3>(buf[b].w, buf[b].s, xu + j * xts, su4 + j * sts); break;
+            default: o = down1_unit_dot<4>(buf[b].w, buf[b].s, xu + j * xts, su4 + j * sts); break;
+          }
+        } else {
+          o = down1_unit_dot<BD>(buf[b].w, buf[b].s, xu + j * xts, su4 + j * sts);
         }
         acc = fmaf(slots[j].w, u < U ? o : 0.0f, acc);
       }
@@ -1182,13 +1221,14 @@ hipError_t launch_down1_b(const DecodeArgs& a, hipStream_t s) {
 }  // namespace
 
 bool down_combines(const DecodeArgs& a) {
-  return a.n == 1 && a.wide_down == 0 && a.down_bits >= 2 && a.down_bits <= 4 && a.I / kUnit <= 16 &&
+  return a.n == 1 && a.wide_down == 0 && a.down_bits <= 4 && a.I / kUnit <= 16 &&
          down1_lds(a) <= 65536;
 }
 
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s) {
   if (down_combines(a)) {
     switch (a.down_bits) {
+      case 0: return launch_down1_b<0>(a, s);  // widths differ between tensors
       case 2: return launch_down1_b<2>(a, s);
       case 3: return launch_down1_b<3>(a, s);
       default: return launch_down1_b<4>(a, s);

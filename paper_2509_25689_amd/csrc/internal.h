@@ -149,7 +149,7 @@ hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 // s2 after the routing and joins it back into s)
 hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2);
-// down x routing weight; for one token with one down width (down_combines)
+// down x routing weight; for one token with 2-4-bit down tensors (down_combines)
 // it also sums the slots into y, and the combine is not launched
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
 bool down_combines(const DecodeArgs& a);
