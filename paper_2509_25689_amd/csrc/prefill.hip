@@ -13,16 +13,19 @@
 // prescale) enter binary16 matrix instructions with float32 accumulation.
 //
 // 2-4-bit tensors whose block scales are positive, finite and within the
-// register decoder's bound (every tensor of the workloads measured here) take
-// the register-decoded GEMMs below (v_mfma_f32_32x32x16_f16, tiles of up to
-// 128 tokens): the packed weights are decoded in registers straight into the
-// matrix operand.  Every other tensor (5, 6 or 8 bits, or scales outside the
-// bound) takes the LDS-decoded GEMMs (gateup_gemm8_kernel, down_gemm8_kernel,
-// v_mfma_f32_16x16x32_f16): 128 tokens x 128 weight rows per workgroup, the
-// weight tile of each K step decoded once into LDS.  Workgroups are mapped to
-// tiles from the tile count on the device: each XCD takes an equal run of
-// consecutive tiles (one expert's tiles share its L2), whatever the
-// worst-case size of the grid.
+// register decoder's bound, with rows of an even number of 128-weight units
+// (every tensor of the workloads measured here), take the register-decoded
+// GEMMs below (v_mfma_f32_32x32x16_f16, tiles of up to 128 tokens): the
+// packed weights are decoded in registers straight into the matrix operand.
+// Every other tensor (5, 6 or 8 bits, scales outside the bound, or an odd
+// unit count) takes the LDS-decoded GEMMs (gateup_gemm8_kernel,
+// down_gemm8_kernel, v_mfma_f32_16x16x32_f16): 128 tokens x 128 weight rows
+// per workgroup, the weight tile of each K step decoded once into LDS.
+// Workgroups are mapped to tiles from counts the device wrote, whatever the
+// worst-case size of the grid: each XCD takes an equal run of list
+// positions, the LDS-decoded tiles in slot order (one expert's tiles share
+// its L2), the register-decoded ones sorted by work and dealt to the XCDs
+// in turn (equal work per XCD).
 #include <atomic>
 
 #include "internal.h"
