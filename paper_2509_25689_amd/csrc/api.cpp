@@ -567,7 +567,10 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
       e = launch_router_gate(a.x, L->router_w, n, a.H, a.E, L->gate_logits, s);
     logits = L->gate_logits;
   }
-  if (e == hipSuccess) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
+  // one token: the gate/up workgroups route the token themselves
+  const RouterParams rp1 = router_params(L, logits);
+  const bool self_routed = !prefill && n == 1 && gateup1_routes(rp1);
+  if (e == hipSuccess && !self_routed) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
   mark(1);
   if (e == hipSuccess) {
     if (prefill) {
@@ -581,6 +584,8 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
       if (e == hipSuccess) e = hipEventRecord(L->join_ev, L->aux);
       if (e == hipSuccess) e = launch_gateup_decode_single(a, s);
       if (e == hipSuccess) e = hipStreamWaitEvent(s, L->join_ev, 0);
+    } else if (self_routed) {
+      e = launch_gateup_decode_routing(a, rp1, L->ws, s);
     } else {
       e = launch_gateup_decode(a, s);
     }

@@ -34,6 +34,7 @@
 // combine kernel: y_t = sum_j partial(t, j) (j in slot order) + shared.
 #include "internal.h"
 #include "layout.h"
+#include "route_wave.h"
 
 namespace moeq {
 
@@ -773,7 +774,9 @@ __device__ __forceinline__ float row_half_dot(const TensorDev& t, int row, int U
 // pieces, 4 per block)
 __device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uint32_t* xl, float2* xs) {
   const int H = a.H;
-  const int t = sl.shared >= 0 ? 0 : a.perm[sl.base] / a.k;
+  // (one token: token 0, without reading the bucket permutation, which the
+  // routing workgroup of gateup1_route_kernel may still be writing)
+  const int t = sl.shared >= 0 || a.n == 1 ? 0 : a.perm[sl.base] / a.k;
   const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
   for (int q = threadIdx.x; q < H / 8; q += 256) {
     float f[8];
@@ -821,10 +824,8 @@ __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl,
   if ((lane & 15) == 15 && row < I) a.h[(size_t)sl.base * a.I + row] = silu(other) * v;
 }
 
-// grid = (I / 16, S + max_active), 256 threads; the buckets of one token
-__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
-  extern __shared__ uint32_t smem[];
-  const Slot sl = slot_info(a, blockIdx.y);
+// one workgroup's share of the gate/up of a bucket of one token
+__device__ __forceinline__ void gateup1_slot(const DecodeArgs& a, const Slot& sl, uint32_t* smem) {
   if (sl.M != 1) return;  // the buckets of one token, of any batch
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
@@ -843,6 +844,70 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
     case 4 * 8 + 4: gateup1_body<4, 4>(a, sl, tg, tu, xl, xs); break;
     default: break;
   }
+}
+
+// grid = (I / 16, S + max_active), 256 threads; the buckets of one token
+__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  gateup1_slot(a, slot_info(a, blockIdx.y), smem);
+}
+
+// The same for a forward of one token that needs no routing launch: wave 0
+// of every workgroup of a routed slot routes the token itself (the routing
+// kernels' selection, deterministic, so every workgroup finds the same
+// experts) while the shared experts' workgroups start at once.  Routed slot
+// i is the i-th chosen expert in ascending id order, as the bucketing lists
+// them.  Workgroup (0, S) also writes what the routing launch would have:
+// idx and w in choice order, offsets, the active list and the permutation,
+// which the down kernel and any 5/6/8-bit gate/up kernel read after this
+// launch.  grid = (I / 16, S + k), 256 threads.
+template <int EPL>
+__global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_route_kernel(DecodeArgs a, RouterParams rp,
+                                                                                Workspace ws) {
+  extern __shared__ uint32_t smem[];
+  __shared__ float gs_l[64];
+  __shared__ int32_t chosen[kMaxTopK];
+  Slot sl;
+  if ((int)blockIdx.y < a.S) {
+    sl = slot_info(a, blockIdx.y);
+  } else {
+    if (threadIdx.x < 64) {
+      // (slots past the choices, which the creation checks rule out, read
+      // expert 0's descriptor: in range, skipped if it holds no tensor)
+      if (threadIdx.x < kMaxTopK) chosen[threadIdx.x] = 0;
+      const bool out = blockIdx.x == 0 && (int)blockIdx.y == a.S;
+      const LaneChoice<EPL> ch =
+          route_token_wave<EPL>(rp, 0, gs_l, out ? ws.idx : nullptr, out ? ws.w : nullptr, nullptr);
+      const int lane = threadIdx.x, E = rp.E_row;
+      const int cnt = __popc(ch.bits);
+      const int below = wave_incl_sum(cnt) - cnt;  // chosen ids of the lanes below
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        const int e = lane * EPL + i;
+        const int r = below + __popc(ch.bits & ((1u << i) - 1u));
+        const bool c = (ch.bits >> i) & 1u;
+        if (c) chosen[r] = e;
+        if (out) {
+          if (e < E) ws.offsets[e] = r;
+          if (c) {
+            ws.active[1 + r] = e;
+            ws.perm[r] = ch.order[i];
+          }
+        }
+      }
+      if (out && lane == 0) {
+        ws.offsets[E] = rp.k;
+        ws.active[0] = rp.k;
+      }
+    }
+    __syncthreads();
+    const int i = blockIdx.y - a.S;
+    sl.desc = chosen[i];
+    sl.base = i;
+    sl.M = 1;
+    sl.shared = -1;
+  }
+  gateup1_slot(a, sl, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -1191,6 +1256,23 @@ hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2) { return launch_gateup_tm<4>(a, s2); }
+
+bool gateup1_routes(const RouterParams& rp) { return !rp.kept_ids && !rp.x && rp.E_row <= 256 && rp.k <= kMaxTopK; }
+
+hipError_t launch_gateup_decode_routing(const DecodeArgs& a, const RouterParams& rp, const Workspace& ws,
+                                        hipStream_t s) {
+  const int U = a.H / kUnit;
+  const size_t lds = (size_t)(U * kXStride + U * 8) * 4;
+  dim3 grid((a.I + 15) / 16, a.S + rp.k);
+  if (rp.E_row <= 64)
+    gateup1_route_kernel<1><<<grid, 256, lds, s>>>(a, rp, ws);
+  else if (rp.E_row <= 128)
+    gateup1_route_kernel<2><<<grid, 256, lds, s>>>(a, rp, ws);
+  else
+    gateup1_route_kernel<4><<<grid, 256, lds, s>>>(a, rp, ws);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? launch_wide_gateup(a, s) : e;
+}
 
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s) {
   hipError_t e = launch_gateup_decode_single(a, s);

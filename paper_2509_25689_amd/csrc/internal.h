@@ -149,6 +149,12 @@ hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 // s2 after the routing and joins it back into s)
 hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s);
 hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2);
+// One token without a routing launch: the gate/up workgroups route the
+// token themselves and one of them writes the routing and bucket outputs
+// (gateup1_routes: the mask-based router with at most 256 experts)
+bool gateup1_routes(const RouterParams& rp);
+hipError_t launch_gateup_decode_routing(const DecodeArgs& a, const RouterParams& rp, const Workspace& ws,
+                                        hipStream_t s);
 // down x routing weight; for one token with 2-4-bit down tensors (down_combines)
 // it also sums the slots into y, and the combine is not launched
 hipError_t launch_down_decode(const DecodeArgs& a, hipStream_t s);
