@@ -786,9 +786,22 @@ __device__ __forceinline__ void stage_x1(const DecodeArgs& a, const Slot sl, uin
   }
 }
 
+// token 0's x staged by threads [t0, t0 + nt) of the workgroup (nt a multiple
+// of 64, t0 of 64: the four pieces of a block stay in four lanes of a wave)
+__device__ __forceinline__ void stage_x1_token0(const DecodeArgs& a, int t0, int nt, uint32_t* xl, float2* xs) {
+  const int H = a.H;
+  const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x));
+  for (int q = (int)threadIdx.x - t0; q < H / 8; q += nt) {
+    float f[8];
+    bf16x8_to_f32(src[q], f);
+    const int uu = q >> 4, cq = q & 15;
+    stage_piece(f, xl + uu * kXStride + cq * 4, xs + uu * 4 + (cq >> 2), (cq & 3) == 0);
+  }
+}
+
 // Each lane requests its first unit before x is staged, so the staging
-// latency overlaps the weight traffic.
-template <int BG, int BU>
+// latency overlaps the weight traffic (STAGED: x is in LDS already).
+template <int BG, int BU, bool STAGED = false>
 __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
                                              const TensorDev& tu, uint32_t* xl, float2* xs) {
   const int H = a.H, I = a.I, U = H / kUnit;
@@ -802,8 +815,10 @@ __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl,
     const TensorDev& t = up ? tu : tg;
     UnitBuf<BG> first;
     load_unit_buf<BG>(first, t, rowc, U, min(j, U - 1), H);
-    stage_x1(a, sl, xl, xs);
-    __syncthreads();
+    if constexpr (!STAGED) {
+      stage_x1(a, sl, xl, xs);
+      __syncthreads();
+    }
     v = row_half_dot<BG>(t, rowc, U, j, H, xl, xs, first);
   } else {
     UnitBuf<BG> fg;
@@ -812,8 +827,10 @@ __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl,
       load_unit_buf<BU>(fu, tu, rowc, U, min(j, U - 1), H);
     else
       load_unit_buf<BG>(fg, tg, rowc, U, min(j, U - 1), H);
-    stage_x1(a, sl, xl, xs);
-    __syncthreads();
+    if constexpr (!STAGED) {
+      stage_x1(a, sl, xl, xs);
+      __syncthreads();
+    }
     if (up)
       v = row_half_dot<BU>(tu, rowc, U, j, H, xl, xs, fu);
     else
@@ -825,6 +842,7 @@ __device__ __forceinline__ void gateup1_body(const DecodeArgs& a, const Slot sl,
 }
 
 // one workgroup's share of the gate/up of a bucket of one token
+template <bool STAGED = false>
 __device__ __forceinline__ void gateup1_slot(const DecodeArgs& a, const Slot& sl, uint32_t* smem) {
   if (sl.M != 1) return;  // the buckets of one token, of any batch
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
@@ -833,15 +851,15 @@ __device__ __forceinline__ void gateup1_slot(const DecodeArgs& a, const Slot& sl
   uint32_t* xl = smem;
   float2* xs = reinterpret_cast<float2*>(smem + U * kXStride);
   switch (tg.bits * 8 + tu.bits) {
-    case 2 * 8 + 2: gateup1_body<2, 2>(a, sl, tg, tu, xl, xs); break;
-    case 2 * 8 + 3: gateup1_body<2, 3>(a, sl, tg, tu, xl, xs); break;
-    case 2 * 8 + 4: gateup1_body<2, 4>(a, sl, tg, tu, xl, xs); break;
-    case 3 * 8 + 2: gateup1_body<3, 2>(a, sl, tg, tu, xl, xs); break;
-    case 3 * 8 + 3: gateup1_body<3, 3>(a, sl, tg, tu, xl, xs); break;
-    case 3 * 8 + 4: gateup1_body<3, 4>(a, sl, tg, tu, xl, xs); break;
-    case 4 * 8 + 2: gateup1_body<4, 2>(a, sl, tg, tu, xl, xs); break;
-    case 4 * 8 + 3: gateup1_body<4, 3>(a, sl, tg, tu, xl, xs); break;
-    case 4 * 8 + 4: gateup1_body<4, 4>(a, sl, tg, tu, xl, xs); break;
+    case 2 * 8 + 2: gateup1_body<2, 2, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 2 * 8 + 3: gateup1_body<2, 3, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 2 * 8 + 4: gateup1_body<2, 4, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 2: gateup1_body<3, 2, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 3: gateup1_body<3, 3, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 3 * 8 + 4: gateup1_body<3, 4, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 2: gateup1_body<4, 2, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 3: gateup1_body<4, 3, STAGED>(a, sl, tg, tu, xl, xs); break;
+    case 4 * 8 + 4: gateup1_body<4, 4, STAGED>(a, sl, tg, tu, xl, xs); break;
     default: break;
   }
 }
@@ -855,7 +873,8 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_kernel(Decode
 // The same for a forward of one token that needs no routing launch: wave 0
 // of every workgroup of a routed slot routes the token itself (the routing
 // kernels' selection, deterministic, so every workgroup finds the same
-// experts) while the shared experts' workgroups start at once.  Routed slot
+// experts; waves 1-3 stage x meanwhile) while the shared experts'
+// workgroups start at once.  Routed slot
 // i is the i-th chosen expert in ascending id order, as the bucketing lists
 // them.  Workgroup (0, S) also writes what the routing launch would have:
 // idx and w in choice order, offsets, the active list and the permutation,
@@ -899,6 +918,10 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_route_kernel(
         ws.offsets[E] = rp.k;
         ws.active[0] = rp.k;
       }
+    } else {
+      // waves 1-3 stage the token's x meanwhile
+      const int U = a.H / kUnit;
+      stage_x1_token0(a, 64, 192, smem, reinterpret_cast<float2*>(smem + U * kXStride));
     }
     __syncthreads();
     const int i = blockIdx.y - a.S;
@@ -906,6 +929,8 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_route_kernel(
     sl.base = i;
     sl.M = 1;
     sl.shared = -1;
+    gateup1_slot<true>(a, sl, smem);
+    return;
   }
   gateup1_slot(a, sl, smem);
 }
