@@ -37,14 +37,16 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 
 # HBM bytes per gate/up launch at batch 1 from rocprofv3 FETCH_SIZE + WRITE_SIZE,
 # each scaled by the same counter's reading for a plain 1 GiB copy (factors
-# 2.0 and 1.0; see profiles/gateup1_kernel_decode_b1_traffic.md).  Valid only for
-# the kernel sources the counters were taken on, identified by their sha256:
-# any change to them reports traffic as null until the counters are retaken.
+# 2.0 and 1.0; see profiles/gateup1_route_kernel_decode_b1_traffic.md).  Valid
+# only for the kernel sources the counters were taken on, identified by their
+# sha256: any change to them reports traffic as null until the counters are
+# retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 128062932,
+    "bytes": 127411908,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "deb96c2056e7006385e6e2fe0cea7752960ce4e70d662ca3514546f58aecbb51",
+        "paper_2509_25689_amd/csrc/decode.hip": "6fc04fcc88991ed20521b98a6c5f67cd90714c9c473af069a7be057f15ad5e7e",
         "paper_2509_25689_amd/csrc/layout.h": "dbc3980ea27988d4bf02afa1c0972c44e3b89fce29981c7bc725f8c626ae5203",
+        "paper_2509_25689_amd/csrc/route_wave.h": "eff5347672eb0ace6f0dd2e9f05a341eed9bc59da75252d4c7705b4ec5f8ee98",
     },
 }
 
@@ -598,7 +600,8 @@ def main():
                      "down": round(st[2] * 1e3, 2), "combine": round(st[3] * 1e3, 2)},
         "down_GBps": round(r["dn_GBps"], 1),
         "roofline": {"bound": "hbm",
-                     "kernel": ("gateup1_kernel" if B == 1 else "gateup_kernel") + " (fused dequant-GEMV gate/up + SwiGLU)",
+                     "kernel": ("gateup1_route_kernel (routing + fused dequant-GEMV gate/up + SwiGLU)" if B == 1
+                                else "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)"),
                      "achieved": round(r["gu_GBps"], 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": gateup_traffic() if B == 1 else None,
                      "bytes_per_launch": int(r["gu_launch_bytes"])},
