@@ -598,6 +598,9 @@ def main():
         "bytes_per_step": int(r["bytes_per_step"]),
         "stage_us": {"route_bucket": round(st[0] * 1e3, 2), "gate_up": round(st[1] * 1e3, 2),
                      "down": round(st[2] * 1e3, 2), "combine": round(st[3] * 1e3, 2)},
+        "stage_note": ("eager forwards timed by events between the stages; at batch 1 the routing runs inside "
+                       "the gate/up kernel and the combine inside the down kernel, so those two stages hold no "
+                       "launch and show only the events' own cost"),
         "down_GBps": round(r["dn_GBps"], 1),
         "roofline": {"bound": "hbm",
                      "kernel": ("gateup1_route_kernel (routing + fused dequant-GEMV gate/up + SwiGLU)" if B == 1
