@@ -32,6 +32,10 @@ CASES = {
     "top12": dict(top_k=12, topk_group=4),
     "one_group": dict(n_group=1, topk_group=1),
     "biased": dict(),
+    # expert counts per router lane of 2 and 4 (the one-token forward routes
+    # inside the gate/up kernel up to 256 experts), 200 with groups of 25
+    "experts128": dict(n_experts=128, n_kept=96, n_group=8, topk_group=4, top_k=8),
+    "experts200": dict(n_experts=200, n_kept=150, n_group=8, topk_group=4, top_k=8),
     "experts512": dict(n_experts=512, n_kept=384, n_group=8, topk_group=4, top_k=8),
     "experts1024": dict(n_experts=1024, n_kept=768, n_group=8, topk_group=4, top_k=8),
 }
