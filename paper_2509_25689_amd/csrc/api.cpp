@@ -16,6 +16,15 @@
 
 #include "internal.h"
 
+// decode forwards of at least MOEQ_HYBRID_FROM tokens send the buckets of
+// more than MOEQ_HYBRID_ABOVE rows to the grouped GEMMs
+#ifndef MOEQ_HYBRID_FROM
+#define MOEQ_HYBRID_FROM 32
+#endif
+#ifndef MOEQ_HYBRID_ABOVE
+#define MOEQ_HYBRID_ABOVE 4
+#endif
+
 using namespace moeq;
 
 namespace {
@@ -557,6 +566,11 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   a.down_bits = L->down_bits;
   const bool prefill =
       L->path == MOEQ_PATH_PREFILL || (L->path == MOEQ_PATH_AUTO && n > L->decode_max);
+  // decode forwards of several tokens: the buckets of more than
+  // MOEQ_HYBRID_ABOVE rows (the large buckets of a skewed routing) take the
+  // grouped GEMMs, which read an expert's weights once for all its tokens
+  const bool hybrid = !prefill && n >= MOEQ_HYBRID_FROM;
+  a.gemm_above = prefill ? 0 : hybrid ? MOEQ_HYBRID_ABOVE : kDecodeMaxTokens;
   hipError_t e = hipSuccess;
   auto mark = [&](int i) {
     if (L->timing && e == hipSuccess) e = hipEventRecord(L->stage_events[i], s);
@@ -570,19 +584,21 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   // one token: the gate/up workgroups route the token themselves
   const RouterParams rp1 = router_params(L, logits);
   const bool self_routed = !prefill && n == 1 && gateup1_routes(rp1);
-  if (e == hipSuccess && !self_routed) e = route_and_bucket(L, logits, n, s, prefill ? x : nullptr);
+  if (e == hipSuccess && !self_routed) e = route_and_bucket(L, logits, n, s, prefill || hybrid ? x : nullptr);
   mark(1);
   if (e == hipSuccess) {
     if (prefill) {
       e = launch_prefill_tiles(a, s);
       if (e == hipSuccess) e = launch_gateup_prefill(a, s);
     } else if (n > 1) {
+      if (hybrid) e = launch_prefill_tiles(a, s);
       // fork: the buckets of 2-64 tokens on the layer's second stream, then join
       if (e == hipSuccess) e = hipEventRecord(L->fork_ev, s);
       if (e == hipSuccess) e = hipStreamWaitEvent(L->aux, L->fork_ev, 0);
       if (e == hipSuccess) e = launch_gateup_decode_multi(a, L->aux);
       if (e == hipSuccess) e = hipEventRecord(L->join_ev, L->aux);
       if (e == hipSuccess) e = launch_gateup_decode_single(a, s);
+      if (e == hipSuccess && hybrid) e = launch_gateup_prefill(a, s);
       if (e == hipSuccess) e = hipStreamWaitEvent(s, L->join_ev, 0);
     } else if (self_routed) {
       e = launch_gateup_decode_routing(a, rp1, L->ws, s);
@@ -592,6 +608,7 @@ moeq_status moeq_forward(moeq_layer* L, const void* x, const float* logits, int3
   }
   mark(2);
   if (e == hipSuccess) e = prefill ? launch_down_prefill(a, s) : launch_down_decode(a, s);
+  if (e == hipSuccess && hybrid) e = launch_down_prefill(a, s);
   mark(3);
   if (e == hipSuccess && (prefill || !down_combines(a))) e = launch_combine(a, s);
   mark(4);

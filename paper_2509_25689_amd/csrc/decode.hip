@@ -367,7 +367,7 @@ template <int LPR, int TM, int RW, int NBUF, int NW>
 __global__ __launch_bounds__(NW * 64, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
+  if (sl.M < 0 || sl.M > a.gemm_above) return;  // (large buckets: the grouped GEMMs)
   if (sl.M == 1) return;  // one-token buckets go to gateup1_kernel
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
@@ -493,7 +493,7 @@ template <int LPR, int TM, int RW, int NBUF>
 __global__ __launch_bounds__(256, TM == 1 ? kDownMinBlocks : 2) void down_kernel(DecodeArgs a) {
   extern __shared__ uint32_t smem[];
   const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
+  if (sl.M < 0 || sl.M > a.gemm_above) return;  // (large buckets: the grouped GEMMs)
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes) return;
   switch (td.bits) {
@@ -1057,7 +1057,7 @@ __device__ __forceinline__ float wide_sum(float v) {
 template <int TM, int LPR>
 __global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
   const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
+  if (sl.M < 0 || sl.M > a.gemm_above) return;  // (large buckets: the grouped GEMMs)
   const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
   if (!tg.codes || !tu.codes) return;
   if (!wide_bits(tg.bits) && !wide_bits(tu.bits)) return;
@@ -1104,7 +1104,7 @@ __global__ __launch_bounds__(256) void wide_gateup_kernel(DecodeArgs a) {
 template <int TM, int LPR>
 __global__ __launch_bounds__(256) void wide_down_kernel(DecodeArgs a) {
   const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0) return;
+  if (sl.M < 0 || sl.M > a.gemm_above) return;  // (large buckets: the grouped GEMMs)
   const TensorDev td = a.desc[sl.desc * 3 + 2];
   if (!td.codes || !wide_bits(td.bits)) return;
   const int H = a.H, I = a.I, U = I / kUnit;

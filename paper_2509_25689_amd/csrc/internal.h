@@ -142,6 +142,10 @@ struct DecodeArgs {
   // many-token path: some kept or shared gate/up (down) tensor is wider than
   // 4 bits or off the register decoder, so the LDS-decoded GEMM runs too
   int32_t lds_gateup, lds_down;
+  // buckets of more rows take the grouped GEMMs (prefill path: 0, every
+  // bucket; decode path: the large buckets of a skewed routing), the others
+  // the dequant-GEMV kernels
+  int32_t gemm_above;
 };
 hipError_t launch_gateup_decode(const DecodeArgs& a, hipStream_t s);
 // the same work split over two streams: the one-token buckets (and the wide

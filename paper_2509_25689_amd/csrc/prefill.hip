@@ -93,6 +93,7 @@ __global__ __launch_bounds__(1024) void prefill_tiles_kernel(DecodeArgs a) {
       const int e = a.active[1 + sl - a.S];
       M = a.offsets[e + 1] - a.offsets[e];
     }
+    if (M <= a.gemm_above) M = 0;  // (small buckets of a decode forward: the GEMV kernels)
     const int rem = M % kRdTile;
     cls[h] = (rem + 31) / 32;
     val[h][0] = (M + BM - 1) / BM;
