@@ -42,9 +42,9 @@ MFMA_F16_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix peak of one MI355X
 # sha256: any change to them reports traffic as null until the counters are
 # retaken.
 GATEUP_TRAFFIC = {
-    "bytes": 127411908,
+    "bytes": 127328412,
     "sources": {
-        "paper_2509_25689_amd/csrc/decode.hip": "6fc04fcc88991ed20521b98a6c5f67cd90714c9c473af069a7be057f15ad5e7e",
+        "paper_2509_25689_amd/csrc/decode.hip": "d261ca65464c3bb7c0e754958fdafdd9a092c3deb7356cdb029970b4e926bf68",
         "paper_2509_25689_amd/csrc/layout.h": "dbc3980ea27988d4bf02afa1c0972c44e3b89fce29981c7bc725f8c626ae5203",
         "paper_2509_25689_amd/csrc/route_wave.h": "eff5347672eb0ace6f0dd2e9f05a341eed9bc59da75252d4c7705b4ec5f8ee98",
     },
