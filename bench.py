@@ -604,7 +604,7 @@ def main():
         "down_GBps": round(r["dn_GBps"], 1),
         "roofline": {"bound": "hbm",
                      "kernel": ("gateup1_route_kernel (routing + fused dequant-GEMV gate/up + SwiGLU)" if B == 1
-                                else "gateup_kernel (fused dequant-GEMV gate/up + SwiGLU)"),
+                                else "gateupn_kernel (fused dequant-GEMV gate/up + SwiGLU, 2 tokens per pass)"),
                      "achieved": round(r["gu_GBps"], 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(r["gu_GBps"] / HBM_PEAK_GBPS, 4), "traffic": gateup_traffic() if B == 1 else None,
                      "bytes_per_launch": int(r["gu_launch_bytes"])},

@@ -243,11 +243,11 @@ moeq_status moeq_dequant(moeq_layer* layer, int32_t expert, int32_t proj, float*
  * (each width's code unpacking of Section 3.3's per-tensor formats), so each
  * can be compared with the format's definition d * (c - 2^(b-1)).
  *   decoder  MOEQ_DECODER_EXACT: the bfloat16-form unpacking (the matrix-vector
- *            kernels for buckets of 2-64 tokens and for 5/6/8-bit tensors),
+ *            kernels for 5/6/8-bit tensors),
  *            out = float32 [rows x K], exact (this is moeq_dequant);
  *            MOEQ_DECODER_GEMV_SUBNORMAL: the binary16-subnormal code pairs
- *            (the one-token gate/up and the 2-4-bit down matrix-vector
- *            kernels), each code rebuilt from its pair value c * 2^(k-24),
+ *            (the 2-4-bit gate/up and down matrix-vector kernels), each code
+ *            rebuilt from its pair value c * 2^(k-24),
  *            out = float32 [rows x K], exact; widths 2-4 only (else
  *            UNSUPPORTED);
  *            MOEQ_DECODER_GEMM_F16: the grouped GEMMs' weight decoder, out =

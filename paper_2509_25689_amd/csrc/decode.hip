@@ -45,23 +45,14 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against LDS bank conflicts
 
-// Pipeline shape: each wave walks kGateUpSteps (kDownSteps) row steps with
-// kGateUpBuf (kDownBuf) register buffers, i.e. NBUF - 1 steps of codes in
-// flight while one is reduced; MinBlocks bounds registers for occupancy.
-#ifndef MOEQ_GATEUP_STEPS
-#define MOEQ_GATEUP_STEPS 8
-#endif
-#ifndef MOEQ_GATEUP_BUF
-#define MOEQ_GATEUP_BUF 2
-#endif
+// Pipeline shape of the down GEMV: each wave walks kDownSteps row steps with
+// kDownBuf register buffers, i.e. NBUF - 1 steps of codes in flight while
+// one is reduced; MinBlocks bounds registers for occupancy.
 #ifndef MOEQ_DOWN_STEPS
 #define MOEQ_DOWN_STEPS 4
 #endif
 #ifndef MOEQ_DOWN_BUF
 #define MOEQ_DOWN_BUF 1
-#endif
-#ifndef MOEQ_GATEUP_MINBLOCKS
-#define MOEQ_GATEUP_MINBLOCKS 4
 #endif
 #ifndef MOEQ_DOWN_MINBLOCKS
 #define MOEQ_DOWN_MINBLOCKS 4
@@ -73,13 +64,11 @@ constexpr int kXStride = 68;  // dwords per staged unit: 64 + 4 padding against 
 #ifndef MOEQ_DOWNM_BUF
 #define MOEQ_DOWNM_BUF 1
 #endif
-constexpr int kGateUpSteps = MOEQ_GATEUP_STEPS, kGateUpBuf = MOEQ_GATEUP_BUF;
-static_assert(MOEQ_GATEUP_STEPS % MOEQ_GATEUP_BUF == 0 && MOEQ_DOWN_STEPS % MOEQ_DOWN_BUF == 0,
-              "steps per wave must be a multiple of the pipeline depth");
+static_assert(MOEQ_DOWN_STEPS % MOEQ_DOWN_BUF == 0, "steps per wave must be a multiple of the pipeline depth");
 constexpr int kDownSteps = MOEQ_DOWN_STEPS, kDownBuf = MOEQ_DOWN_BUF;
 constexpr int kDownStepsM = MOEQ_DOWNM_STEPS, kDownBufM = MOEQ_DOWNM_BUF;
 static_assert(MOEQ_DOWNM_STEPS % MOEQ_DOWNM_BUF == 0, "steps per wave must be a multiple of the pipeline depth");
-constexpr int kGateUpMinBlocks = MOEQ_GATEUP_MINBLOCKS, kDownMinBlocks = MOEQ_DOWN_MINBLOCKS;
+constexpr int kDownMinBlocks = MOEQ_DOWN_MINBLOCKS;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
@@ -150,13 +139,6 @@ __device__ __forceinline__ float block_dot(const uint32_t (&p)[16], const uint32
     }
   }
   return fmaf(ds, fmaf(-192.0f, X, acc), acc_out);
-}
-
-// block q's scale (binary16, 4 per unit in sc) times 2^(b-7)
-template <int B>
-__device__ __forceinline__ float block_scale(u32x2 sc, int q) {
-  const uint32_t s16 = ((q < 2 ? sc.x : sc.y) >> (16 * (q & 1))) & 0xFFFFu;
-  return half_to_float(s16) * (1.0f / (float)(1 << (7 - B)));
 }
 
 // block q's scale (binary16, 4 per unit in sc) times 2^24, for subnormal pairs
@@ -247,143 +229,6 @@ __device__ __forceinline__ float group_sum(float v) {
 }
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + expf(-g)); }
-
-// ---------------------------------------------------------------------------
-// gate/up + SwiGLU for one (slot, row tile), gate/up widths BG/BU.  Each wave
-// owns RW consecutive row steps (GPW rows each) and walks them with two
-// register buffers: the codes of step i+1 are in flight while step i is
-// reduced, so every wave keeps HBM requests outstanding.
-template <int BG, int BU>
-struct GateUpRows {
-  uint32_t wg[4 * BG], wu[4 * BU];
-  u32x2 sg, su;
-};
-
-template <int BG, int BU>
-__device__ __forceinline__ void load_gateup(GateUpRows<BG, BU>& b, const TensorDev& tg, const TensorDev& tu,
-                                            int row, int U, int u, int H) {
-  load_unit<BG>(tg.codes + (size_t)row * BG * U * 4, U, u, b.wg);
-  load_unit<BU>(tu.codes + (size_t)row * BU * U * 4, U, u, b.wu);
-  b.sg = *gptr(reinterpret_cast<const u32x2*>(tg.scales + (size_t)row * (H / kBlock) + 4 * u));
-  b.su = *gptr(reinterpret_cast<const u32x2*>(tu.scales + (size_t)row * (H / kBlock) + 4 * u));
-}
-
-template <int BG, int BU, int LPR, int TM>
-__device__ __forceinline__ void compute_gateup(const GateUpRows<BG, BU>& b, bool active, const uint32_t* xu,
-                                               const float* su4, int xts, int sts, int mc, int u,
-                                               int hrow0, int row, const DecodeArgs& a) {
-  float g[TM], up[TM];
-#pragma unroll
-  for (int m = 0; m < TM; ++m) g[m] = up[m] = 0.0f;
-  if (active) {
-    const PairConsts pk = pair_consts();
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t p[16];
-      block_pairs<BG>(b.wg + q * BG, pk, p);
-      const float dg = block_scale<BG>(b.sg, q);
-#pragma unroll
-      for (int m = 0; m < TM; ++m)
-        if (m < mc) g[m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, dg, su4[m * sts + q], g[m]);
-      block_pairs<BU>(b.wu + q * BU, pk, p);
-      const float du = block_scale<BU>(b.su, q);
-#pragma unroll
-      for (int m = 0; m < TM; ++m)
-        if (m < mc) up[m] = block_dot<1>(p, xu + m * xts + 16 * q, 0, du, su4[m * sts + q], up[m]);
-    }
-  }
-#pragma unroll
-  for (int m = 0; m < TM; ++m) {
-    if (m < mc) {
-      const float gs = group_sum<LPR>(g[m]), us = group_sum<LPR>(up[m]);
-      if (u == LPR - 1) a.h[(size_t)(hrow0 + m) * a.I + row] = silu(gs) * us;
-    }
-  }
-}
-
-template <int BG, int BU, int LPR, int TM, int RW, int NBUF, int NW>
-__device__ __forceinline__ void gateup_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
-                                            const TensorDev& tu, uint32_t* smem) {
-  const int H = a.H, I = a.I, U = H / kUnit;
-  const int xts = U * kXStride, sts = U * 4;  // per-token LDS strides (dwords, floats)
-  uint32_t* xl = smem;
-  float* xs = reinterpret_cast<float*>(smem + TM * xts);
-
-  constexpr int GPW = 64 / LPR;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int grp = lane / LPR, u = lane % LPR;
-  const bool uok = u < U;
-  const int row0 = blockIdx.x * (NW * GPW * RW) + wave * (GPW * RW) + grp;  // + step * GPW
-
-  GateUpRows<BG, BU> buf[NBUF];
-  for (int m0 = 0; m0 < sl.M; m0 += TM) {
-    const int mc = min(TM, sl.M - m0);
-    asm volatile("" ::: "memory");  // weight loads stay inside the chunk loop
-    // the first NBUF row steps are requested before x is staged, so the
-    // staging latency overlaps the weight traffic
-#pragma unroll
-    for (int st = 0; st < NBUF; ++st)
-      if (st < RW && uok && row0 + st * GPW < I) load_gateup(buf[st], tg, tu, row0 + st * GPW, U, u, H);
-    __syncthreads();
-    // stage the chunk's x rows: 16-byte pieces, 4 per block of 32
-    for (int m = 0; m < mc; ++m) {
-      const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
-      const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
-      for (int q = threadIdx.x; q < H / 8; q += NW * 64) {
-        const u32x4 v = src[q];
-        float s = 0.0f;
-        s += bf16_lo(v.x); s += bf16_hi(v.x); s += bf16_lo(v.y); s += bf16_hi(v.y);
-        s += bf16_lo(v.z); s += bf16_hi(v.z); s += bf16_lo(v.w); s += bf16_hi(v.w);
-        s += __shfl_xor(s, 1, 64);
-        s += __shfl_xor(s, 2, 64);
-        const int uu = q >> 4, cq = q & 15;
-        *reinterpret_cast<u32x4*>(xl + m * xts + uu * kXStride + cq * 4) = v;
-        if ((cq & 3) == 0) xs[m * sts + uu * 4 + (cq >> 2)] = s;
-      }
-    }
-    __syncthreads();
-    const uint32_t* xu = xl + u * kXStride;
-    const float* su4 = xs + u * 4;
-    // groups of NBUF steps: buffer indices are static inside a group; step st
-    // is reduced from buffer st % NBUF, which then takes step st + NBUF
-#pragma unroll 1
-    for (int g0 = 0; g0 < RW; g0 += NBUF) {
-      asm volatile("" ::: "memory");
-#pragma unroll
-      for (int b = 0; b < NBUF; ++b) {
-        const int st = g0 + b;
-        const int r = row0 + st * GPW;
-        if (r < I) compute_gateup<BG, BU, LPR, TM>(buf[b], uok, xu, su4, xts, sts, mc, u, sl.base + m0, r, a);
-        const int rn = row0 + (st + NBUF) * GPW;
-        if (st + NBUF < RW && uok && rn < I) load_gateup(buf[b], tg, tu, rn, U, u, H);
-      }
-    }
-  }
-}
-
-// grid = (row tiles of I, S + max_active), NW waves per workgroup (one
-// staging of the tokens' activations shared by NW waves)
-template <int LPR, int TM, int RW, int NBUF, int NW>
-__global__ __launch_bounds__(NW * 64, TM == 1 ? kGateUpMinBlocks : 2) void gateup_kernel(DecodeArgs a) {
-  extern __shared__ uint32_t smem[];
-  const Slot sl = slot_info(a, blockIdx.y);
-  if (sl.M < 0 || sl.M > a.gemm_above) return;  // (large buckets: the grouped GEMMs)
-  if (sl.M == 1) return;  // one-token buckets go to gateup1_kernel
-  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
-  if (!tg.codes || !tu.codes) return;
-  switch (tg.bits * 8 + tu.bits) {
-    case 2 * 8 + 2: gateup_body<2, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 3: gateup_body<2, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 2 * 8 + 4: gateup_body<2, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 2: gateup_body<3, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 3: gateup_body<3, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 3 * 8 + 4: gateup_body<3, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 2: gateup_body<4, 2, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 3: gateup_body<4, 3, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    case 4 * 8 + 4: gateup_body<4, 4, LPR, TM, RW, NBUF, NW>(a, sl, tg, tu, smem); break;
-    default: break;
-  }
-}
 
 // ---------------------------------------------------------------------------
 // down x routing weight for one (slot, row tile), down width BD; the same
@@ -936,6 +781,141 @@ __global__ __launch_bounds__(256, MOEQ_GU1_MINBLOCKS) void gateup1_route_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Buckets of 2 or more tokens, in the one-token kernel's layout (16 lanes per
+// row pair, lane j of a half walking the units j, j + 8, ... of its row, code
+// pairs as binary16 subnormals), TM tokens staged per pass: each unit's code
+// pairs are unpacked once and multiplied with every staged token.  Measured
+// at 16 tokens: 2 tokens per pass (four workgroups per compute unit) 427 us
+// per step, 3 per pass 427, 4 per pass (two workgroups per CU) 451, against
+// 446 for a kernel that gave a whole wave to each row and staged 4 tokens
+// in bfloat16.
+
+// token t's x into LDS at xl / xs (binary16 with per-block prescales)
+__device__ __forceinline__ void stage_x_token(const DecodeArgs& a, int t, uint32_t* xl, float2* xs) {
+  const int H = a.H;
+  const MOEQ_GLOBAL u32x4* src = gptr(reinterpret_cast<const u32x4*>(a.x + (size_t)t * H));
+  for (int q = threadIdx.x; q < H / 8; q += 256) {
+    float f[8];
+    bf16x8_to_f32(src[q], f);
+    const int uu = q >> 4, cq = q & 15;
+    stage_piece(f, xl + uu * kXStride + cq * 4, xs + uu * 4 + (cq >> 2), (cq & 3) == 0);
+  }
+}
+
+// the half's partial dots over its units for the mc <= TM staged tokens
+template <int B, int TM>
+__device__ __forceinline__ void row_half_dot_tm(const TensorDev& t, int row, int U, int j, int H, const uint32_t* xl,
+                                                const float2* xs, int xts, int sts, int mc,
+                                                const UnitBuf<B>& first, float (&acc)[TM]) {
+  constexpr int NB = MOEQ_GU1_DEPTH;
+  const int UPL = (U + 7) / 8;
+  UnitBuf<B> buf[NB];
+  buf[0] = first;
+#pragma unroll
+  for (int i = 1; i < NB - 1; ++i) load_unit_buf<B>(buf[i], t, row, U, min(j + 8 * min(i, UPL - 1), U - 1), H);
+#pragma unroll
+  for (int m = 0; m < TM; ++m) acc[m] = 0.0f;
+#pragma unroll 1
+  for (int i0 = 0; i0 < UPL; i0 += NB) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int i = i0 + b;
+      if (i < UPL) {
+        load_unit_buf<B>(buf[(b + NB - 1) % NB], t, row, U, min(j + 8 * min(i + NB - 1, UPL - 1), U - 1), H);
+        const int u = j + 8 * i;
+        if (u < U) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint32_t p[16];
+            block_pairs_sub<B>(buf[b].w + q * B, p);
+            const float ds = block_scale_sub(buf[b].s, q);
+#pragma unroll
+            for (int m = 0; m < TM; ++m)
+              if (m < mc)
+                acc[m] = block_dot_sub<B>(p, xl + m * xts + u * kXStride + 16 * q, ds, xs[m * sts + u * 4 + q],
+                                          acc[m]);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int BG, int BU, int TM>
+__device__ __forceinline__ void gateupn_body(const DecodeArgs& a, const Slot sl, const TensorDev& tg,
+                                             const TensorDev& tu, uint32_t* smem) {
+  const int H = a.H, I = a.I, U = H / kUnit;
+  const int xts = U * kXStride, sts = U * 4;  // per-token LDS strides (dwords, float2)
+  uint32_t* xl = smem;
+  float2* xs = reinterpret_cast<float2*>(smem + TM * xts);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 16 + wave * 4 + (lane >> 4);
+  const bool up = (lane & 8) != 0;
+  const int j = lane & 7;
+  const int rowc = min(row, I - 1);
+  for (int m0 = 0; m0 < sl.M; m0 += TM) {
+    const int mc = min(TM, sl.M - m0);
+    // the first unit is requested before x is staged
+    UnitBuf<BG> fg;
+    UnitBuf<BU> fu;
+    if constexpr (BG == BU) {
+      load_unit_buf<BG>(fg, up ? tu : tg, rowc, U, min(j, U - 1), H);
+    } else {
+      if (up)
+        load_unit_buf<BU>(fu, tu, rowc, U, min(j, U - 1), H);
+      else
+        load_unit_buf<BG>(fg, tg, rowc, U, min(j, U - 1), H);
+    }
+    if (m0 > 0) __syncthreads();  // the previous pass has read its x
+    for (int m = 0; m < mc; ++m) {
+      const int t = sl.shared >= 0 ? m0 + m : a.perm[sl.base + m0 + m] / a.k;
+      stage_x_token(a, t, xl + m * xts, xs + m * sts);
+    }
+    __syncthreads();
+    float acc[TM];
+    if constexpr (BG == BU) {
+      row_half_dot_tm<BG, TM>(up ? tu : tg, rowc, U, j, H, xl, xs, xts, sts, mc, fg, acc);
+    } else {
+      if (up)
+        row_half_dot_tm<BU, TM>(tu, rowc, U, j, H, xl, xs, xts, sts, mc, fu, acc);
+      else
+        row_half_dot_tm<BG, TM>(tg, rowc, U, j, H, xl, xs, xts, sts, mc, fg, acc);
+    }
+#pragma unroll
+    for (int m = 0; m < TM; ++m) {
+      if (m < mc) {
+        const float v = half_sum8(acc[m]);
+        const float other = dpp_f<0x128>(v);  // row_ror:8: the gate half's total
+        if ((lane & 15) == 15 && row < I) a.h[(size_t)(sl.base + m0 + m) * I + row] = silu(other) * v;
+      }
+    }
+  }
+}
+
+// grid = (I / 16, S + max_active), 256 threads; buckets of 2 .. gemm_above tokens
+template <int TM>
+__global__ __launch_bounds__(256, TM <= 2 ? 4 : 2) void gateupn_kernel(DecodeArgs a) {
+  extern __shared__ uint32_t smem[];
+  const Slot sl = slot_info(a, blockIdx.y);
+  if (sl.M < 2 || sl.M > a.gemm_above) return;
+  const TensorDev tg = a.desc[sl.desc * 3 + 0], tu = a.desc[sl.desc * 3 + 1];
+  if (!tg.codes || !tu.codes) return;
+  switch (tg.bits * 8 + tu.bits) {
+    case 2 * 8 + 2: gateupn_body<2, 2, TM>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 3: gateupn_body<2, 3, TM>(a, sl, tg, tu, smem); break;
+    case 2 * 8 + 4: gateupn_body<2, 4, TM>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 2: gateupn_body<3, 2, TM>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 3: gateupn_body<3, 3, TM>(a, sl, tg, tu, smem); break;
+    case 3 * 8 + 4: gateupn_body<3, 4, TM>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 2: gateupn_body<4, 2, TM>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 3: gateupn_body<4, 3, TM>(a, sl, tg, tu, smem); break;
+    case 4 * 8 + 4: gateupn_body<4, 4, TM>(a, sl, tg, tu, smem); break;
+    default: break;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Wide tensors (5, 6 and 8 bits).  The kernels above skip a slot whose gate or
 // up (down) tensor is wide; these take exactly those slots.  LPR lanes per
 // row (8, 16 or 32): lane j walks the units j, j + LPR, ... of its row with the
@@ -1213,30 +1193,8 @@ hipError_t launch_wide_down(const DecodeArgs& a, hipStream_t s) {
   return few ? launch_wide_down_tm<4, 16>(a, s) : launch_wide_down_tm<4, 8>(a, s);
 }
 
-// Rows per wave step are 64 / LPR; a workgroup covers 4 * (64 / LPR) * steps
-// rows of one slot.
-
-template <int LPR, int TM, int NW>
-hipError_t launch_gateup_lpr_tm_nw(const DecodeArgs& a, hipStream_t s) {
-  const int slots = a.S + a.max_active;
-  const int U = a.H / kUnit;
-  const size_t lds = (size_t)TM * (U * kXStride + U * 4) * 4;
-  const int rows_wg = NW * (64 / LPR) * kGateUpSteps;
-  dim3 grid((a.I + rows_wg - 1) / rows_wg, slots);
-  return launch_lds(gateup_kernel<LPR, TM, kGateUpSteps, NW == 8 ? 1 : kGateUpBuf, NW>, grid, lds, s, a, NW * 64);
-}
-
-// From MOEQ_GATEUP_WIDE_FROM tokens on, workgroups of 8 waves (one register
-// buffer each) share one staging of the 4 tokens' activations: measured
-// faster from 32 tokens (-2 % at 32, -4 % at 48 and 64), slower below.
-#ifndef MOEQ_GATEUP_WIDE_FROM
-#define MOEQ_GATEUP_WIDE_FROM 32
-#endif
-template <int LPR, int TM>
-hipError_t launch_gateup_lpr_tm(const DecodeArgs& a, hipStream_t s) {
-  return a.n >= MOEQ_GATEUP_WIDE_FROM ? launch_gateup_lpr_tm_nw<LPR, TM, 8>(a, s)
-                                      : launch_gateup_lpr_tm_nw<LPR, TM, 4>(a, s);
-}
+// Rows per wave step of the down GEMV are 64 / LPR; a workgroup covers
+// 4 * (64 / LPR) * steps rows of one slot.
 
 template <int LPR, int TM>
 hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
@@ -1247,14 +1205,6 @@ hipError_t launch_down_lpr_tm(const DecodeArgs& a, hipStream_t s) {
   const int rows_wg = 4 * (64 / LPR) * RW;
   dim3 grid((a.H + rows_wg - 1) / rows_wg, slots);
   return launch_lds(down_kernel<LPR, TM, RW, NB>, grid, lds, s, a);
-}
-
-template <int TM>
-hipError_t launch_gateup_tm(const DecodeArgs& a, hipStream_t s) {
-  const int U = a.H / kUnit;
-  if (U > 32) return launch_gateup_lpr_tm<64, TM>(a, s);
-  if (U > 16) return launch_gateup_lpr_tm<32, TM>(a, s);
-  return launch_gateup_lpr_tm<16, TM>(a, s);
 }
 
 template <int TM>
@@ -1280,7 +1230,17 @@ hipError_t launch_gateup_decode_single(const DecodeArgs& a, hipStream_t s) {
   return e == hipSuccess ? launch_wide_gateup(a, s) : e;
 }
 
-hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2) { return launch_gateup_tm<4>(a, s2); }
+// tokens staged per pass of the 2-64-token gate/up kernel
+#ifndef MOEQ_GATEUPN_TOKENS
+#define MOEQ_GATEUPN_TOKENS 2
+#endif
+hipError_t launch_gateup_decode_multi(const DecodeArgs& a, hipStream_t s2) {
+  constexpr int TM = MOEQ_GATEUPN_TOKENS;
+  const int U = a.H / kUnit;
+  const size_t lds = (size_t)TM * (U * kXStride + U * 8) * 4;
+  dim3 grid((a.I + 15) / 16, a.S + a.max_active);
+  return launch_lds(gateupn_kernel<TM>, grid, lds, s2, a);
+}
 
 bool gateup1_routes(const RouterParams& rp) { return !rp.kept_ids && !rp.x && rp.E_row <= 256 && rp.k <= kMaxTopK; }
 

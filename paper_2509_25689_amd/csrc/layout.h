@@ -176,8 +176,8 @@ __device__ __forceinline__ void block_pairs<6>(const uint32_t* w, const PairCons
   p[15] = and_or(shl<-9>(w[5]), k.m2, and_or(shl<-11>(w[3]), lo4, k.base));
 }
 
-// Code pairs as binary16 subnormals (widths 2-4, the 2-64-token and
-// one-token GEMVs): a dword masked so that only one code pair remains, at bit
+// Code pairs as binary16 subnormals (widths 2-4, the gate/up and down
+// GEMVs): a dword masked so that only one code pair remains, at bit
 // offset k of each half, with the exponent fields zero, is two binary16 values
 // c * 2^(k - 24), exact, for v_dot2_f32_f16 (which keeps subnormal inputs).
 // The layout puts several pairs at offsets inside the 10-bit mantissa, so most

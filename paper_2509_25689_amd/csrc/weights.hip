@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void repack_kernel(const uint8_t* canon, int r
 }
 
 // one thread per (row, unit): the bfloat16-form unpacking of block_pairs
-// (the 2-64-token gate/up and the 5/6/8-bit matrix-vector kernels), then
+// (the 5/6/8-bit matrix-vector kernels), then
 // d * (c - 2^(b-1)) exactly
 template <int B>
 __global__ __launch_bounds__(256) void dequant_kernel(TensorDev t, float* out) {

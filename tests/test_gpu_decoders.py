@@ -2,9 +2,9 @@
 the format's definition (Section 3.3's per-tensor widths in this library's
 block format: weight = d * (c - 2^(b-1))).
 
-* the bfloat16-form unpacking (matrix-vector kernels for buckets of 2-64
-  tokens and for 5/6/8-bit tensors): float32 d * (c - z), exact;
-* the binary16-subnormal code pairs (one-token gate/up and 2-4-bit down
+* the bfloat16-form unpacking (matrix-vector kernels for 5/6/8-bit
+  tensors): float32 d * (c - z), exact;
+* the binary16-subnormal code pairs (the 2-4-bit gate/up and down
   matrix-vector kernels): each code rebuilt from its pair value, float32
   d * (c - z), exact;
 * the grouped GEMMs' weight decoder: binary16(d * (c - z)), one rounding to

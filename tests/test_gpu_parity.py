@@ -246,8 +246,8 @@ def test_forward_v3_decode_batch16(gpu_lib, v3_decode):
 def test_forward_v3_auto_gemv(gpu_lib, v3_prefill, n, kind):
     """31-64 tokens on the automatic path (the decode path by default):
     buckets of one token through the one-token gate/up kernel, those of 2-4
-    through the 4-token kernels, and from 32 tokens the larger ones through
-    the grouped GEMMs (below 32 through the 4-token kernels too); mixed
+    through the 2-64-token GEMVs, and from 32 tokens the larger ones through
+    the grouped GEMMs (below 32 through the 2-64-token GEMVs too); mixed
     2/3/4-bit widths."""
     data, L = v3_prefill
     E = data.shape.n_experts
