@@ -87,8 +87,8 @@ typedef struct moeq_layer moeq_layer; /* opaque; owns every device buffer it all
  *   decode_max_tokens  forward takes the decode path (dequant-GEMV) for
  *                   n_tokens <= this and the prefill path (grouped GEMM on
  *                   MFMA) above it; 0 selects the library default (64).
- *                   From 32 tokens on, the decode path sends the buckets of
- *                   more than 4 tokens to the grouped GEMMs as well
+ *                   From 24 tokens on, the decode path sends the buckets of
+ *                   more than 2 tokens to the grouped GEMMs as well
  *   regroup         0: routing groups are the original id ranges with pruned
  *                   experts masked; 1: the kept experts, in ascending id order,
  *                   are cut into n_group equal contiguous groups (Section 3.2's

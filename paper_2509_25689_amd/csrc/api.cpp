@@ -19,10 +19,10 @@
 // decode forwards of at least MOEQ_HYBRID_FROM tokens send the buckets of
 // more than MOEQ_HYBRID_ABOVE rows to the grouped GEMMs
 #ifndef MOEQ_HYBRID_FROM
-#define MOEQ_HYBRID_FROM 32
+#define MOEQ_HYBRID_FROM 24
 #endif
 #ifndef MOEQ_HYBRID_ABOVE
-#define MOEQ_HYBRID_ABOVE 4
+#define MOEQ_HYBRID_ABOVE 2
 #endif
 
 using namespace moeq;

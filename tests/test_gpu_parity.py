@@ -203,12 +203,12 @@ def test_prefill_tile_edges(request, gpu_lib, which, n):
     _forward_check(gpu_lib, data, L, n, "tile-edges", gpu_lib.MOEQ_PATH_PREFILL, logits=logits)
 
 
-@pytest.mark.parametrize("n", [31, 32, 33])
+@pytest.mark.parametrize("n", [23, 24, 25])
 @pytest.mark.parametrize("which", ["tiny", "tiny_mixed"])
 def test_decode_hybrid_cutover(request, gpu_lib, which, n):
-    """The decode path around its hybrid cutover: from 32 tokens, buckets of
-    more than 4 rows take the grouped GEMMs and the smaller ones the
-    dequant-GEMV kernels, both summed by one combine (below 32 tokens every
+    """The decode path around its hybrid cutover: from 24 tokens, buckets of
+    more than 2 rows take the grouped GEMMs and the smaller ones the
+    dequant-GEMV kernels, both summed by one combine (below 24 tokens every
     bucket takes the GEMVs).  The inputs give buckets on both sides of that
     size, which the oracle's routing confirms here; every token compared."""
     data, L = request.getfixturevalue(which)
@@ -217,7 +217,7 @@ def test_decode_hybrid_cutover(request, gpu_lib, which, n):
     idx, _ = _route_oracle(shape, data.mask, logits)
     sizes = np.bincount(idx.ravel())
     sizes = sizes[sizes > 0]
-    assert (sizes <= 4).any() and (sizes > 4).any(), sizes
+    assert (sizes <= 2).any() and (sizes > 2).any(), sizes
     _forward_check(gpu_lib, data, L, n, "hybrid-cutover", gpu_lib.MOEQ_PATH_DECODE, logits=logits)
 
 
@@ -242,12 +242,12 @@ def test_forward_v3_decode_batch16(gpu_lib, v3_decode):
     _forward_check(gpu_lib, data, L, 16, "fwd-v3-b16", gpu_lib.MOEQ_PATH_AUTO)
 
 
-@pytest.mark.parametrize("n,kind", [(31, "zipf"), (32, "zipf"), (48, "normal"), (64, "zipf")])
+@pytest.mark.parametrize("n,kind", [(23, "zipf"), (24, "zipf"), (48, "normal"), (64, "zipf")])
 def test_forward_v3_auto_gemv(gpu_lib, v3_prefill, n, kind):
-    """31-64 tokens on the automatic path (the decode path by default):
-    buckets of one token through the one-token gate/up kernel, those of 2-4
-    through the 2-64-token GEMVs, and from 32 tokens the larger ones through
-    the grouped GEMMs (below 32 through the 2-64-token GEMVs too); mixed
+    """23-64 tokens on the automatic path (the decode path by default):
+    buckets of one token through the one-token gate/up kernel, those of 2
+    through the 2-64-token GEMVs, and from 24 tokens the larger ones through
+    the grouped GEMMs (below 24 through the 2-64-token GEMVs too); mixed
     2/3/4-bit widths."""
     data, L = v3_prefill
     E = data.shape.n_experts
