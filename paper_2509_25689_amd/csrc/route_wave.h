@@ -106,12 +106,21 @@ __device__ LaneChoice<EPL> route_token_wave(const RouterParams& rp, int t, float
     // more than 2^28 below the largest, then rounded to nearest even)
     const MOEQ_GLOBAL u32x4* xr = gptr(reinterpret_cast<const u32x4*>(rp.x + (size_t)t * rp.H));
     const int C = rp.H / 8;
+    // XB pieces per lane requested together in each pass (indices past the
+    // row read its last piece again: loads that do not depend on a
+    // condition go out before the first is used)
+    constexpr int XB = EPL >= 8 ? 4 : 8;
     uint32_t mx = 0;
-    for (int c = lane; c < C; c += 64) {
-      const u32x4 v = xr[c];
-      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
+    for (int c0 = lane; c0 < C; c0 += 64 * XB) {
+      u32x4 v[XB];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) mx = max(mx, max(q[j] & 0x7FFFu, (q[j] >> 16) & 0x7FFFu));
+      for (int b = 0; b < XB; ++b) v[b] = xr[min(c0 + 64 * b, C - 1)];
+#pragma unroll
+      for (int b = 0; b < XB; ++b) {
+        const uint32_t q[4] = {v[b].x, v[b].y, v[b].z, v[b].w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mx = max(mx, max(q[j] & 0x7FFFu, (q[j] >> 16) & 0x7FFFu));
+      }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off, 64));
@@ -119,17 +128,22 @@ __device__ LaneChoice<EPL> route_token_wave(const RouterParams& rp, int t, float
     if (lane == 0) rp.xexp[t] = e;
     const float sc = __builtin_amdgcn_ldexpf(1.0f, -e);
     MOEQ_GLOBAL u32x4* hr = (MOEQ_GLOBAL u32x4*)(rp.x16 + (size_t)t * rp.H);
-    for (int c = lane; c < C; c += 64) {
-      const u32x4 v = xr[c];
-      const uint32_t q[4] = {v.x, v.y, v.z, v.w};
-      uint32_t o[4];
+    for (int c0 = lane; c0 < C; c0 += 64 * XB) {
+      u32x4 v[XB];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float lo = __uint_as_float(q[j] << 16) * sc, hi = __uint_as_float(q[j] & 0xFFFF0000u) * sc;
-        o[j] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
-               ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+      for (int b = 0; b < XB; ++b) v[b] = xr[min(c0 + 64 * b, C - 1)];
+#pragma unroll
+      for (int b = 0; b < XB; ++b) {
+        const uint32_t q[4] = {v[b].x, v[b].y, v[b].z, v[b].w};
+        uint32_t o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float lo = __uint_as_float(q[j] << 16) * sc, hi = __uint_as_float(q[j] & 0xFFFF0000u) * sc;
+          o[j] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+                 ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+        }
+        if (c0 + 64 * b < C) hr[c0 + 64 * b] = u32x4{o[0], o[1], o[2], o[3]};
       }
-      hr[c] = u32x4{o[0], o[1], o[2], o[3]};
     }
   }
   const int E = rp.E, G = rp.G, per = rp.E / rp.G;
