@@ -842,19 +842,6 @@ __device__ __forceinline__ uint32_t rd_dword(const RdUnit<B>& u, int i) {
   return u.c[i >> 2][i & 3];
 }
 
-// Loads unit `unit` of the row (chunk base rc, scale pairs rs); a unit past
-// the row (a partial last stage) is loaded clamped and given scale 0, so its
-// weights decode to exact zeros.
-template <int B>
-__device__ __forceinline__ void rd_load(RdUnit<B>& u, const MOEQ_GLOBAL u32x4* rc, const MOEQ_GLOBAL u32x2* rs,
-                                        int Uk, int unit) {
-  const int uc = min(unit, Uk - 1);
-#pragma unroll
-  for (int j = 0; j < B; ++j) u.c[j] = __builtin_nontemporal_load(rc + (size_t)j * Uk + uc);
-  const u32x2 s = rs[uc];
-  u.s = unit < Uk ? s : u32x2{0u, 0u};
-}
-
 // Register decode of the code pairs (weights 2i and 2i + 1 sit in the low
 // and high halves of a dword).  The pair is shifted and masked to bit
 // P = 10 - b of each half with the exponent field zero: two binary16
